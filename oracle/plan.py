@@ -1,0 +1,434 @@
+"""Planner oracle (test infrastructure only): cost model + greedy asymmetric mapping.
+
+The paper (Sec. III) chooses one data-flow strategy per table with a linear
+cost model (Eq. (2)), then maps tables, or row chunks of them, onto the K
+cores of the SoC with a greedy algorithm (Sec. III-B, "Sharding and Load
+Balancing", steps 1-4) and falls back to symmetric (batch-split) partitioning
+when the load imbalance factor LIF = t_max / t_avg crosses a threshold.
+
+This module restates that algorithm for the GPU strategies (LDS-resident
+table/chunk, hot-row LDS cache, tile sort/dedup, direct HBM gather) in a form
+with every tie-break pinned, so that the C++ planner can be checked against it
+byte for byte.  It uses binary64 ``+ - * /`` and ``floor`` only; every cost is
+floored to integer picoseconds right after it is computed, and every decision
+compares integers.
+
+Steps (names follow the paper's notation: m_t rows, s_t sequence length /
+pooling factor, B batch, K cores = GPU workers, L persistent-buffer size = LDS
+budget for rows):
+
+  P1  strategy choice per table at split k: minimum cost among the feasible
+      strategies in the fixed order LDS, HOT, DEDUP, GATHER (ties -> earlier).
+  P2  (paper step 1) a table larger than L is split into the fewest chunks of
+      at most floor(min(chunk_max, L) / R) rows, but only if its best unsplit
+      cost exceeds the sum of the chunk costs (the speed-up exceeds the number
+      of chunks); chunks use the LDS strategy.
+  P3  tau = ceil(sum of item costs / K), the ideal per-worker load.
+  P4  an item costing more than tau is batch-split k ways (symmetric
+      partitioning of Sec. III-A applied to that item, the paper's optional
+      replication): the smallest k in [2, min(K, B)] whose best cost is at most
+      max(tau, 2 x its fixed cost); all chunks of one table share one k.
+  P5  (paper step 2) slices sorted by (cost desc, s desc, m asc, t, chunk, j)
+      -- longest-processing-time first with the paper's keys as tie-breaks --
+      or, with order_mode 1, by the paper's literal key (s desc, m asc, t,
+      chunk, j).
+  P6  (paper step 2) each slice goes to the least-loaded worker (ties -> lowest
+      index).  (Paper step 3, "L1 if available", is per item here: LDS does not
+      persist across launches, so every item re-stages its own rows.)
+  P7  (paper step 4) if LIF (in thousandths) exceeds the threshold, the last r
+      tables of the paper's order (s desc, m asc, t) become symmetric -- split
+      min(K, B) ways with slice j on worker j, placed first -- for r = 1, 2, ...
+      until LIF is within the threshold; if no r gets there, the r (0
+      included) with the smallest maximum load.
+  P8  canonical text: one line per slice in worker order then placement order.
+"""
+from __future__ import annotations
+
+import heapq
+import math
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence, Tuple
+
+# strategies (same numbering as the C header)
+LDS, HOT, DEDUP, GATHER = 0, 1, 2, 3
+AUTO = -1
+STRAT_ORDER = (LDS, HOT, DEDUP, GATHER)
+
+# beta layout (picoseconds; per item, per lookup, per staged byte)
+G0, G1, L0, L1, S, I, H0, P, D0, D1 = range(10)
+NBETA = 10
+
+MAX_HOT = 4096
+MAX_CHUNKS = 65536
+
+
+class PlanError(ValueError):
+    pass
+
+
+def default_beta(R: int) -> List[float]:
+    """Placeholder coefficients from rooflines until a fit replaces them (Eq. (2) is fitted by OLS).
+
+    G1: a row of R bytes at one worker's share of HBM (8 TB/s / 256 = 32 ps per
+        byte) derated by 0.7;  L1: a row from LDS at 128 B/clk x 2.4 GHz;
+    S: one staged byte at the HBM share;  I: one index scanned by a chunk;
+    P: one hot-set probe;  D1: sorting one index in a tile;  *0: 0.2 us per item.
+    """
+    b = [0.0] * NBETA
+    b[G0] = 200000.0
+    b[G1] = (float(R) * 32.0) / 0.7
+    b[L0] = 200000.0
+    b[L1] = float(R) / 0.3072
+    b[S] = 32.0
+    b[I] = 256.0
+    b[H0] = 200000.0
+    b[P] = 100.0
+    b[D0] = 200000.0
+    b[D1] = 4000.0
+    return b
+
+
+@dataclass
+class Stat:
+    mean_pooling: float
+    max_pooling: int = 0
+    hot_freq: Sequence[float] = ()
+    unique_frac: float = -1.0
+
+    @property
+    def n_hot(self) -> int:
+        return len(self.hot_freq)
+
+
+@dataclass
+class Options:
+    lds_budget: int = 131072
+    lif_milli: int = 1250
+    chunk_max_bytes: int = 0          # <= 0 -> lds_budget
+    order_mode: int = 0
+    beta: Optional[Sequence[float]] = None
+    force: Optional[Sequence[int]] = None
+
+
+@dataclass
+class Slice:
+    wg: int
+    t: int
+    strat: int
+    chunk: int
+    nchunks: int
+    r0: int
+    r1: int
+    k: int
+    j: int
+    C: int
+    cost: int
+    seq: int = 0          # placement sequence number
+
+
+@dataclass
+class Plan:
+    T: int
+    E: int
+    dtype: str
+    R: int
+    K: int
+    L: int
+    B: int
+    theta: int
+    order_mode: int
+    slices: List[Slice] = field(default_factory=list)
+    max_ps: int = 0
+    sum_ps: int = 0
+    lif_milli: int = 0
+    r_sym: int = 0
+
+    def text(self) -> str:
+        lines = ["embx-plan v1",
+                 f"T {self.T} E {self.E} dtype {self.dtype} R {self.R} K {self.K} L {self.L} B {self.B} "
+                 f"theta {self.theta} order {self.order_mode}"]
+        for s in sorted(self.slices, key=lambda x: (x.wg, x.seq)):
+            lines.append(f"item {s.wg} {s.t} {s.strat} {s.chunk} {s.nchunks} {s.r0} {s.r1} {s.k} {s.j} {s.C} {s.cost}")
+        lines.append(f"end max {self.max_ps} sum {self.sum_ps} lif {self.lif_milli} sym {self.r_sym}")
+        return "\n".join(lines) + "\n"
+
+
+def _fl(x: float) -> int:
+    """floor to integer picoseconds, never negative."""
+    if not math.isfinite(x):
+        raise PlanError("non-finite cost")
+    v = math.floor(x)
+    return v if v > 0 else 0
+
+
+# --- Eq. (2), one worker's cost for one slice; lam = expected lookups of the slice -------------
+
+def cost_gather(b, lam):
+    return _fl(b[G0] + b[G1] * lam), _fl(b[G0])
+
+
+def cost_lds(b, mu, R, lam):
+    return _fl(b[L0] + b[S] * float(mu * R) + b[L1] * lam), _fl(b[L0] + b[S] * float(mu * R))
+
+
+def cost_chunk(b, mu, R, lam, c):
+    return (_fl(b[L0] + b[S] * float(mu * R) + b[I] * lam + b[L1] * (lam / float(c))),
+            _fl(b[L0] + b[S] * float(mu * R)))
+
+
+def cost_hot(b, C, R, h, lam):
+    return (_fl(b[H0] + b[S] * float(C * R) + lam * (b[P] + h * b[L1] + (1.0 - h) * b[G1])),
+            _fl(b[H0] + b[S] * float(C * R)))
+
+
+def cost_dedup(b, u, lam):
+    return _fl(b[D0] + b[D1] * lam + (b[G1] * u) * lam), _fl(b[D0])
+
+
+class _Table:
+    def __init__(self, t, m, st: Stat, R, L, B, force):
+        self.t, self.m, self.R = t, m, R
+        self.s = float(st.mean_pooling)
+        self.Lam = float(B) * self.s
+        cap = L // R
+        self.C = min(st.n_hot, cap)
+        h = 0.0
+        for k in range(self.C):
+            h = h + float(st.hot_freq[k])
+        self.h = h
+        u = float(st.unique_frac)
+        self.u = u if (u > 0.0 and u <= 1.0) else 1.0
+        self.fits = m * R <= L
+        self.force = force
+
+    def allowed(self):
+        out = []
+        for s in STRAT_ORDER:
+            if self.force != AUTO and s != self.force:
+                continue
+            if s == LDS and not self.fits:
+                continue
+            if s == HOT and self.C < 1:
+                continue
+            out.append(s)
+        return out
+
+    def cost(self, b, strat, k):
+        lam = self.Lam / float(k)
+        if strat == LDS:
+            return cost_lds(b, self.m, self.R, lam)
+        if strat == HOT:
+            return cost_hot(b, self.C, self.R, self.h, lam)
+        if strat == DEDUP:
+            return cost_dedup(b, self.u, lam)
+        return cost_gather(b, lam)
+
+    def best(self, b, k):
+        """(strategy, cost, fixed cost) -- P1, ties to the earlier strategy."""
+        best = None
+        for s in self.allowed():
+            c, f = self.cost(b, s, k)
+            if best is None or c < best[1]:
+                best = (s, c, f)
+        return best
+
+
+@dataclass
+class _Item:
+    t: int
+    chunk: int
+    nchunks: int
+    r0: int
+    r1: int
+    strat: int = GATHER
+    k: int = 1
+    cost: int = 0          # cost of one slice at split k
+
+
+def _validate(rows, E, dtype, stats, B, K, opts: Options):
+    T = len(rows)
+    if T < 1 or len(stats) != T:
+        raise PlanError("need T >= 1 tables with stats")
+    if dtype not in ("f32", "f16"):
+        raise PlanError("dtype")
+    esz = 4 if dtype == "f32" else 2
+    if E < 1 or E > 256 or (E * esz) % 16 != 0:
+        raise PlanError("E must make 16-byte multiple rows, E <= 256")
+    if B < 1 or K < 1:
+        raise PlanError("B and K must be >= 1")
+    R = E * esz
+    L = int(opts.lds_budget)
+    if L < R:
+        raise PlanError("LDS budget below one row")
+    for m in rows:
+        if m < 1 or m >= (1 << 31):
+            raise PlanError("rows must be in [1, 2^31)")
+    for st in stats:
+        if not (math.isfinite(st.mean_pooling) and st.mean_pooling >= 0.0):
+            raise PlanError("mean_pooling")
+        if st.n_hot > MAX_HOT:
+            raise PlanError("n_hot")
+        for f in st.hot_freq:
+            if not (math.isfinite(f) and f >= 0.0):
+                raise PlanError("hot_freq")
+        if not math.isfinite(st.unique_frac):
+            raise PlanError("unique_frac")
+    if opts.order_mode not in (0, 1):
+        raise PlanError("order_mode")
+    beta = list(opts.beta) if opts.beta is not None else default_beta(R)
+    if len(beta) != NBETA or not all(math.isfinite(x) for x in beta):
+        raise PlanError("beta")
+    force = list(opts.force) if opts.force is not None else [AUTO] * T
+    if len(force) != T or any(f not in (AUTO, LDS, HOT, DEDUP, GATHER) for f in force):
+        raise PlanError("force_strategy")
+    return T, R, L, beta, force
+
+
+def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat], B: int, K: int,
+                   opts: Optional[Options] = None) -> Plan:
+    opts = opts or Options()
+    T, R, L, b, force = _validate(rows, E, dtype, stats, B, K, opts)
+    cm = opts.chunk_max_bytes if opts.chunk_max_bytes > 0 else L
+    crow = min(cm, L) // R
+    if crow < 1:
+        raise PlanError("chunk_max_bytes below one row")
+    tabs = [_Table(t, int(rows[t]), stats[t], R, L, B, force[t]) for t in range(T)]
+    for tb in tabs:
+        if tb.force == HOT and tb.C < 1:
+            raise PlanError("HOT forced on a table without hot rows")
+
+    # P1 + P2: strategy per table, chunking of tables larger than L
+    items: List[_Item] = []
+    groups: List[List[_Item]] = []
+    for tb in tabs:
+        chunked = False
+        c = 1
+        if not tb.fits and tb.force in (AUTO, LDS):
+            c = (tb.m + crow - 1) // crow
+            if tb.force == LDS:
+                if c > MAX_CHUNKS:
+                    raise PlanError("too many chunks")
+                chunked = True
+            elif 2 <= c <= K:
+                csum = 0
+                for i in range(c):
+                    r0, r1 = (i * tb.m) // c, ((i + 1) * tb.m) // c
+                    csum += cost_chunk(b, r1 - r0, R, tb.Lam, c)[0]
+                chunked = tb.best(b, 1)[1] > csum
+        g = []
+        if chunked:
+            for i in range(c):
+                r0, r1 = (i * tb.m) // c, ((i + 1) * tb.m) // c
+                it = _Item(tb.t, i, c, r0, r1, LDS, 1, cost_chunk(b, r1 - r0, R, tb.Lam, c)[0])
+                g.append(it)
+        else:
+            s, cst, _ = tb.best(b, 1)
+            g.append(_Item(tb.t, 0, 1, 0, tb.m, s, 1, cst))
+        groups.append(g)
+        items.extend(g)
+
+    # P3
+    total1 = sum(it.cost for it in items)
+    tau = (total1 + K - 1) // K
+    kmax = min(K, B)
+
+    # P4
+    def split_k(it: _Item):
+        """smallest k in [2, kmax] with cost_k <= max(tau, 2 fixed_k), else kmax."""
+        tb = tabs[it.t]
+        for k in range(2, kmax + 1):
+            s, cst, fx = _item_best(tb, it, k)
+            if cst <= max(tau, 2 * fx):
+                return k
+        return kmax
+
+    def _item_best(tb, it, k):
+        if it.nchunks > 1:
+            lam = tb.Lam / float(k)
+            c, f = cost_chunk(b, it.r1 - it.r0, R, lam, it.nchunks)
+            return LDS, c, f
+        return tb.best(b, k)
+
+    for g in groups:
+        ks = [1 if it.cost <= tau else split_k(it) for it in g]
+        k = max(ks)
+        for it in g:
+            s, cst, _ = _item_best(tabs[it.t], it, k)
+            it.strat, it.k, it.cost = s, k, cst
+
+    def slices_of(it: _Item) -> List[Slice]:
+        C = tabs[it.t].C if it.strat == HOT else 0
+        return [Slice(-1, it.t, it.strat, it.chunk, it.nchunks, it.r0, it.r1, it.k, j, C, it.cost)
+                for j in range(it.k)]
+
+    def key(sl: Slice):
+        tb = tabs[sl.t]
+        if opts.order_mode == 0:
+            return (-sl.cost, -tb.s, tb.m, sl.t, sl.chunk, sl.j)
+        return (-tb.s, tb.m, sl.t, sl.chunk, sl.j)
+
+    paper_order = sorted(range(T), key=lambda t: (-tabs[t].s, tabs[t].m, t))
+
+    def place(demoted: List[int]):
+        """P5 + P6 (+ symmetric tables of P7 first). Returns (slices, loads)."""
+        loads = [0] * K
+        seq = 0
+        out: List[Slice] = []
+        dem = set(demoted)
+        for t in [x for x in paper_order if x in dem]:
+            for it in groups[t]:
+                tb = tabs[t]
+                s, cst, _ = _item_best(tb, it, kmax)
+                sym = _Item(it.t, it.chunk, it.nchunks, it.r0, it.r1, s, kmax, cst)
+                for sl in slices_of(sym):
+                    sl.wg = sl.j
+                    sl.seq = seq
+                    seq += 1
+                    loads[sl.wg] += sl.cost
+                    out.append(sl)
+        rest = [sl for g in groups if g[0].t not in dem for it in g for sl in slices_of(it)]
+        rest.sort(key=key)
+        heap = [(loads[w], w) for w in range(K)]
+        heapq.heapify(heap)
+        for sl in rest:
+            ld, w = heapq.heappop(heap)
+            sl.wg = w
+            sl.seq = seq
+            seq += 1
+            loads[w] = ld + sl.cost
+            heapq.heappush(heap, (loads[w], w))
+            out.append(sl)
+        return out, loads
+
+    def lif_of(loads):
+        tot = sum(loads)
+        return (1000 * K * max(loads)) // tot if tot > 0 else 1000
+
+    best_r, best_slices, best_loads = 0, *place([])
+    lif = lif_of(best_loads)
+    if lif > opts.lif_milli:
+        found = False
+        cand = (max(best_loads), 0, best_slices, best_loads)
+        for r in range(1, T + 1):
+            sl_r, ld_r = place(paper_order[T - r:])
+            if lif_of(ld_r) <= opts.lif_milli:
+                best_r, best_slices, best_loads = r, sl_r, ld_r
+                found = True
+                break
+            if max(ld_r) < cand[0]:
+                cand = (max(ld_r), r, sl_r, ld_r)
+        if not found:
+            _, best_r, best_slices, best_loads = cand
+
+    plan = Plan(T, E, dtype, R, K, L, B, opts.lif_milli, opts.order_mode)
+    plan.slices = best_slices
+    plan.max_ps = max(best_loads)
+    plan.sum_ps = sum(best_loads)
+    plan.lif_milli = lif_of(best_loads)
+    plan.r_sym = best_r
+    return plan
+
+
+def stats_from_workload(ts) -> Stat:
+    """Adapter from ``workloads.TableStats`` (host lists only)."""
+    return Stat(float(ts.mean_pooling), int(ts.max_pooling), [float(x) for x in ts.hot_freq], float(ts.unique_frac))

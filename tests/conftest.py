@@ -1,0 +1,20 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    config.addinivalue_line("markers", "slow: long-running GPU case at full workload size")
+
+
+@pytest.fixture(scope="session")
+def gpu_lib():
+    """The HIP library (loads only; fails loudly if it is not built)."""
+    import paper_2507_01676_amd as embx
+    return embx

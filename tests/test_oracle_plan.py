@@ -1,0 +1,283 @@
+"""Pins of the planner oracle.
+
+The paper prints no worked plan, so the plan is pinned by properties that any
+correct reading must satisfy: the cost formulas agree with each other in the
+cases where two strategies coincide, every bag of every table (or row chunk)
+is covered exactly once, LDS capacity holds per item, the reported loads and
+LIF recompute from the slices, special cases have known answers, and the
+greedy placement obeys the classical list-scheduling bounds against a
+brute-force optimum (Graham 1969: LPT <= (4/3 - 1/(3K)) OPT, any list order
+<= (2 - 1/K) OPT).
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+from hypothesis import HealthCheck, given, settings
+from hypothesis import strategies as st
+
+from oracle import plan as OPL
+
+
+def _b(R=256):
+    return OPL.default_beta(R)
+
+
+# ---------------------------------------------------------------- cost model cross-checks
+
+def test_cost_formulas_coincide_where_strategies_do():
+    b = _b()
+    R, lam = 256, 12345.0
+    # gather is affine in lam: the slope is the per-lookup coefficient
+    g1, _ = OPL.cost_gather(b, lam)
+    g2, _ = OPL.cost_gather(b, 2 * lam)
+    assert abs((g2 - g1) - b[OPL.G1] * lam) <= 1
+    # a hot set that catches nothing with a free probe is a gather plus staging
+    bz = list(b)
+    bz[OPL.P] = 0.0
+    bz[OPL.H0] = bz[OPL.G0]
+    hot0, fx = OPL.cost_hot(bz, 100, R, 0.0, lam)
+    assert abs(hot0 - (g1 + b[OPL.S] * 100 * R)) <= 1 and fx == math.floor(bz[OPL.G0] + b[OPL.S] * 100 * R)
+    # a hot set that catches everything with a free probe is an LDS table of C rows
+    bl = list(bz)
+    bl[OPL.H0] = bl[OPL.L0]
+    hot1, _ = OPL.cost_hot(bl, 100, R, 1.0, lam)
+    lds, _ = OPL.cost_lds(bl, 100, R, lam)
+    assert abs(hot1 - lds) <= 1
+    # one chunk with a free index scan is the whole-table LDS cost
+    bi = list(b)
+    bi[OPL.I] = 0.0
+    assert OPL.cost_chunk(bi, 77, R, lam, 1) == OPL.cost_lds(bi, 77, R, lam)
+    # dedup with every lookup unique and free sorting is a gather
+    bd = list(b)
+    bd[OPL.D1] = 0.0
+    bd[OPL.D0] = bd[OPL.G0]
+    assert OPL.cost_dedup(bd, 1.0, lam) == OPL.cost_gather(bd, lam)
+    # all costs grow with lam and never go negative
+    for f in (lambda l: OPL.cost_gather(b, l), lambda l: OPL.cost_lds(b, 50, R, l),
+              lambda l: OPL.cost_hot(b, 50, R, 0.5, l), lambda l: OPL.cost_dedup(b, 0.3, l),
+              lambda l: OPL.cost_chunk(b, 50, R, l, 3)):
+        assert 0 <= f(0.0)[0] <= f(10.0)[0] <= f(1e6)[0]
+    neg = [-1e9] * OPL.NBETA
+    assert OPL.cost_gather(neg, 5.0) == (0, 0)
+
+
+# ---------------------------------------------------------------- invariants on random instances
+
+def _random_instance(seed, T=None, K=None):
+    g = np.random.default_rng(seed)
+    T = T or int(g.integers(1, 14))
+    K = K or int(g.integers(1, 24))
+    B = int(g.integers(1, 3000))
+    rows = [int(math.floor(math.exp(g.uniform(0, math.log(3e6))))) + 1 for _ in range(T)]
+    stats = []
+    for _ in range(T):
+        nh = int(g.integers(0, 40))
+        f = np.sort(g.random(nh))[::-1]
+        f = f / (f.sum() * g.uniform(1.0, 3.0)) if nh else f
+        stats.append(OPL.Stat(float(g.choice([0.0, 1.0, 3.5, 8.0, 50.0])), 20, [float(x) for x in f],
+                              float(g.choice([-1.0, 0.05, 0.5, 1.0]))))
+    E = int(g.choice([32, 64, 128]))
+    dtype = str(g.choice(["f32", "f16"]))
+    opts = OPL.Options(lds_budget=int(g.choice([16384, 65536, 131072])), lif_milli=int(g.choice([1000, 1250, 2000])),
+                       order_mode=int(g.integers(0, 2)))
+    return rows, E, dtype, stats, B, K, opts
+
+
+def check_plan_invariants(p: OPL.Plan, rows, stats, B):
+    R, L, K = p.R, p.L, p.K
+    by_item = {}
+    for s in p.slices:
+        assert 0 <= s.wg < K
+        by_item.setdefault((s.t, s.chunk), []).append(s)
+        if s.strat == OPL.LDS:
+            assert (s.r1 - s.r0) * R <= L
+        if s.strat == OPL.HOT:
+            assert 1 <= s.C and s.C * R <= L and s.C <= len(stats[s.t].hot_freq)
+        else:
+            assert s.C == 0
+        if s.nchunks > 1:
+            assert s.strat == OPL.LDS
+    for t in range(p.T):
+        chunks = sorted(c for (tt, c) in by_item if tt == t)
+        assert chunks == list(range(len(chunks))) and len(chunks) >= 1
+        bounds = []
+        ks = set()
+        for c in chunks:
+            sl = by_item[(t, c)]
+            k = sl[0].k
+            ks.add(k)
+            assert sorted(x.j for x in sl) == list(range(k))       # every slice once
+            assert all(x.k == k and x.nchunks == len(chunks) for x in sl)
+            assert len({(x.r0, x.r1) for x in sl}) == 1
+            bounds.append((sl[0].r0, sl[0].r1))
+            assert 1 <= k <= max(1, min(K, B))
+        assert len(ks) == 1                                        # one split per table
+        pos = 0
+        for r0, r1 in bounds:                                      # chunks tile [0, m)
+            assert r0 == pos and r1 > r0
+            pos = r1
+        assert pos == rows[t]
+        # the batch slices of a split cover every bag exactly once
+        k = ks.pop()
+        cover = np.zeros(B, np.int64)
+        for j in range(k):
+            cover[(j * B) // k: ((j + 1) * B) // k] += 1
+        assert np.all(cover == 1)
+    loads = [0] * K
+    for s in p.slices:
+        loads[s.wg] += s.cost
+    assert p.max_ps == max(loads) and p.sum_ps == sum(loads)
+    tot = sum(loads)
+    assert p.lif_milli == ((1000 * K * max(loads)) // tot if tot else 1000)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_plan_invariants_random(seed):
+    rows, E, dtype, stats, B, K, opts = _random_instance(seed)
+    p = OPL.plan_reference(rows, E, dtype, stats, B, K, opts)
+    check_plan_invariants(p, rows, stats, B)
+    assert p.text().startswith("embx-plan v1\n") and p.text().endswith(f"sym {p.r_sym}\n")
+
+
+@settings(max_examples=60, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(st.integers(0, 10 ** 6))
+def test_plan_invariants_hypothesis(seed):
+    rows, E, dtype, stats, B, K, opts = _random_instance(seed)
+    check_plan_invariants(OPL.plan_reference(rows, E, dtype, stats, B, K, opts), rows, stats, B)
+
+
+# ---------------------------------------------------------------- special cases
+
+def test_K_identical_tables_one_per_worker():
+    K = 8
+    rows = [5_000_000] * K
+    stats = [OPL.Stat(1.0)] * K
+    p = OPL.plan_reference(rows, 64, "f32", stats, 2048, K)
+    assert sorted(s.wg for s in p.slices) == list(range(K))
+    assert all(s.k == 1 and s.strat == OPL.GATHER for s in p.slices)
+    assert p.lif_milli == 1000
+
+
+def test_one_huge_table_is_split_over_all_workers():
+    K, B = 16, 1000
+    p = OPL.plan_reference([10_000_000], 64, "f32", [OPL.Stat(50.0)], B, K)
+    assert len(p.slices) == K and sorted(s.wg for s in p.slices) == list(range(K))
+    sizes = [((s.j + 1) * B) // K - (s.j * B) // K for s in p.slices]
+    assert max(sizes) - min(sizes) <= 1
+    assert p.lif_milli == 1000
+
+
+def test_tiny_tables_with_many_lookups_stay_in_lds():
+    rows = [10, 40, 100, 300]
+    stats = [OPL.Stat(20.0)] * 4
+    p = OPL.plan_reference(rows, 64, "f32", stats, 4096, 64)
+    assert all(s.strat == OPL.LDS for s in p.slices)
+
+
+def test_chunking_decision_follows_the_speedup_rule():
+    # LDS nearly free, HBM gather very expensive: a 4-chunk table is split (speed-up > 4)
+    b = [0.0] * OPL.NBETA
+    b[OPL.G1] = 1e6
+    b[OPL.L1] = 1.0
+    b[OPL.S] = 1e-3
+    b[OPL.I] = 1.0
+    b[OPL.D1] = 1e6
+    b[OPL.P] = 1e6
+    R, L = 256, 65536
+    m = 4 * (L // R)
+    p = OPL.plan_reference([m], 64, "f32", [OPL.Stat(10.0)], 100, 8, OPL.Options(lds_budget=L, beta=b))
+    assert {s.nchunks for s in p.slices} == {4} and all(s.strat == OPL.LDS for s in p.slices)
+    # scanning indices costs as much as gathering: the chunks cannot win
+    b2 = list(b)
+    b2[OPL.I] = 1e6
+    p2 = OPL.plan_reference([m], 64, "f32", [OPL.Stat(10.0)], 100, 8, OPL.Options(lds_budget=L, beta=b2))
+    assert {s.nchunks for s in p2.slices} == {1} and p2.slices[0].strat == OPL.GATHER
+    # forcing LDS on a table larger than L chunks it regardless of cost
+    p3 = OPL.plan_reference([m + 1], 64, "f32", [OPL.Stat(10.0)], 100, 2,
+                            OPL.Options(lds_budget=L, force=[OPL.LDS]))
+    assert {s.nchunks for s in p3.slices} == {5}
+
+
+def test_force_strategy_and_errors():
+    stats = [OPL.Stat(2.0, 4, [0.3, 0.2], 0.5), OPL.Stat(2.0)]
+    for f in (OPL.HOT, OPL.DEDUP, OPL.GATHER):
+        p = OPL.plan_reference([1000, 2000], 64, "f32", stats, 64, 4, OPL.Options(force=[f, OPL.GATHER]))
+        assert {s.strat for s in p.slices if s.t == 0} == {f}
+    with pytest.raises(OPL.PlanError):
+        OPL.plan_reference([1000, 2000], 64, "f32", stats, 64, 4, OPL.Options(force=[OPL.AUTO, OPL.HOT]))
+    with pytest.raises(OPL.PlanError):
+        OPL.plan_reference([1000], 6, "f32", [OPL.Stat(1.0)], 64, 4)            # 24-byte rows
+    with pytest.raises(OPL.PlanError):
+        OPL.plan_reference([0], 64, "f32", [OPL.Stat(1.0)], 64, 4)
+    with pytest.raises(OPL.PlanError):
+        OPL.plan_reference([10], 64, "f32", [OPL.Stat(float("nan"))], 64, 4)
+
+
+def test_order_mode_one_is_paper_order():
+    rows = [100000, 200000, 300000, 400000]
+    stats = [OPL.Stat(1.0), OPL.Stat(4.0), OPL.Stat(4.0), OPL.Stat(2.0)]
+    p = OPL.plan_reference(rows, 64, "f32", stats, 1, 4, OPL.Options(order_mode=1, lif_milli=10 ** 9))
+    first = [s.t for s in sorted(p.slices, key=lambda s: s.seq)]
+    assert first == [1, 2, 3, 0]                  # s desc, then m asc
+
+
+def test_lif_fallback_never_worsens_the_makespan():
+    # one table that cannot be split (B = 1) dominates: LIF stays high
+    rows = [5_000_000, 1000, 2000, 3000]
+    stats = [OPL.Stat(100.0), OPL.Stat(1.0), OPL.Stat(1.0), OPL.Stat(1.0)]
+    p0 = OPL.plan_reference(rows, 64, "f32", stats, 1, 8, OPL.Options(lif_milli=10 ** 9))
+    p1 = OPL.plan_reference(rows, 64, "f32", stats, 1, 8, OPL.Options(lif_milli=1000))
+    assert p1.max_ps <= p0.max_ps
+
+
+def test_lif_fallback_makes_trailing_tables_symmetric():
+    # two huge equal tables on three workers: LPT leaves one worker idle (LIF 1.5);
+    # making the last table of the paper order symmetric spreads it over all workers
+    rows = [1_000_000, 1_000_001]
+    stats = [OPL.Stat(1.0), OPL.Stat(1.0)]
+    b = OPL.default_beta(256)
+    b[OPL.G0] = 1e9            # a big fixed cost keeps P4 from splitting
+    p = OPL.plan_reference(rows, 64, "f32", stats, 3, 3, OPL.Options(beta=b, lif_milli=1200))
+    assert p.r_sym >= 1
+    sym = [s for s in p.slices if s.t == 1]
+    assert sorted(s.wg for s in sym) == [0, 1, 2] and all(s.k == 3 for s in sym)
+
+
+# ---------------------------------------------------------------- scheduling bounds vs brute force
+
+def _opt_makespan(costs, K):
+    best = float("inf")
+    for assign in itertools.product(range(K), repeat=len(costs)):
+        loads = [0] * K
+        for c, w in zip(costs, assign):
+            loads[w] += c
+        best = min(best, max(loads))
+    return best
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_greedy_within_list_scheduling_bounds(seed):
+    g = np.random.default_rng(1000 + seed)
+    T = int(g.integers(2, 8))
+    K = int(g.integers(2, 4))
+    rows = [int(g.integers(100000, 3_000_000)) for _ in range(T)]
+    stats = [OPL.Stat(float(g.integers(1, 30))) for _ in range(T)]
+    for mode in (0, 1):
+        p = OPL.plan_reference(rows, 64, "f32", stats, 1, K, OPL.Options(order_mode=mode, lif_milli=10 ** 9))
+        assert all(s.k == 1 for s in p.slices)        # B = 1: nothing can be split
+        opt = _opt_makespan([s.cost for s in p.slices], K)
+        bound = (4.0 / 3.0 - 1.0 / (3 * K)) if mode == 0 else (2.0 - 1.0 / K)
+        assert p.max_ps <= bound * opt + 1e-9, (mode, p.max_ps, opt)
+
+
+def test_lpt_bound_is_tight_on_the_classic_instance():
+    # Graham's tight example for K = 2: jobs 3,3,2,2,2 -> LPT 7, OPT 6
+    b = [0.0] * OPL.NBETA
+    b[OPL.G1] = 1.0
+    stats = [OPL.Stat(float(x)) for x in (3, 3, 2, 2, 2)]
+    rows = [10 ** 6 + i for i in range(5)]
+    p = OPL.plan_reference(rows, 64, "f32", stats, 1, 2, OPL.Options(beta=b, lif_milli=10 ** 9))
+    assert sorted(s.cost for s in p.slices) == [2, 2, 2, 3, 3]
+    assert p.max_ps == 7 and _opt_makespan([2, 2, 2, 3, 3], 2) == 6
