@@ -1,0 +1,279 @@
+#!/usr/bin/env python3
+"""Benchmark of the multi-table embedding-bag lookup on one MI355X.
+
+One step = one emb_lookup over one batch of the workload (all tables, all
+samples).  Inputs (tables, indices, offsets) are resident in HBM before timing;
+R distinct batches are cycled.  Prints ONE JSON line:
+
+  value            lookups/s over the K timed steps (whole job, one GPU)
+  queries_per_s    samples/s (the paper's TPS)
+  p99_us           nearest-rank P99 of the per-batch latency (HIP events around each launch)
+  useful_hbm_frac  (lookups x row bytes)/s over the 8 TB/s HBM peak
+  roofline         algorithmic bytes per launch (rows + indices + offsets + output) over the
+                   mean launch duration, against the 8 TB/s HBM peak
+  cpu_baseline     the CPU oracle timed on a bounded sample of the same workload
+
+  python bench.py [--config 2] [--steps 200] [--warmup 20]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "embedding lookups/s + queries/s, P99 batch latency, % HBM peak (1 MI355X)"
+DEFAULT_CONFIG = 2
+KERNEL_SOURCES = ["paper_2507_01676_amd/csrc/lookup.hip", "paper_2507_01676_amd/csrc/device_types.hpp"]
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def p99(xs):
+    s = sorted(xs)
+    return s[max(0, math.ceil(0.99 * len(s)) - 1)]
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(c: W.Config, batches, budget_s: float):
+    """The CPU oracle (plain NumPy, float64 accumulation) on a bounded sample of the workload."""
+    from oracle import pool as OP
+    t0 = time.time()
+    if c.cfg_id == 5:
+        # the full table set (~100 GB) does not fit a host budget: the sample is the
+        # tables of at most 2M rows, over a 4096-query sub-batch
+        keep = [t for t, m in enumerate(c.rows) if m <= 2_000_000]
+        Bs = 4096
+    else:
+        keep = list(range(c.T))
+        Bs = c.batch
+    weights = [W.materialize_table(t, c.rows[t], c.E, c.dtype, seed=c.value_seeds[t], lo=c.lo, hi=c.hi)
+               for t in keep]
+    log(f"cpu baseline: materialized {len(keep)} tables in {time.time() - t0:.1f}s")
+    subs = []
+    for bt in batches:
+        B = bt.B
+        Bs = min(Bs, B)
+        parts, lens = [], []
+        for t in keep:
+            lo, hi = bt.offsets[t * B], bt.offsets[t * B + Bs]
+            parts.append(bt.indices[lo:hi])
+            lens.append(np.diff(bt.offsets[t * B: t * B + Bs + 1]))
+        off = np.zeros(len(keep) * Bs + 1, np.int64)
+        np.cumsum(np.concatenate(lens), out=off[1:])
+        subs.append((np.concatenate(parts), off))
+    lat = []
+    n_look = 0
+    start = time.perf_counter()
+    i = 0
+    while True:
+        idx, off = subs[i % len(subs)]
+        t1 = time.perf_counter()
+        OP.pool_reference(weights, idx, off, Bs)
+        lat.append(time.perf_counter() - t1)
+        n_look += int(off[-1])
+        i += 1
+        if (time.perf_counter() - start >= budget_s and i >= 3) or i >= 1000:
+            break
+    tot = sum(lat)
+    sample = (f"{'all' if len(keep) == c.T else len(keep)} of {c.T} tables, {Bs}-query batches, "
+              f"{i} batches cycled over {len(subs)} distinct")
+    return {"value": n_look / tot, "unit": "lookups/s", "cores": 1, "kind": "oracle", "sample": sample,
+            "queries_per_s": Bs * i / tot, "p99_us": p99(lat) * 1e6, "cpu_model": cpu_model(),
+            "cpu_count": os.cpu_count()}
+
+
+def copy_bandwidth_gbps() -> float:
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 10
+    del a, b
+    return 2 * n / (ms * 1e-3) / 1e9
+
+
+def load_traffic(workload: str, src_hash: str):
+    """HBM bytes per launch from the committed counter summary, if it matches this kernel."""
+    p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        d = json.load(f)
+    if d.get("kernel_source_hash") != src_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=DEFAULT_CONFIG, help="workload 1..5")
+    ap.add_argument("--batches", type=int, default=0, help="distinct resident batches (default 8, 4 for workload 5)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-copy", action="store_true")
+    ap.add_argument("--lds-budget", type=int, default=0)
+    ap.add_argument("--force", type=str, default="", help="force one strategy for all tables (lds|hot|dedup|gather)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the lookup runs on a single MI355X "
+              "(multi-GPU sharding is a design note, not part of this build); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2507_01676_amd as embx
+    assert torch.cuda.is_available(), "no GPU"
+    torch.cuda.set_device(0)
+
+    c = W.make_config(args.config)
+    R = args.batches or (4 if args.config == 5 else 8)
+    t0 = time.time()
+    log(f"workload {c.cfg_id}: {c.name}; generating {R} batches + statistics")
+    batches = [W.gen_batch(c, i) for i in range(R)]
+    stats = W.history_stats(c)
+    log(f"inputs generated in {time.time() - t0:.1f}s; filling {sum(c.rows) * c.row_bytes / 1e9:.2f} GB of tables")
+    dt = torch.float16 if c.dtype == "f16" else torch.float32
+    weights = []
+    for t, m in enumerate(c.rows):
+        w = torch.empty((m, c.E), dtype=dt, device="cuda")
+        embx.fill_table(w, t, c.value_seeds[t], c.lo, c.hi)
+        weights.append(w)
+    d_idx = [torch.from_numpy(b.indices).cuda() for b in batches]
+    d_off = [torch.from_numpy(b.offsets).cuda() for b in batches]
+    out = torch.empty((c.batch, c.T, c.E), dtype=torch.float32, device="cuda")
+    opts = {}
+    if args.lds_budget:
+        opts["lds_budget"] = args.lds_budget
+    if args.force:
+        opts["force"] = [{"lds": 0, "hot": 1, "dedup": 2, "gather": 3}[args.force]] * c.T
+    tp = time.time()
+    plan = embx.Plan(c.rows, c.E, c.dtype, stats, c.batch, **opts).bind(weights)
+    plan_ms = (time.time() - tp) * 1e3
+    info = plan.info()
+    torch.cuda.synchronize()
+    log(f"plan: {info['n_strategy']} items={info['num_items']} lif={info['lif_milli']} ({plan_ms:.1f} ms)")
+
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    ptrs = [(d_idx[i].data_ptr(), d_off[i].data_ptr()) for i in range(R)]
+    n_look = [b.n_lookups for b in batches]
+    outp = out.data_ptr()
+    B = c.batch
+
+    for i in range(args.warmup):
+        ip, op = ptrs[i % R]
+        plan.lookup_ptr(ip, op, B, outp, sp)
+    torch.cuda.synchronize()
+    assert plan.check_errors() == 0
+
+    K = args.steps
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for i in range(K):
+        ip, op = ptrs[i % R]
+        ev0[i].record(stream)
+        plan.lookup_ptr(ip, op, B, outp, sp)
+        ev1[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    lat_ms = [ev0[i].elapsed_time(ev1[i]) for i in range(K)]
+    total_lookups = sum(n_look[i % R] for i in range(K))
+    mean_ms = sum(lat_ms) / K
+
+    R_b = c.row_bytes
+    alg = [W.algorithmic_bytes(c, n_look[i % R])["total"] for i in range(K)]
+    alg_mean = sum(alg) / K
+    useful_mean = sum(n_look[i % R] for i in range(K)) * R_b / K
+    achieved = alg_mean / (mean_ms * 1e-3) / 1e9
+    src_hash = kernel_source_hash()
+    workload = f"workload{c.cfg_id}"
+    traffic = load_traffic(workload, src_hash)
+
+    copy_gbps = None if args.no_copy else copy_bandwidth_gbps()
+    cpu = None
+    if not args.no_cpu:
+        log("timing the CPU oracle")
+        cpu = cpu_baseline(c, batches, args.cpu_seconds)
+
+    res = {
+        "metric": METRIC,
+        "value": total_lookups / wall,
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{workload}: {c.name}", "tables": c.T, "E": c.E, "table_dtype": c.dtype,
+                   "batch": c.batch, "lookups_per_batch": int(sum(n_look) / R), "resident_batches": R,
+                   "table_bytes": sum(c.rows) * R_b},
+        "queries_per_s": B * K / wall,
+        "p99_us": p99(lat_ms) * 1e3,
+        "mean_us": mean_ms * 1e3,
+        "useful_gbps": useful_mean / (mean_ms * 1e-3) / 1e9,
+        "useful_hbm_frac": useful_mean / (mean_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "algorithmic_bytes_per_launch": alg_mean, "kernel": "lookup_kernel"},
+        "copy_gbps": copy_gbps,
+        "plan": {"strategies": info["n_strategy"], "items": info["num_items"], "lif_milli": info["lif_milli"],
+                 "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms},
+        "kernel_source_hash": src_hash,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,186 @@
+/*
+ * embx -- multi-table embedding-bag lookup with sum pooling for DLRM inference
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Ruggeri et al., "Deep Recommender Models Inference: Automatic
+ * Asymmetric Data Flow Optimization", Sec. II-B; sum reduction per Sec. IV-A):
+ * for every sample b of a batch and every table t (m_t rows of E elements),
+ * look up the bag of rows the sample names in that table and reduce them to
+ * one E-vector:
+ *
+ *     out[b, t, :] = sum over k in bag(t, b) of  W_t[indices[k], :]
+ *
+ * Planning follows Sec. III: a linear cost model (Eq. (2)) scores each table
+ * under four per-core data flows and a greedy algorithm maps tables, row chunks
+ * and batch slices asymmetrically onto the GPU's workers (Sec. III-B steps 1-4,
+ * with the LIF fallback to symmetric partitioning of Sec. III-A).
+ *
+ * All functions return an emb_status_t (0 = EMB_OK); no C++ exception crosses
+ * this interface.  Pointers documented as "device" must point to device memory
+ * of the current HIP device; "host" pointers are read during the call only.
+ * A "stream" argument is a hipStream_t passed as void* (NULL = null stream).
+ */
+#ifndef EMBX_H
+#define EMBX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EMB_OK = 0,
+  EMB_ERR_INVALID_ARGUMENT = 1,   /* bad pointer, size, shape, option or statistic   */
+  EMB_ERR_UNSUPPORTED = 2,        /* E / dtype / size outside what the kernels handle */
+  EMB_ERR_OUT_OF_MEMORY = 3,      /* device allocation at plan creation failed        */
+  EMB_ERR_DEVICE = 4,             /* a HIP runtime call failed                        */
+  EMB_ERR_NOT_BOUND = 5,          /* lookup before emb_plan_bind_weights              */
+  EMB_ERR_INDEX_OUT_OF_RANGE = 6, /* emb_plan_check_errors found bad indices          */
+  EMB_ERR_BUFFER_TOO_SMALL = 7    /* serialization buffer too small (len_out is set)  */
+} emb_status_t;
+
+typedef enum { EMB_DTYPE_F32 = 0, EMB_DTYPE_F16 = 1 } emb_dtype_t;
+
+/* Per-table data flows (Sec. II-B mapped onto a CU):
+ *   LDS    -- the table, or a row chunk of it (Sec. III-B), staged into LDS and read from there
+ *             (the paper's L1 / L1-UB flows; LDS does not persist across launches, so the
+ *             staging is paid by every launch);
+ *   HOT    -- the table's hottest rows staged into LDS behind an LDS hash of their ids; misses
+ *             gather from HBM;
+ *   DEDUP  -- each tile of indices is sorted, each distinct row fetched once into LDS, bags
+ *             read their rows from there;
+ *   GATHER -- one row per sub-wavefront straight from HBM with 16-byte loads (the GM flow). */
+typedef enum {
+  EMB_STRAT_AUTO = -1,
+  EMB_STRAT_LDS = 0,
+  EMB_STRAT_HOT = 1,
+  EMB_STRAT_DEDUP = 2,
+  EMB_STRAT_GATHER = 3
+} emb_strategy_t;
+
+/* Cost-model coefficients (Eq. (2) extended per strategy), picoseconds.  Layout of
+ * emb_plan_options_t.beta: per-item (*0), per-lookup (*1, P, I), per staged byte (S).
+ *   gather  = G0 + G1*lam
+ *   lds     = L0 + S*(rows*R) + L1*lam
+ *   chunk   = L0 + S*(rows*R) + I*lam + L1*lam/c
+ *   hot     = H0 + S*(C*R) + lam*(P + h*L1 + (1-h)*G1)
+ *   dedup   = D0 + D1*lam + G1*u*lam
+ * with lam the expected lookups of the slice, R the row bytes, c the chunk count,
+ * C the hot rows staged, h the fraction of lookups they catch, u the unique fraction. */
+enum {
+  EMB_BETA_G0 = 0, EMB_BETA_G1, EMB_BETA_L0, EMB_BETA_L1, EMB_BETA_S, EMB_BETA_I,
+  EMB_BETA_H0, EMB_BETA_P, EMB_BETA_D0, EMB_BETA_D1, EMB_BETA_COUNT
+};
+
+#define EMB_MAX_HOT_STATS 4096   /* hot rows a table's statistics may list     */
+#define EMB_MAX_HOT_SLOTS 2048   /* hot rows one HOT item stages at most        */
+#define EMB_MAX_E 256
+
+/* Per-table index statistics: the paper's S (sequence lengths) and I (query
+ * distribution), Sec. III-A.  Measured on a representative batch. */
+typedef struct {
+  double mean_pooling;      /* s_t >= 0: mean lookups per bag                                   */
+  int32_t max_pooling;      /* upper bound on lookups per bag, 0 = unknown (informational)      */
+  int32_t n_hot;            /* entries in hot_rows / hot_freq, 0..EMB_MAX_HOT_STATS             */
+  const int64_t* hot_rows;  /* host, hottest first, distinct, each in [0, rows)                 */
+  const double* hot_freq;   /* host, fraction of the table's lookups that hit each hot row       */
+  double unique_frac;       /* distinct rows / lookups in a batch, in (0, 1]; <= 0 = unknown      */
+} emb_table_stats_t;
+
+typedef struct {
+  int32_t wg_per_cu;        /* workers per CU; 0 -> 1.  K = CUs * wg_per_cu unless num_workers   */
+  int32_t lds_budget_bytes; /* L, LDS bytes for staged rows per worker; 0 -> 131072 (capped by
+                               the device's LDS per workgroup minus a 28 KiB metadata reserve)   */
+  int32_t lif_milli;        /* LIF threshold x 1000 (Sec. III-B step 4); 0 -> 1250               */
+  int32_t order_mode;       /* 0 = longest first with the paper's keys as tie-breaks;
+                               1 = the paper's order (s desc, m asc)                             */
+  int64_t chunk_max_bytes;  /* max row-chunk bytes (Sec. III-B); <= 0 -> lds_budget_bytes      */
+  const double* beta;       /* host, EMB_BETA_COUNT coefficients; NULL -> built-in placeholders  */
+  const int32_t* force_strategy; /* host, T entries of emb_strategy_t, or NULL (all AUTO)        */
+  int32_t num_workers;      /* > 0 overrides K (must not exceed 65535)                          */
+  int32_t reserved;
+} emb_plan_options_t;
+
+typedef struct emb_plan emb_plan_t;   /* opaque */
+
+typedef struct {
+  int32_t num_tables, embedding_dim, dtype, row_bytes;
+  int32_t num_workers;      /* K = grid size of every lookup launch            */
+  int32_t block_threads;    /* threads per worker                              */
+  int32_t lds_bytes;        /* dynamic LDS per worker                          */
+  int32_t num_items;        /* slices in the plan                              */
+  int32_t max_batch;
+  int32_t lds_budget_bytes;
+  int64_t max_load_ps, sum_load_ps;
+  int32_t lif_milli, r_symmetric;
+  int32_t n_strategy[4];    /* slices per strategy                             */
+} emb_plan_info_t;
+
+/* Builds a plan for T tables of rows[t] x E elements of `dtype`, for batches of up to
+ * max_batch samples, on the current HIP device (Sec. III-A problem statement: N, M, S, B,
+ * K, I, L).  Host-side work plus one upload of the plan's metadata; allocates the device
+ * workspace for row-chunk partial sums.  rows[t] in [1, 2^31); E a multiple of 4 (fp32) or
+ * 8 (fp16), E <= 256; opts may be NULL.  On success *plan_out owns everything it allocated. */
+emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows,
+                             int32_t embedding_dim, emb_dtype_t dtype,
+                             const emb_table_stats_t* stats, int32_t max_batch,
+                             const emb_plan_options_t* opts);
+
+/* Records the T device pointers of the tables (weights[t] -> rows[t] x E contiguous,
+ * row-major, 16-byte aligned).  The caller keeps ownership and keeps them alive. */
+emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights);
+
+/* One batch.  indices: device int64 [offsets[T*batch]], table-local row ids;
+ * offsets: device int64 [T*batch + 1], table-major CSR (bag (t, b) is
+ * indices[offsets[t*batch+b] .. offsets[t*batch+b+1]) ), offsets[0] = 0, non-decreasing;
+ * out: device fp32 [batch, T, E].  Enqueues exactly one kernel on `stream`; never
+ * allocates or synchronizes.  batch == 0 is a no-op.  An index outside [0, rows[t])
+ * contributes nothing and is counted (see emb_plan_check_errors).  Empty bags give +0.0.
+ * Calls on one plan must not overlap (the chunk workspace is per plan). */
+emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets,
+                        int32_t batch, float* out, void* stream);
+
+/* Synchronizes `stream`, returns the number of out-of-range indices seen since the last
+ * call in *n_bad (may be NULL) and resets the counter; EMB_ERR_INDEX_OUT_OF_RANGE if any. */
+emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_bad);
+
+/* Canonical text of the plan (one line per slice: worker, table, strategy, chunk, chunks,
+ * first row, end row, split, slice, hot rows, cost in ps).  Writes at most cap bytes
+ * (NUL-terminated when it fits); *len_out = text length without the NUL. */
+emb_status_t emb_plan_serialize(const emb_plan_t* plan, char* buf, size_t cap, size_t* len_out);
+
+emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info);
+
+/* Frees the plan's device and host memory.  NULL is a no-op. */
+emb_status_t emb_plan_destroy(emb_plan_t* plan);
+
+/* Host-only planner: the same plan text emb_plan_create would produce for
+ * num_workers workers (no device call; lds_budget_bytes 0 -> 131072). */
+emb_status_t emb_plan_text(int32_t num_tables, const int64_t* rows, int32_t embedding_dim,
+                           emb_dtype_t dtype, const emb_table_stats_t* stats, int32_t max_batch,
+                           int32_t num_workers, const emb_plan_options_t* opts, char* buf,
+                           size_t cap, size_t* len_out);
+
+const char* emb_status_string(emb_status_t s);
+
+/* ---- index-handling probes (tests of the exact integer work) ---------------------------
+ * Both run the same device functions as emb_lookup on one workgroup. */
+
+/* Sorts and deduplicates one tile of n <= 2048 row ids (device int64, each in [0, 2^31)):
+ * uniq (device int32 [n]) gets the distinct ids ascending, inv (device int32 [n]) the slot
+ * of each input in uniq, *n_uniq (device int32) the count. */
+emb_status_t emb_debug_dedup_tile(const int64_t* idx, int32_t n, int32_t* uniq, int32_t* inv,
+                                  int32_t* n_uniq, void* stream);
+
+/* Probes table t's LDS hot-row hash of a HOT plan for n ids (device int64): slot (device
+ * int32 [n]) = position of the id among the table's first C hot rows, or -1.
+ * EMB_ERR_INVALID_ARGUMENT if no HOT item of table t exists. */
+emb_status_t emb_debug_hot_probe(const emb_plan_t* plan, int32_t table, const int64_t* idx,
+                                 int32_t n, int32_t* slot, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EMBX_H */

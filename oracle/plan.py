@@ -19,6 +19,10 @@ budget for rows):
 
   P1  strategy choice per table at split k: minimum cost among the feasible
       strategies in the fixed order LDS, HOT, DEDUP, GATHER (ties -> earlier).
+      LDS is feasible iff m_t R <= L; HOT iff C_t >= 1 with C_t = min(hot rows
+      listed, floor(L / R), 2048) the hot rows staged, h_t the fraction of
+      lookups they catch (summed in list order); u_t = unique fraction (1 if
+      unknown).
   P2  (paper step 1) a table larger than L is split into the fewest chunks of
       at most floor(min(chunk_max, L) / R) rows, but only if its best unsplit
       cost exceeds the sum of the chunk costs (the speed-up exceeds the number
@@ -58,7 +62,8 @@ STRAT_ORDER = (LDS, HOT, DEDUP, GATHER)
 G0, G1, L0, L1, S, I, H0, P, D0, D1 = range(10)
 NBETA = 10
 
-MAX_HOT = 4096
+MAX_HOT = 4096          # hot rows a table's statistics may list
+MAX_HOT_SLOTS = 2048    # hot rows one HOT item stages at most
 MAX_CHUNKS = 65536
 
 
@@ -153,10 +158,14 @@ class Plan:
         return "\n".join(lines) + "\n"
 
 
+COST_CAP = 2.0 ** 40          # a slice costing more (about 1.1 s) is rejected
+MAX_SLICES = 1 << 20
+
+
 def _fl(x: float) -> int:
     """floor to integer picoseconds, never negative."""
-    if not math.isfinite(x):
-        raise PlanError("non-finite cost")
+    if not math.isfinite(x) or x >= COST_CAP:
+        raise PlanError("cost model out of range")
     v = math.floor(x)
     return v if v > 0 else 0
 
@@ -190,8 +199,7 @@ class _Table:
         self.t, self.m, self.R = t, m, R
         self.s = float(st.mean_pooling)
         self.Lam = float(B) * self.s
-        cap = L // R
-        self.C = min(st.n_hot, cap)
+        self.C = min(st.n_hot, L // R, MAX_HOT_SLOTS)
         h = 0.0
         for k in range(self.C):
             h = h + float(st.hot_freq[k])
@@ -387,6 +395,8 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
                     loads[sl.wg] += sl.cost
                     out.append(sl)
         rest = [sl for g in groups if g[0].t not in dem for it in g for sl in slices_of(it)]
+        if len(rest) + len(out) > MAX_SLICES:
+            raise PlanError("too many slices")
         rest.sort(key=key)
         heap = [(loads[w], w) for w in range(K)]
         heapq.heapify(heap)

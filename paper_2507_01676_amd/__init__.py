@@ -1,0 +1,288 @@
+"""Python binding of libembx (ctypes): argument marshalling only.
+
+Every step of the lookup runs in the library's HIP kernels; PyTorch provides
+device memory and streams.  Names follow include/embx.h.  Importing this
+package fails loudly if the native library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libembx.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"embx native library missing: {LIB_PATH} (build it with: python paper_2507_01676_amd/build.py)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+# ---------------------------------------------------------------- constants (include/embx.h)
+OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_OUT_OF_MEMORY, ERR_DEVICE, ERR_NOT_BOUND, \
+    ERR_INDEX_OUT_OF_RANGE, ERR_BUFFER_TOO_SMALL = range(8)
+DTYPE_F32, DTYPE_F16 = 0, 1
+STRAT_AUTO, STRAT_LDS, STRAT_HOT, STRAT_DEDUP, STRAT_GATHER = -1, 0, 1, 2, 3
+STRATEGY_NAMES = {0: "LDS", 1: "HOT", 2: "DEDUP", 3: "GATHER"}
+BETA_COUNT = 10
+MAX_HOT_STATS = 4096
+
+EXPORTED = ["emb_plan_create", "emb_plan_bind_weights", "emb_lookup", "emb_plan_check_errors",
+            "emb_plan_serialize", "emb_plan_get_info", "emb_plan_destroy", "emb_plan_text",
+            "emb_status_string", "emb_debug_dedup_tile", "emb_debug_hot_probe", "embx_fill_table"]
+
+
+class EmbxError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {status_string(code)} ({code})")
+
+
+class _Stats(ctypes.Structure):
+    _fields_ = [("mean_pooling", ctypes.c_double), ("max_pooling", ctypes.c_int32), ("n_hot", ctypes.c_int32),
+                ("hot_rows", ctypes.POINTER(ctypes.c_int64)), ("hot_freq", ctypes.POINTER(ctypes.c_double)),
+                ("unique_frac", ctypes.c_double)]
+
+
+class _Opts(ctypes.Structure):
+    _fields_ = [("wg_per_cu", ctypes.c_int32), ("lds_budget_bytes", ctypes.c_int32), ("lif_milli", ctypes.c_int32),
+                ("order_mode", ctypes.c_int32), ("chunk_max_bytes", ctypes.c_int64),
+                ("beta", ctypes.POINTER(ctypes.c_double)), ("force_strategy", ctypes.POINTER(ctypes.c_int32)),
+                ("num_workers", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("num_tables", ctypes.c_int32), ("embedding_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("row_bytes", ctypes.c_int32), ("num_workers", ctypes.c_int32), ("block_threads", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int32), ("num_items", ctypes.c_int32), ("max_batch", ctypes.c_int32),
+                ("lds_budget_bytes", ctypes.c_int32), ("max_load_ps", ctypes.c_int64),
+                ("sum_load_ps", ctypes.c_int64), ("lif_milli", ctypes.c_int32), ("r_symmetric", ctypes.c_int32),
+                ("n_strategy", ctypes.c_int32 * 4)]
+
+
+_vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+_lib.emb_status_string.restype = ctypes.c_char_p
+_lib.emb_status_string.argtypes = [_i32]
+_lib.emb_plan_create.argtypes = [ctypes.POINTER(_vp), _i32, ctypes.POINTER(_i64), _i32, _i32,
+                                 ctypes.POINTER(_Stats), _i32, ctypes.POINTER(_Opts)]
+_lib.emb_plan_bind_weights.argtypes = [_vp, ctypes.POINTER(_vp)]
+_lib.emb_lookup.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp]
+_lib.emb_plan_check_errors.argtypes = [_vp, _vp, ctypes.POINTER(_i64)]
+_lib.emb_plan_serialize.argtypes = [_vp, ctypes.c_char_p, _sz, ctypes.POINTER(_sz)]
+_lib.emb_plan_get_info.argtypes = [_vp, ctypes.POINTER(_Info)]
+_lib.emb_plan_destroy.argtypes = [_vp]
+_lib.emb_plan_text.argtypes = [_i32, ctypes.POINTER(_i64), _i32, _i32, ctypes.POINTER(_Stats), _i32, _i32,
+                               ctypes.POINTER(_Opts), ctypes.c_char_p, _sz, ctypes.POINTER(_sz)]
+_lib.emb_debug_dedup_tile.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
+_lib.emb_debug_hot_probe.argtypes = [_vp, _i32, _vp, _i32, _vp, _vp]
+_lib.embx_fill_table.argtypes = [_vp, _i64, _i64, _i32, _i32, _i32, ctypes.c_uint64, ctypes.c_double,
+                                 ctypes.c_double, _i32, _vp]
+for _f in EXPORTED:
+    if _f != "emb_status_string":
+        getattr(_lib, _f).restype = _i32
+
+
+def status_string(code: int) -> str:
+    return _lib.emb_status_string(int(code)).decode()
+
+
+def _check(code: int, what: str):
+    if code != OK:
+        raise EmbxError(code, what)
+
+
+def _dtype_code(dtype) -> int:
+    if dtype in ("f32", "fp32", "float32", DTYPE_F32):
+        return DTYPE_F32
+    if dtype in ("f16", "fp16", "float16", DTYPE_F16):
+        return DTYPE_F16
+    try:
+        import torch
+        if dtype == torch.float32:
+            return DTYPE_F32
+        if dtype == torch.float16:
+            return DTYPE_F16
+    except ImportError:
+        pass
+    raise ValueError(f"unsupported dtype {dtype!r}")
+
+
+def _get(s, name, default=None):
+    if isinstance(s, dict):
+        return s.get(name, default)
+    return getattr(s, name, default)
+
+
+class _Marshal:
+    """Holds the ctypes views of the statistics and options for one call."""
+
+    def __init__(self, rows, stats, opts: dict, T: int):
+        self.rows = (ctypes.c_int64 * T)(*[int(r) for r in rows])
+        self.stats = (_Stats * T)()
+        self.keep = []
+        for t, s in enumerate(stats):
+            hr = np.ascontiguousarray(np.asarray(_get(s, "hot_rows", []), dtype=np.int64)[:MAX_HOT_STATS])
+            hf = np.ascontiguousarray(np.asarray(_get(s, "hot_freq", []), dtype=np.float64)[:MAX_HOT_STATS])
+            n = min(hr.size, hf.size)
+            self.keep += [hr, hf]
+            st = self.stats[t]
+            st.mean_pooling = float(_get(s, "mean_pooling", 1.0))
+            st.max_pooling = int(_get(s, "max_pooling", 0) or 0)
+            st.n_hot = n
+            st.hot_rows = hr.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if n else None
+            st.hot_freq = hf.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) if n else None
+            uf = _get(s, "unique_frac", -1.0)
+            st.unique_frac = float(-1.0 if uf is None else uf)
+        o = _Opts()
+        o.wg_per_cu = int(opts.get("wg_per_cu", 0))
+        o.lds_budget_bytes = int(opts.get("lds_budget", 0))
+        o.lif_milli = int(opts.get("lif_milli", 0))
+        o.order_mode = int(opts.get("order_mode", 0))
+        o.chunk_max_bytes = int(opts.get("chunk_max_bytes", 0))
+        o.num_workers = int(opts.get("num_workers", 0))
+        beta = opts.get("beta")
+        if beta is not None:
+            b = np.ascontiguousarray(np.asarray(beta, dtype=np.float64))
+            assert b.size == BETA_COUNT
+            self.keep.append(b)
+            o.beta = b.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+        force = opts.get("force")
+        if force is not None:
+            f = np.ascontiguousarray(np.asarray(force, dtype=np.int32))
+            assert f.size == T
+            self.keep.append(f)
+            o.force_strategy = f.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        self.opts = o
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def plan_text(rows: Sequence[int], E: int, dtype, stats, max_batch: int, num_workers: int, **opts) -> str:
+    """The planner alone (host only): the canonical text of the plan for ``num_workers`` workers."""
+    T = len(rows)
+    m = _Marshal(rows, stats, opts, T)
+    n = _sz(0)
+    code = _lib.emb_plan_text(T, m.rows, int(E), _dtype_code(dtype), m.stats, int(max_batch), int(num_workers),
+                              ctypes.byref(m.opts), None, 0, ctypes.byref(n))
+    if code not in (OK, ERR_BUFFER_TOO_SMALL):
+        raise EmbxError(code, "emb_plan_text")
+    buf = ctypes.create_string_buffer(n.value + 1)
+    _check(_lib.emb_plan_text(T, m.rows, int(E), _dtype_code(dtype), m.stats, int(max_batch), int(num_workers),
+                              ctypes.byref(m.opts), buf, n.value + 1, ctypes.byref(n)), "emb_plan_text")
+    return buf.value.decode()
+
+
+class Plan:
+    """A lookup plan on the current HIP device (emb_plan_create .. emb_plan_destroy)."""
+
+    def __init__(self, rows: Sequence[int], E: int, dtype, stats, max_batch: int, **opts):
+        self.T = len(rows)
+        self.E = int(E)
+        self.dtype = _dtype_code(dtype)
+        self.max_batch = int(max_batch)
+        m = _Marshal(rows, stats, opts, self.T)
+        h = _vp()
+        _check(_lib.emb_plan_create(ctypes.byref(h), self.T, m.rows, self.E, self.dtype, m.stats, self.max_batch,
+                                    ctypes.byref(m.opts)), "emb_plan_create")
+        self._h = h
+        self._weights = None
+
+    def bind(self, weights: List) -> "Plan":
+        import torch
+        assert len(weights) == self.T
+        want = torch.float16 if self.dtype == DTYPE_F16 else torch.float32
+        for w in weights:
+            if not (w.is_cuda and w.dtype == want and w.dim() == 2 and w.shape[1] == self.E and w.is_contiguous()):
+                raise ValueError("weights must be contiguous [rows, E] device tensors of the plan's dtype")
+        arr = (_vp * self.T)(*[w.data_ptr() for w in weights])
+        _check(_lib.emb_plan_bind_weights(self._h, arr), "emb_plan_bind_weights")
+        self._weights = list(weights)
+        return self
+
+    def lookup(self, indices, offsets, batch: int, out=None, stream=None):
+        import torch
+        if out is None:
+            out = torch.empty((batch, self.T, self.E), dtype=torch.float32, device=indices.device)
+        assert indices.dtype == torch.int64 and offsets.dtype == torch.int64 and out.dtype == torch.float32
+        assert out.is_contiguous() and out.numel() >= batch * self.T * self.E
+        assert offsets.numel() >= self.T * batch + 1
+        _check(_lib.emb_lookup(self._h, indices.data_ptr(), offsets.data_ptr(), int(batch), out.data_ptr(),
+                               _stream_ptr(stream)), "emb_lookup")
+        return out
+
+    def lookup_ptr(self, indices_ptr: int, offsets_ptr: int, batch: int, out_ptr: int, stream_ptr) -> None:
+        """Raw-pointer launch (benchmark loop)."""
+        _check(_lib.emb_lookup(self._h, indices_ptr, offsets_ptr, int(batch), out_ptr, stream_ptr), "emb_lookup")
+
+    def check_errors(self, stream=None) -> int:
+        n = _i64(0)
+        code = _lib.emb_plan_check_errors(self._h, _stream_ptr(stream), ctypes.byref(n))
+        if code not in (OK, ERR_INDEX_OUT_OF_RANGE):
+            raise EmbxError(code, "emb_plan_check_errors")
+        return int(n.value)
+
+    def serialize(self) -> str:
+        n = _sz(0)
+        _lib.emb_plan_serialize(self._h, None, 0, ctypes.byref(n))
+        buf = ctypes.create_string_buffer(n.value + 1)
+        _check(_lib.emb_plan_serialize(self._h, buf, n.value + 1, ctypes.byref(n)), "emb_plan_serialize")
+        return buf.value.decode()
+
+    def info(self) -> dict:
+        i = _Info()
+        _check(_lib.emb_plan_get_info(self._h, ctypes.byref(i)), "emb_plan_get_info")
+        d = {k: getattr(i, k) for k, _ in _Info._fields_ if k != "n_strategy"}
+        d["n_strategy"] = {STRATEGY_NAMES[s]: i.n_strategy[s] for s in range(4)}
+        return d
+
+    def hot_probe(self, table: int, idx, stream=None):
+        import torch
+        slot = torch.empty(idx.numel(), dtype=torch.int32, device=idx.device)
+        _check(_lib.emb_debug_hot_probe(self._h, int(table), idx.data_ptr(), idx.numel(), slot.data_ptr(),
+                                        _stream_ptr(stream)), "emb_debug_hot_probe")
+        return slot
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _check(_lib.emb_plan_destroy(self._h), "emb_plan_destroy")
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def fill_table(w, table_id: int, seed: int, lo: float = -0.05, hi: float = 0.05, mode: int = 0,
+               row_begin: int = 0, stream=None):
+    """Fills device tensor ``w`` [n, E] with rows [row_begin, row_begin+n) of the synthetic table."""
+    import torch
+    assert w.is_cuda and w.is_contiguous() and w.dim() == 2
+    dt = DTYPE_F16 if w.dtype == torch.float16 else DTYPE_F32
+    _check(_lib.embx_fill_table(w.data_ptr(), int(row_begin), int(w.shape[0]), int(w.shape[1]), dt, int(table_id),
+                                int(seed) & ((1 << 64) - 1), float(lo), float(hi), int(mode), _stream_ptr(stream)),
+           "embx_fill_table")
+    return w
+
+
+def dedup_tile(idx, stream=None):
+    """Device tile sort/dedup of up to 2048 row ids: (sorted distinct ids, slot of each input)."""
+    import torch
+    n = idx.numel()
+    uniq = torch.empty(max(n, 1), dtype=torch.int32, device=idx.device)
+    inv = torch.empty(max(n, 1), dtype=torch.int32, device=idx.device)
+    nu = torch.zeros(1, dtype=torch.int32, device=idx.device)
+    _check(_lib.emb_debug_dedup_tile(idx.data_ptr(), n, uniq.data_ptr(), inv.data_ptr(), nu.data_ptr(),
+                                     _stream_ptr(stream)), "emb_debug_dedup_tile")
+    k = int(nu.item())
+    return uniq[:k], inv[:n]

@@ -1,0 +1,438 @@
+// C ABI of the embedding-bag lookup library: plan creation (host planner + one
+// upload of the plan's metadata), weight binding, the per-batch launch, error
+// reporting and plan introspection.  See include/embx.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/embx.h"
+#include "../../include/embx_fill.h"
+#include "device_types.hpp"
+#include "planner.hpp"
+
+using namespace embx;
+
+struct emb_plan {
+  PlanOut plan;
+  int device = 0;
+  int32_t T = 0, E = 0, R = 0, G = 0, K = 0, Bmax = 0;
+  bool f16 = false;
+  int lds_bytes = 0;
+  int32_t lds_rows = 0;
+  bool bound = false;
+  std::vector<DevTable> h_tables;
+  std::vector<int32_t> hot_table_log2;   // per table: hash log2 (0 = no HOT item)
+  std::vector<int64_t> hot_table_off;    // per table: element offset of hash / ids
+  char* d_meta = nullptr;                // items, wg_ptr, tables, hash, ids, counters, err
+  float* d_partials = nullptr;
+  DevItem* d_items = nullptr;
+  int32_t* d_wg_ptr = nullptr;
+  DevTable* d_tables = nullptr;
+  int32_t* d_hot_keys = nullptr;
+  uint16_t* d_hot_slots = nullptr;
+  int32_t* d_hot_ids = nullptr;
+  int32_t* d_counters = nullptr;
+  unsigned long long* d_err = nullptr;
+};
+
+namespace {
+
+emb_status_t st(int code) { return static_cast<emb_status_t>(code); }
+
+int next_pow2_log2(int64_t x) {
+  int l = 0;
+  while ((int64_t(1) << l) < x) ++l;
+  return l;
+}
+
+int lanes_per_row(int32_t R) {
+  int g = 1;
+  while (g * 16 < R) g <<= 1;
+  return g;
+}
+
+// Fills a PlanIn from the C arguments (validation of the raw pointers only; the
+// planner validates values).
+emb_status_t to_plan_in(int32_t T, const int64_t* rows, int32_t E, emb_dtype_t dtype, const emb_table_stats_t* stats,
+                        int32_t max_batch, int32_t K, const emb_plan_options_t* opts, int64_t L, PlanIn* in) {
+  if (T < 1 || !rows || !stats) return EMB_ERR_INVALID_ARGUMENT;
+  if (dtype != EMB_DTYPE_F32 && dtype != EMB_DTYPE_F16) return EMB_ERR_UNSUPPORTED;
+  in->tables.resize(T);
+  for (int32_t t = 0; t < T; ++t) {
+    in->tables[t].rows = rows[t];
+    in->tables[t].mean_pooling = stats[t].mean_pooling;
+    in->tables[t].n_hot = stats[t].n_hot;
+    in->tables[t].hot_freq = stats[t].hot_freq;
+    in->tables[t].unique_frac = stats[t].unique_frac;
+  }
+  in->E = E;
+  in->esize = dtype == EMB_DTYPE_F16 ? 2 : 4;
+  in->B = max_batch;
+  in->K = K;
+  in->L = L;
+  if (opts) {
+    if (opts->lif_milli < 0 || opts->order_mode < 0 || opts->wg_per_cu < 0 || opts->num_workers < 0)
+      return EMB_ERR_INVALID_ARGUMENT;
+    if (opts->lif_milli > 0) in->lif_milli = opts->lif_milli;
+    in->chunk_max = opts->chunk_max_bytes;
+    in->order_mode = opts->order_mode;
+    if (opts->beta) {
+      in->has_beta = true;
+      for (int i = 0; i < B_COUNT; ++i) in->beta[i] = opts->beta[i];
+    }
+    if (opts->force_strategy) in->force.assign(opts->force_strategy, opts->force_strategy + T);
+  }
+  return EMB_OK;
+}
+
+emb_status_t write_text(const std::string& s, char* buf, size_t cap, size_t* len_out) {
+  if (len_out) *len_out = s.size();
+  if (!buf || cap < s.size() + 1) return EMB_ERR_BUFFER_TOO_SMALL;
+  std::memcpy(buf, s.data(), s.size());
+  buf[s.size()] = '\0';
+  return EMB_OK;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace
+
+extern "C" {
+
+const char* emb_status_string(emb_status_t s) {
+  switch (s) {
+    case EMB_OK: return "ok";
+    case EMB_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case EMB_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case EMB_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case EMB_ERR_DEVICE: return "HIP runtime error";
+    case EMB_ERR_NOT_BOUND: return "weights not bound";
+    case EMB_ERR_INDEX_OUT_OF_RANGE: return "index out of range";
+    case EMB_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+  }
+  return "unknown status";
+}
+
+emb_status_t emb_plan_text(int32_t num_tables, const int64_t* rows, int32_t embedding_dim, emb_dtype_t dtype,
+                           const emb_table_stats_t* stats, int32_t max_batch, int32_t num_workers,
+                           const emb_plan_options_t* opts, char* buf, size_t cap, size_t* len_out) {
+  if (num_workers < 1 || num_workers > 65535) return EMB_ERR_INVALID_ARGUMENT;
+  int64_t L = 131072;
+  if (opts && opts->lds_budget_bytes < 0) return EMB_ERR_INVALID_ARGUMENT;
+  if (opts && opts->lds_budget_bytes > 0) L = opts->lds_budget_bytes;
+  PlanIn in;
+  emb_status_t s = to_plan_in(num_tables, rows, embedding_dim, dtype, stats, max_batch, num_workers, opts, L, &in);
+  if (s != EMB_OK) return s;
+  PlanOut out;
+  std::string err;
+  const int rc = build_plan(in, &out, &err);
+  if (rc != 0) return st(rc);
+  return write_text(plan_text(out), buf, cap, len_out);
+}
+
+emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows, int32_t embedding_dim,
+                             emb_dtype_t dtype, const emb_table_stats_t* stats, int32_t max_batch,
+                             const emb_plan_options_t* opts) {
+  if (!plan_out) return EMB_ERR_INVALID_ARGUMENT;
+  *plan_out = nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return EMB_ERR_DEVICE;
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return EMB_ERR_DEVICE;
+  const int cus = prop.multiProcessorCount;
+  const int64_t smem = static_cast<int64_t>(prop.sharedMemPerBlock);
+  // LDS for staged rows: the caller's budget, or 128 KiB, within what a workgroup may
+  // allocate once the metadata region and the kernel's own static LDS are set aside
+  const int64_t room = ((smem - kMetaReserve - 1024) / 16) * 16;
+  if (room < 16) return EMB_ERR_UNSUPPORTED;
+  int64_t L = std::min<int64_t>(131072, room);
+  if (opts && opts->lds_budget_bytes < 0) return EMB_ERR_INVALID_ARGUMENT;
+  if (opts && opts->lds_budget_bytes > 0) {
+    if (opts->lds_budget_bytes > room) return EMB_ERR_UNSUPPORTED;
+    L = opts->lds_budget_bytes;
+  }
+  int K = cus * ((opts && opts->wg_per_cu > 0) ? opts->wg_per_cu : 1);
+  if (opts && opts->num_workers > 0) K = opts->num_workers;
+  if (K < 1 || K > 65535) return EMB_ERR_INVALID_ARGUMENT;
+  if (max_batch < 1) return EMB_ERR_INVALID_ARGUMENT;
+
+  PlanIn in;
+  emb_status_t s = to_plan_in(num_tables, rows, embedding_dim, dtype, stats, max_batch, K, opts, L, &in);
+  if (s != EMB_OK) return s;
+  emb_plan* p = new (std::nothrow) emb_plan();
+  if (!p) return EMB_ERR_OUT_OF_MEMORY;
+  std::string err;
+  const int rc = build_plan(in, &p->plan, &err);
+  if (rc != 0) {
+    delete p;
+    return st(rc);
+  }
+  const PlanOut& P = p->plan;
+  p->device = dev;
+  p->T = num_tables;
+  p->E = embedding_dim;
+  p->R = P.R;
+  p->G = lanes_per_row(P.R);
+  p->K = K;
+  p->Bmax = max_batch;
+  p->f16 = dtype == EMB_DTYPE_F16;
+  p->lds_rows = static_cast<int32_t>(L);
+
+  // hot hashes (one per table with a HOT slice), chunk workspaces, combine counters
+  const int32_t T = num_tables;
+  std::vector<char> table_hot(T, 0);
+  std::vector<int32_t> nchunks(T, 1), ksplit(T, 1);
+  bool staged = false;
+  for (const PSlice& x : P.slices) {
+    if (x.strat == S_HOT) table_hot[x.t] = 1;
+    nchunks[x.t] = x.nchunks;
+    ksplit[x.t] = x.k;
+    if (x.strat != S_GATHER) staged = true;
+  }
+  p->hot_table_log2.assign(T, 0);
+  p->hot_table_off.assign(T, 0);
+  std::vector<int32_t> h_keys, h_ids;
+  std::vector<uint16_t> h_slots;
+  for (int32_t t = 0; t < T; ++t) {
+    if (!table_hot[t]) continue;
+    const int32_t C = P.C_of_table[t];
+    if (C < 1 || !stats[t].hot_rows) {
+      delete p;
+      return EMB_ERR_INVALID_ARGUMENT;
+    }
+    const int lg = std::max(1, next_pow2_log2(C + C / 2 + 1));
+    const int H = 1 << lg;
+    const int64_t base = static_cast<int64_t>(h_keys.size());
+    p->hot_table_log2[t] = lg;
+    p->hot_table_off[t] = base;
+    h_keys.resize(base + H, -1);
+    h_slots.resize(base + H, 0);
+    h_ids.resize(base + H, 0);
+    for (int32_t s2 = 0; s2 < C; ++s2) {
+      const int64_t r = stats[t].hot_rows[s2];
+      if (r < 0 || r >= rows[t]) {
+        delete p;
+        return EMB_ERR_INVALID_ARGUMENT;
+      }
+      uint32_t h = hot_hash(static_cast<uint32_t>(r), lg);
+      while (h_keys[base + h] >= 0) {
+        if (h_keys[base + h] == static_cast<int32_t>(r)) {   // listed twice
+          delete p;
+          return EMB_ERR_INVALID_ARGUMENT;
+        }
+        h = (h + 1u) & static_cast<uint32_t>(H - 1);
+      }
+      h_keys[base + h] = static_cast<int32_t>(r);
+      h_slots[base + h] = static_cast<uint16_t>(s2);
+      h_ids[base + s2] = static_cast<int32_t>(r);
+    }
+  }
+  p->h_tables.assign(T, DevTable{nullptr, 0, 0, 1, 0});
+  int64_t part_floats = 0;
+  std::vector<int32_t> ctr_base(T, 0);
+  int32_t n_ctr = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    p->h_tables[t].rows = rows[t];
+    p->h_tables[t].nchunks = nchunks[t];
+    if (nchunks[t] > 1) {
+      p->h_tables[t].part_base = part_floats;
+      part_floats += static_cast<int64_t>(nchunks[t]) * max_batch * embedding_dim;
+      ctr_base[t] = n_ctr;
+      n_ctr += ksplit[t];
+    }
+  }
+
+  // items in worker order
+  std::vector<DevItem> items;
+  std::vector<int32_t> wg_ptr(K + 1, 0);
+  items.reserve(P.slices.size());
+  for (const PSlice& x : P.slices) {
+    DevItem d{};
+    d.table = x.t;
+    d.strat = x.strat;
+    d.chunk = x.chunk;
+    d.nchunks = x.nchunks;
+    d.r0 = x.r0;
+    d.r1 = x.r1;
+    d.k = x.k;
+    d.j = x.j;
+    d.C = x.strat == S_HOT ? x.C : 0;
+    d.hash_log2 = x.strat == S_HOT ? p->hot_table_log2[x.t] : 0;
+    d.hot_off = x.strat == S_HOT ? p->hot_table_off[x.t] : 0;
+    d.counter = x.nchunks > 1 ? ctr_base[x.t] + x.j : 0;
+    items.push_back(d);
+    wg_ptr[x.wg + 1] += 1;
+  }
+  for (int w = 0; w < K; ++w) wg_ptr[w + 1] += wg_ptr[w];
+
+  // one metadata allocation
+  size_t o_items = 0;
+  size_t o_wg = align_up(o_items + items.size() * sizeof(DevItem), 256);
+  size_t o_tab = align_up(o_wg + wg_ptr.size() * sizeof(int32_t), 256);
+  size_t o_keys = align_up(o_tab + T * sizeof(DevTable), 256);
+  size_t o_slots = align_up(o_keys + h_keys.size() * sizeof(int32_t), 256);
+  size_t o_ids = align_up(o_slots + h_slots.size() * sizeof(uint16_t), 256);
+  size_t o_ctr = align_up(o_ids + h_ids.size() * sizeof(int32_t), 256);
+  size_t o_err = align_up(o_ctr + static_cast<size_t>(n_ctr) * sizeof(int32_t), 256);
+  size_t total = align_up(o_err + sizeof(unsigned long long), 256);
+  if (hipMalloc(&p->d_meta, total) != hipSuccess) {
+    delete p;
+    return EMB_ERR_OUT_OF_MEMORY;
+  }
+  if (part_floats > 0 && hipMalloc(&p->d_partials, part_floats * sizeof(float)) != hipSuccess) {
+    (void)hipFree(p->d_meta);
+    delete p;
+    return EMB_ERR_OUT_OF_MEMORY;
+  }
+  p->d_items = reinterpret_cast<DevItem*>(p->d_meta + o_items);
+  p->d_wg_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_wg);
+  p->d_tables = reinterpret_cast<DevTable*>(p->d_meta + o_tab);
+  p->d_hot_keys = reinterpret_cast<int32_t*>(p->d_meta + o_keys);
+  p->d_hot_slots = reinterpret_cast<uint16_t*>(p->d_meta + o_slots);
+  p->d_hot_ids = reinterpret_cast<int32_t*>(p->d_meta + o_ids);
+  p->d_counters = reinterpret_cast<int32_t*>(p->d_meta + o_ctr);
+  p->d_err = reinterpret_cast<unsigned long long*>(p->d_meta + o_err);
+  std::vector<char> host(total, 0);
+  if (!items.empty()) std::memcpy(host.data() + o_items, items.data(), items.size() * sizeof(DevItem));
+  std::memcpy(host.data() + o_wg, wg_ptr.data(), wg_ptr.size() * sizeof(int32_t));
+  std::memcpy(host.data() + o_tab, p->h_tables.data(), T * sizeof(DevTable));
+  if (!h_keys.empty()) {
+    std::memcpy(host.data() + o_keys, h_keys.data(), h_keys.size() * sizeof(int32_t));
+    std::memcpy(host.data() + o_slots, h_slots.data(), h_slots.size() * sizeof(uint16_t));
+    std::memcpy(host.data() + o_ids, h_ids.data(), h_ids.size() * sizeof(int32_t));
+  }
+  if (hipMemcpy(p->d_meta, host.data(), total, hipMemcpyHostToDevice) != hipSuccess ||
+      (p->d_partials && hipMemset(p->d_partials, 0, part_floats * sizeof(float)) != hipSuccess)) {
+    emb_plan_destroy(p);
+    return EMB_ERR_DEVICE;
+  }
+  p->lds_bytes = staged ? static_cast<int>(L) + kMetaReserve : 0;
+  if (prepare_lookup_kernels(std::max(p->lds_bytes, kMetaReserve)) != 0) {
+    emb_plan_destroy(p);
+    return EMB_ERR_DEVICE;
+  }
+  *plan_out = p;
+  return EMB_OK;
+}
+
+emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights) {
+  if (!plan || !weights) return EMB_ERR_INVALID_ARGUMENT;
+  for (int32_t t = 0; t < plan->T; ++t) {
+    if (!weights[t] || (reinterpret_cast<uintptr_t>(weights[t]) & 15u) != 0) return EMB_ERR_INVALID_ARGUMENT;
+  }
+  for (int32_t t = 0; t < plan->T; ++t) plan->h_tables[t].w = weights[t];
+  if (hipMemcpy(plan->d_tables, plan->h_tables.data(), plan->T * sizeof(DevTable), hipMemcpyHostToDevice) !=
+      hipSuccess)
+    return EMB_ERR_DEVICE;
+  plan->bound = true;
+  return EMB_OK;
+}
+
+emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets, int32_t batch, float* out,
+                        void* stream) {
+  if (!plan) return EMB_ERR_INVALID_ARGUMENT;
+  if (batch < 0 || batch > plan->Bmax) return EMB_ERR_INVALID_ARGUMENT;
+  if (!plan->bound) return EMB_ERR_NOT_BOUND;
+  if (batch == 0) return EMB_OK;
+  if (!indices || !offsets || !out) return EMB_ERR_INVALID_ARGUMENT;
+  if ((reinterpret_cast<uintptr_t>(out) & 15u) != 0 || (reinterpret_cast<uintptr_t>(indices) & 7u) != 0 ||
+      (reinterpret_cast<uintptr_t>(offsets) & 7u) != 0)
+    return EMB_ERR_INVALID_ARGUMENT;
+  LookupArgs a;
+  a.items = plan->d_items;
+  a.wg_ptr = plan->d_wg_ptr;
+  a.tables = plan->d_tables;
+  a.hot_keys = plan->d_hot_keys;
+  a.hot_slots = plan->d_hot_slots;
+  a.hot_ids = plan->d_hot_ids;
+  a.indices = indices;
+  a.offsets = offsets;
+  a.out = out;
+  a.partials = plan->d_partials;
+  a.counters = plan->d_counters;
+  a.err = plan->d_err;
+  a.B = batch;
+  a.Bmax = plan->Bmax;
+  a.T = plan->T;
+  a.E = plan->E;
+  a.R = plan->R;
+  a.lds_rows = plan->lds_rows;
+  return st(launch_lookup(a, plan->G, plan->f16, plan->K, plan->lds_bytes, stream));
+}
+
+emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_bad) {
+  if (!plan) return EMB_ERR_INVALID_ARGUMENT;
+  if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return EMB_ERR_DEVICE;
+  unsigned long long v = 0;
+  if (hipMemcpy(&v, plan->d_err, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return EMB_ERR_DEVICE;
+  if (v != 0 && hipMemset(plan->d_err, 0, sizeof v) != hipSuccess) return EMB_ERR_DEVICE;
+  if (n_bad) *n_bad = static_cast<int64_t>(v);
+  return v ? EMB_ERR_INDEX_OUT_OF_RANGE : EMB_OK;
+}
+
+emb_status_t emb_plan_serialize(const emb_plan_t* plan, char* buf, size_t cap, size_t* len_out) {
+  if (!plan) return EMB_ERR_INVALID_ARGUMENT;
+  return write_text(plan_text(plan->plan), buf, cap, len_out);
+}
+
+emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info) {
+  if (!plan || !info) return EMB_ERR_INVALID_ARGUMENT;
+  std::memset(info, 0, sizeof *info);
+  info->num_tables = plan->T;
+  info->embedding_dim = plan->E;
+  info->dtype = plan->f16 ? EMB_DTYPE_F16 : EMB_DTYPE_F32;
+  info->row_bytes = plan->R;
+  info->num_workers = plan->K;
+  info->block_threads = kBlock;
+  info->lds_bytes = plan->lds_bytes;
+  info->num_items = static_cast<int32_t>(plan->plan.slices.size());
+  info->max_batch = plan->Bmax;
+  info->lds_budget_bytes = plan->lds_rows;
+  info->max_load_ps = plan->plan.max_ps;
+  info->sum_load_ps = plan->plan.sum_ps;
+  info->lif_milli = static_cast<int32_t>(plan->plan.lif_milli);
+  info->r_symmetric = plan->plan.r_sym;
+  for (const PSlice& x : plan->plan.slices) info->n_strategy[x.strat] += 1;
+  return EMB_OK;
+}
+
+emb_status_t emb_plan_destroy(emb_plan_t* plan) {
+  if (!plan) return EMB_OK;
+  emb_status_t s = EMB_OK;
+  if (plan->d_partials && hipFree(plan->d_partials) != hipSuccess) s = EMB_ERR_DEVICE;
+  if (plan->d_meta && hipFree(plan->d_meta) != hipSuccess) s = EMB_ERR_DEVICE;
+  delete plan;
+  return s;
+}
+
+emb_status_t emb_debug_dedup_tile(const int64_t* idx, int32_t n, int32_t* uniq, int32_t* inv, int32_t* n_uniq,
+                                  void* stream) {
+  if (n < 0 || n > kTile || (n > 0 && (!idx || !uniq || !inv)) || !n_uniq) return EMB_ERR_INVALID_ARGUMENT;
+  if (prepare_lookup_kernels(kMetaReserve) != 0) return EMB_ERR_DEVICE;
+  return st(launch_dedup_probe(idx, n, uniq, inv, n_uniq, stream));
+}
+
+emb_status_t emb_debug_hot_probe(const emb_plan_t* plan, int32_t table, const int64_t* idx, int32_t n,
+                                 int32_t* slot, void* stream) {
+  if (!plan || table < 0 || table >= plan->T || n < 0 || (n > 0 && (!idx || !slot))) return EMB_ERR_INVALID_ARGUMENT;
+  const int lg = plan->hot_table_log2[table];
+  if (lg == 0) return EMB_ERR_INVALID_ARGUMENT;
+  const int64_t off = plan->hot_table_off[table];
+  return st(launch_hot_probe(plan->d_hot_keys + off, plan->d_hot_slots + off, lg, idx, n, slot, stream));
+}
+
+emb_status_t embx_fill_table(void* dst, int64_t row_begin, int64_t n_rows, int32_t embedding_dim, emb_dtype_t dtype,
+                             int32_t table_id, uint64_t seed, double lo, double hi, int32_t mode, void* stream) {
+  if (!dst || row_begin < 0 || n_rows < 0 || embedding_dim < 1 || embedding_dim > 256 || table_id < 0 ||
+      table_id >= (1 << 23) || (mode != 0 && mode != 1) || row_begin + n_rows > (int64_t(1) << 32))
+    return EMB_ERR_INVALID_ARGUMENT;
+  if (dtype != EMB_DTYPE_F32 && dtype != EMB_DTYPE_F16) return EMB_ERR_UNSUPPORTED;
+  return st(launch_fill(dst, row_begin, n_rows, embedding_dim, dtype == EMB_DTYPE_F16, table_id, seed, lo, hi, mode,
+                        stream));
+}
+
+}  // extern "C"

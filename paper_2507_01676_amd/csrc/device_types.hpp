@@ -1,0 +1,77 @@
+// Plan metadata as the lookup kernel reads it from device memory, and the
+// argument block of one launch.  Shared by the host API and the kernels.
+#pragma once
+
+#include <cstdint>
+
+namespace embx {
+
+constexpr int kBlock = 1024;        // threads per worker (16 wave64s: one worker per CU)
+constexpr int kTile = 2048;         // DEDUP: lookups per sorted tile
+constexpr int kMetaReserve = 28928;   // LDS beyond the row budget: hot hash or dedup tile
+
+// One slice of the plan: table t (or rows [r0, r1) of it), batch slice j of k.
+struct DevItem {
+  int32_t table;
+  int32_t strat;        // 0 LDS, 1 HOT, 2 DEDUP, 3 GATHER
+  int32_t chunk;
+  int32_t nchunks;
+  int64_t r0, r1;
+  int32_t k, j;
+  int32_t C;            // HOT: rows staged
+  int32_t hash_log2;    // HOT: log2 of the hash size
+  int64_t hot_off;      // HOT: element offset of this table's hash / hot ids
+  int32_t counter;      // chunked: combine counter of (table, j)
+  int32_t pad;
+};
+
+struct DevTable {
+  const void* w;        // rows x E, row-major
+  int64_t rows;
+  int64_t part_base;    // chunked tables: float offset of the [nchunks, Bmax, E] partial slab
+  int32_t nchunks;
+  int32_t pad;
+};
+
+struct LookupArgs {
+  const DevItem* items;
+  const int32_t* wg_ptr;        // [K + 1] item ranges per worker
+  const DevTable* tables;
+  const int32_t* hot_keys;      // hash keys (row ids, -1 = empty)
+  const uint16_t* hot_slots;    // hash values (slot in the hot list)
+  const int32_t* hot_ids;       // hot row ids in slot order
+  const int64_t* indices;
+  const int64_t* offsets;
+  float* out;
+  float* partials;
+  int32_t* counters;
+  unsigned long long* err;
+  int32_t B;                    // runtime batch
+  int32_t Bmax;
+  int32_t T;
+  int32_t E;
+  int32_t R;                    // row bytes
+  int32_t lds_rows;             // LDS bytes for rows (the budget L)
+};
+
+// Host-callable launchers (defined in lookup.hip).
+int launch_lookup(const LookupArgs& a, int G, bool f16, int grid, int lds_bytes, void* stream);
+int prepare_lookup_kernels(int lds_bytes);
+int launch_dedup_probe(const int64_t* idx, int n, int32_t* uniq, int32_t* inv, int32_t* n_uniq, void* stream);
+int launch_hot_probe(const int32_t* keys, const uint16_t* slots, int hash_log2, const int64_t* idx, int n,
+                     int32_t* slot, void* stream);
+int launch_fill(void* dst, int64_t row_begin, int64_t n_rows, int E, bool f16, int table_id, uint64_t seed,
+                double lo, double hi, int mode, void* stream);
+
+#if defined(__HIP__)
+#define EMBX_HD __host__ __device__
+#else
+#define EMBX_HD
+#endif
+
+// Hash of a hot row id into a table of 2^log2 entries (multiplicative, Knuth).
+EMBX_HD inline uint32_t hot_hash(uint32_t row, int log2) {
+  return (row * 0x9E3779B1u) >> (32 - log2);
+}
+
+}  // namespace embx

@@ -1,0 +1,206 @@
+"""GPU parity: the HIP path against the oracle, element by element, on small inputs
+that span several tiles, ragged tails and the method's degenerate cases."""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import index as OI
+from oracle import pool as OP
+
+from gpu_helpers import TOL, check_full, host_tables, log, plan_for, to_device, upload_tables
+
+pytestmark = pytest.mark.gpu
+
+STRATS = {"auto": -1, "lds": 0, "hot": 1, "dedup": 2, "gather": 3}
+MIXED_ROWS = [1, 7, 300, 512, 513, 2000, 50000, 300000]
+
+
+def mixed_config(cfg_id, E, dtype, B=97, pf_mean=4.0, pf_hi=12, rows=MIXED_ROWS):
+    tabs = []
+    for t, m in enumerate(rows):
+        dist = "zipf" if t % 2 == 0 else "uniform"
+        tabs.append(W.TableSpec(m, "poisson", pf_mean, 0, pf_hi, dist, 1.1))
+    c = W.Config(cfg_id, f"mixed E{E} {dtype}", E, dtype, -1.0, 1.0, B, tabs)
+    c.value_seeds = [W.value_seed(cfg_id, t) for t in range(c.T)]
+    return c
+
+
+def run(c, batch, weights_dev, force=None, B=None, **opts):
+    import torch
+    B = batch.B if B is None else B
+    if force is not None and force >= 0:
+        opts["force"] = [force] * c.T
+    p = plan_for(c, c.batch, **opts)
+    p.bind(weights_dev)
+    idx, off = to_device(batch)
+    out = torch.full((B, c.T, c.E), float("nan"), device="cuda")
+    p.lookup(idx, off, B, out)
+    torch.cuda.synchronize()
+    nbad = p.check_errors()
+    return p, out.cpu().numpy(), nbad
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2507_01676_amd as embx
+    return embx
+
+
+@pytest.mark.parametrize("E,dtype", [(64, "f32"), (128, "f16"), (32, "f32"), (256, "f32"), (96, "f32"),
+                                     (8, "f16"), (4, "f32")])
+@pytest.mark.parametrize("strat", list(STRATS))
+def test_integer_tables_bit_exact(gpu, E, dtype, strat):
+    log(f"integer tables E={E} {dtype} strategy={strat}")
+    c = mixed_config(101, E, dtype)
+    batch = W.gen_batch(c, 0)
+    hw = host_tables(c, W.VAL_INTEGER)
+    p, got, nbad = run(c, batch, upload_tables(hw), STRATS[strat])
+    check_full(got, hw, batch, dtype, exact=True)
+    assert nbad == 0
+    if strat != "auto":
+        assert p.info()["n_strategy"][strat.upper()] == p.info()["num_items"]
+
+
+@pytest.mark.parametrize("E,dtype", [(64, "f32"), (128, "f16")])
+@pytest.mark.parametrize("strat", list(STRATS))
+def test_uniform_tables_within_tolerance_and_deterministic(gpu, E, dtype, strat):
+    import torch
+    log(f"uniform tables E={E} {dtype} strategy={strat}")
+    c = mixed_config(102, E, dtype, B=301, pf_mean=9.0, pf_hi=40)
+    batch = W.gen_batch(c, 0)
+    hw = host_tables(c)
+    wd = upload_tables(hw)
+    p, got, nbad = run(c, batch, wd, STRATS[strat])
+    err, _ = check_full(got, hw, batch, dtype)
+    log(f"  pooled error {err:.2e}")
+    # a second launch (chunk counters must have been reset) gives the same bits
+    idx, off = to_device(batch)
+    out2 = p.lookup(idx, off, batch.B)
+    torch.cuda.synchronize()
+    assert np.array_equal(out2.cpu().numpy(), got)
+
+
+def test_chunked_lds_many_chunks_small_budget(gpu):
+    import torch
+    log("forced LDS with a 4 KiB budget: many row chunks and the chunk combine")
+    c = mixed_config(103, 64, "f32", B=200, pf_mean=6.0, pf_hi=20, rows=[5000, 40000, 3])
+    batch = W.gen_batch(c, 0)
+    hw = host_tables(c, W.VAL_INTEGER)
+    wd = upload_tables(hw)
+    p, got, _ = run(c, batch, wd, STRATS["lds"], lds_budget=4096)
+    txt = p.serialize()
+    assert max(int(ln.split()[5]) for ln in txt.splitlines() if ln.startswith("item ")) > 100
+    check_full(got, hw, batch, "f32", exact=True)
+    for _ in range(3):
+        idx, off = to_device(batch)
+        o = p.lookup(idx, off, batch.B)
+        torch.cuda.synchronize()
+        assert np.array_equal(o.cpu().numpy(), got)
+
+
+def test_out_of_range_indices_are_skipped_and_counted(gpu):
+    log("out-of-range and negative indices")
+    c = mixed_config(104, 64, "f32", B=64)
+    batch = W.gen_batch(c, 0)
+    g = np.random.default_rng(0)
+    pos = g.choice(batch.indices.size, size=40, replace=False)
+    bad_vals = np.array([-1, -(1 << 40), 1 << 33], dtype=np.int64)
+    batch.indices[pos] = bad_vals[g.integers(0, 3, size=40)]
+    t_of = np.searchsorted(batch.offsets, np.arange(batch.indices.size), side="right") - 1
+    edge = g.choice(batch.indices.size, size=10, replace=False)
+    for k in edge:                                  # exactly m (one past the end)
+        batch.indices[k] = c.rows[t_of[k] // batch.B]
+    hw = host_tables(c, W.VAL_INTEGER)
+    want_bad = OI.range_errors(batch.indices, batch.offsets, c.rows, batch.B)
+    for strat in STRATS:
+        p, got, nbad = run(c, batch, upload_tables(hw), STRATS[strat])
+        _, bad = check_full(got, hw, batch, "f32", exact=True)
+        assert nbad == bad == want_bad, (strat, nbad, want_bad)
+
+
+def test_edge_shapes(gpu):
+    import torch
+    log("B=1, T=1, m=1, index m-1, batch below max_batch, batch 0, unbound plan")
+    # single table of one row, one sample
+    c = mixed_config(105, 64, "f32", B=1, rows=[1])
+    batch = W.batch_from_bags(1, 1, [[0, 0, 0]])
+    hw = host_tables(c, W.VAL_INTEGER)
+    for strat in STRATS:
+        _, got, _ = run(c, batch, upload_tables(hw), STRATS[strat])
+        assert np.array_equal(got[0, 0], 3 * hw[0][0])
+    # last row of each table, and a batch smaller than the plan's max
+    c = mixed_config(106, 64, "f32", B=97)
+    hw = host_tables(c, W.VAL_INTEGER)
+    bags = [[m - 1] * (b % 3) for m in c.rows for b in range(50)]
+    batch = W.batch_from_bags(c.T, 50, bags)
+    for strat in STRATS:
+        _, got, _ = run(c, batch, upload_tables(hw), STRATS[strat], B=50)
+        check_full(got, hw, batch, "f32", exact=True)
+    # batch 0 is a no-op; lookup before binding weights is refused
+    import paper_2507_01676_amd as embx
+    p = plan_for(c, 97)
+    idx, off = to_device(batch)
+    with pytest.raises(embx.EmbxError) as e:
+        p.lookup(idx, off, 50)
+    assert e.value.code == embx.ERR_NOT_BOUND
+    p.bind(upload_tables(hw))
+    out = torch.full((1, c.T, c.E), 7.0, device="cuda")
+    p.lookup(idx, off, 0, out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+    big_off = torch.zeros(c.T * 98 + 1, dtype=torch.int64, device="cuda")
+    big_out = torch.empty((98, c.T, c.E), device="cuda")
+    with pytest.raises(embx.EmbxError) as e:
+        p.lookup(idx, big_off, 98, big_out)             # batch above the plan's max_batch
+    assert e.value.code == embx.ERR_INVALID_ARGUMENT
+
+
+def test_fixed_distribution_and_long_bags(gpu):
+    log("all indices equal (the paper's 'fixed' distribution) and bags longer than a dedup tile")
+    c = mixed_config(107, 64, "f32", B=97)
+    hw = host_tables(c, W.VAL_INTEGER)
+    bags = [[min(5, m - 1)] * 5 for m in c.rows for _ in range(97)]
+    batch = W.batch_from_bags(c.T, 97, bags)
+    for strat in STRATS:
+        _, got, _ = run(c, batch, upload_tables(hw), STRATS[strat])
+        check_full(got, hw, batch, "f32", exact=True)
+    g = np.random.default_rng(2)
+    lens = [0, 3000, 1, 2049, 2048, 0, 700, 5]
+    bags = [[int(x) for x in g.integers(0, m, size=lens[(t + b) % len(lens)])] for t, m in enumerate(c.rows)
+            for b in range(8)]
+    batch = W.batch_from_bags(c.T, 8, bags)
+    for strat in STRATS:
+        _, got, _ = run(c, batch, upload_tables(hw), STRATS[strat])
+        check_full(got, hw, batch, "f32", exact=True)
+
+
+@pytest.mark.parametrize("n", [0, 1, 2, 3, 100, 1000, 2047, 2048])
+def test_dedup_tile_matches_unique(gpu, n):
+    import torch
+    g = np.random.default_rng(n)
+    idx = W.zipf_ranks(g, 5000, 1.1, n) * 7919 % 2_000_000_000
+    d = torch.from_numpy(idx).cuda()
+    uniq, inv = gpu.dedup_tile(d)
+    u, i, _ = OI.dedup_tile(idx)
+    assert np.array_equal(uniq.cpu().numpy(), u)
+    assert np.array_equal(inv.cpu().numpy(), i)
+
+
+def test_hot_probe_matches_membership(gpu):
+    import torch
+    c = mixed_config(108, 64, "f32", B=200)
+    stats = W.history_stats(c, 200)
+    p = plan_for(c, 200, stats=stats, force=[1] * c.T)
+    C = {}
+    for ln in p.serialize().splitlines():
+        if ln.startswith("item "):
+            f = ln.split()
+            C[int(f[2])] = int(f[10])
+    g = np.random.default_rng(4)
+    for t in range(c.T):
+        idx = np.concatenate([stats[t].hot_rows[:50], g.integers(0, c.rows[t], size=3000)])
+        slot = p.hot_probe(t, torch.from_numpy(idx).cuda()).cpu().numpy()
+        want = OI.hot_slots(idx, stats[t].hot_rows[:C[t]])
+        assert np.array_equal(slot, want)

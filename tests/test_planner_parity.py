@@ -1,0 +1,105 @@
+"""The C++ planner inside libembx against the planner oracle, byte for byte (host only)."""
+import subprocess
+
+import numpy as np
+import pytest
+from hypothesis import HealthCheck, given, settings
+from hypothesis import strategies as st
+
+import workloads as W
+from oracle import plan as OPL
+
+from test_oracle_plan import _random_instance
+
+
+def _lib():
+    import paper_2507_01676_amd as embx
+    return embx
+
+
+def test_library_exports_every_declared_symbol():
+    embx = _lib()
+    import os
+    import re
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    declared = []
+    for h in ("embx.h", "embx_fill.h"):
+        src = open(os.path.join(root, "include", h)).read()
+        declared += re.findall(r"^(?:emb_status_t|const char\*)\s+(\w+)\(", src, flags=re.M)
+    assert len(declared) >= 12
+    out = subprocess.run(["nm", "-D", "--defined-only", embx.LIB_PATH], capture_output=True, text=True).stdout
+    names = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    missing = [d for d in declared if d not in names]
+    assert not missing, missing
+    assert set(declared) == set(embx.EXPORTED)
+    assert embx.status_string(embx.ERR_NOT_BOUND) == "weights not bound"
+
+
+def _both(rows, E, dtype, stats, B, K, opts: OPL.Options):
+    embx = _lib()
+    want = OPL.plan_reference(rows, E, dtype, stats, B, K, opts).text()
+    cst = [dict(mean_pooling=s.mean_pooling, max_pooling=s.max_pooling,
+                hot_rows=list(range(len(s.hot_freq))), hot_freq=list(s.hot_freq), unique_frac=s.unique_frac)
+           for s in stats]
+    got = embx.plan_text(rows, E, dtype, cst, B, K, lds_budget=opts.lds_budget, lif_milli=opts.lif_milli,
+                         chunk_max_bytes=opts.chunk_max_bytes, order_mode=opts.order_mode, beta=opts.beta,
+                         force=opts.force)
+    return got, want
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_cpp_planner_equals_oracle_random(seed):
+    rows, E, dtype, stats, B, K, opts = _random_instance(seed)
+    got, want = _both(rows, E, dtype, stats, B, K, opts)
+    assert got == want
+
+
+@settings(max_examples=80, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(st.integers(0, 10 ** 7), st.sampled_from([None, "skewbeta", "force"]))
+def test_cpp_planner_equals_oracle_hypothesis(seed, variant):
+    rows, E, dtype, stats, B, K, opts = _random_instance(seed)
+    g = np.random.default_rng(seed)
+    if variant == "skewbeta":
+        opts.beta = [float(x) for x in g.uniform(0.0, 5e4, size=OPL.NBETA)]
+        opts.chunk_max_bytes = int(g.choice([0, 4096, 32768]))
+    elif variant == "force":
+        f = []
+        for s in stats:
+            choices = [OPL.AUTO, OPL.LDS, OPL.DEDUP, OPL.GATHER] + ([OPL.HOT] if len(s.hot_freq) else [])
+            f.append(int(g.choice(choices)))
+        opts.force = f
+    try:
+        want = OPL.plan_reference(rows, E, dtype, stats, B, K, opts).text()
+    except OPL.PlanError:
+        embx = _lib()
+        with pytest.raises(embx.EmbxError):
+            _both(rows, E, dtype, stats, B, K, opts)
+        return
+    got, _ = _both(rows, E, dtype, stats, B, K, opts)
+    assert got == want
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_cpp_planner_equals_oracle_on_workloads(cfg):
+    c = W.make_config(cfg)
+    st_ = W.history_stats(c)
+    stats = [OPL.stats_from_workload(s) for s in st_]
+    for K in (256, 97):
+        got, want = _both(c.rows, c.E, c.dtype, stats, c.batch, K, OPL.Options())
+        assert got == want
+        assert want.count("\nitem ") >= K or K > 200
+
+
+def test_cpp_planner_rejects_what_the_oracle_rejects():
+    embx = _lib()
+    bad = [
+        ([0], 64, "f32", [OPL.Stat(1.0)]),
+        ([10], 6, "f32", [OPL.Stat(1.0)]),
+        ([10], 64, "f32", [OPL.Stat(float("nan"))]),
+        ([10], 64, "f32", [OPL.Stat(-1.0)]),
+    ]
+    for rows, E, dt, stats in bad:
+        with pytest.raises(OPL.PlanError):
+            OPL.plan_reference(rows, E, dt, stats, 8, 4)
+        with pytest.raises(embx.EmbxError):
+            embx.plan_text(rows, E, dt, [dict(mean_pooling=x.mean_pooling) for x in stats], 8, 4)

@@ -82,9 +82,9 @@ VAL_UNIFORM = 0     # uniform in [lo, hi)
 VAL_INTEGER = 1     # small integers that make every pooled sum exact
 
 
-def table_rows_block(t: int, r0: int, r1: int, E: int, dtype: str, *, seed: int,
-                     lo: float = -0.05, hi: float = 0.05, mode: int = VAL_UNIFORM) -> np.ndarray:
-    """Rows [r0, r1) of table t as an array [r1-r0, E] of ``dtype`` ('f32'|'f16').
+def table_rows_at(t: int, rows: np.ndarray, E: int, dtype: str, *, seed: int,
+                  lo: float = -0.05, hi: float = 0.05, mode: int = VAL_UNIFORM) -> np.ndarray:
+    """Rows ``rows`` (any row ids) of table t as an array [len(rows), E] of ``dtype`` ('f32'|'f16').
 
     key = (t << 40) | (r << 8) | c;  x = mix(key + seed * GOLDEN mod 2**64)
 
@@ -96,9 +96,9 @@ def table_rows_block(t: int, r0: int, r1: int, E: int, dtype: str, *, seed: int,
                  is an integer in [0, 2047], exact in fp16, and any sum of up to
                  8192 of them is exact in fp32.
     """
-    assert 0 <= r0 <= r1 and E <= 256 and t < (1 << 23)
-    n = r1 - r0
-    r = np.arange(r0, r1, dtype=np.uint64)[:, None]
+    assert E <= 256 and t < (1 << 23)
+    rr = np.asarray(rows, dtype=np.int64).reshape(-1)
+    r = rr.astype(np.uint64)[:, None]
     c = np.arange(E, dtype=np.uint64)[None, :]
     key = (np.uint64(t) << np.uint64(40)) | (r << np.uint64(8)) | c
     key = key + np.uint64((seed * GOLDEN) & M64)
@@ -112,7 +112,6 @@ def table_rows_block(t: int, r0: int, r1: int, E: int, dtype: str, *, seed: int,
         v = u.astype(np.float32)
     elif mode == VAL_INTEGER:
         v = (x >> np.uint64(53)).astype(np.float32)
-        rr = np.arange(r0, r1, dtype=np.int64)
         v[:, 0] = 1.0
         if E > 1:
             v[:, 1] = (rr & 2047).astype(np.float32)
@@ -127,7 +126,14 @@ def table_rows_block(t: int, r0: int, r1: int, E: int, dtype: str, *, seed: int,
     if dtype == "f16":
         return v.astype(np.float16)
     assert dtype == "f32"
-    return v.reshape(n, E)
+    return v
+
+
+def table_rows_block(t: int, r0: int, r1: int, E: int, dtype: str, *, seed: int,
+                     lo: float = -0.05, hi: float = 0.05, mode: int = VAL_UNIFORM) -> np.ndarray:
+    """Rows [r0, r1) of table t (see ``table_rows_at``)."""
+    assert 0 <= r0 <= r1
+    return table_rows_at(t, np.arange(r0, r1, dtype=np.int64), E, dtype, seed=seed, lo=lo, hi=hi, mode=mode)
 
 
 def materialize_table(t: int, rows: int, E: int, dtype: str, *, seed: int, lo: float = -0.05,
