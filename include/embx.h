@@ -153,6 +153,18 @@ emb_status_t emb_plan_serialize(const emb_plan_t* plan, char* buf, size_t cap, s
 
 emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info);
 
+/* Per-slice timers for fitting the cost model (Sec. III-A: the coefficients of Eq. (2) are
+ * fitted by least squares on hardware measurements).  With trace != NULL (device, at least
+ * *needed uint64 entries, 8-byte aligned) every following emb_lookup on this plan records
+ * 100 MHz real-time counter ticks:
+ *   worker w (w < K):  trace[w*18 + 0] start, [w*18 + 1] end of its staged slices,
+ *                      [w*18 + 2 + v] end of wavefront v (v < 16);
+ *   slice i in emb_plan_serialize order:  trace[K*18 + 2i] begin, [K*18 + 2i + 1] end
+ *                      (staged slices only; gather slices run merged per worker).
+ * Timed lookups add one workgroup barrier per staged slice.  trace == NULL switches the
+ * timers off; *needed (may be NULL) receives the required entry count either way. */
+emb_status_t emb_plan_set_trace(emb_plan_t* plan, uint64_t* trace, size_t capacity, size_t* needed);
+
 /* Frees the plan's device and host memory.  NULL is a no-op. */
 emb_status_t emb_plan_destroy(emb_plan_t* plan);
 

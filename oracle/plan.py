@@ -28,10 +28,14 @@ budget for rows):
       cost exceeds the sum of the chunk costs (the speed-up exceeds the number
       of chunks); chunks use the LDS strategy.
   P3  tau = ceil(sum of item costs / K), the ideal per-worker load.
-  P4  an item costing more than tau is batch-split k ways (symmetric
-      partitioning of Sec. III-A applied to that item, the paper's optional
+  P4  an item whose best strategy is GATHER is split k = min(K, B) ways
+      (symmetric partitioning, Sec. III-A: a gather slice stages nothing, so
+      every worker takes 1/k of every such table and the mix of cache-resident
+      and HBM-bound tables is the same on every worker).  Any other item
+      costing more than tau is batch-split k ways (the paper's optional
       replication): the smallest k in [2, min(K, B)] whose best cost is at most
-      max(tau, 2 x its fixed cost); all chunks of one table share one k.
+      max(tau, 2 x its fixed cost); all chunks of one table share one k.  A
+      split item keeps the strategy that is best at its k.
   P5  (paper step 2) slices sorted by (cost desc, s desc, m asc, t, chunk, j)
       -- longest-processing-time first with the paper's keys as tie-breaks --
       or, with order_mode 1, by the paper's literal key (s desc, m asc, t,
@@ -358,7 +362,10 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
         return tb.best(b, k)
 
     for g in groups:
-        ks = [1 if it.cost <= tau else split_k(it) for it in g]
+        if g[0].nchunks == 1 and g[0].strat == GATHER:
+            ks = [kmax]
+        else:
+            ks = [1 if it.cost <= tau else split_k(it) for it in g]
         k = max(ks)
         for it in g:
             s, cst, _ = _item_best(tabs[it.t], it, k)

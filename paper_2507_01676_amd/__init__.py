@@ -13,7 +13,7 @@ from typing import List, Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libembx.so")
+LIB_PATH = os.environ.get("EMBX_LIBRARY") or os.path.join(_HERE, "libembx.so")
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"embx native library missing: {LIB_PATH} (build it with: python paper_2507_01676_amd/build.py)")
@@ -31,7 +31,8 @@ MAX_HOT_STATS = 4096
 
 EXPORTED = ["emb_plan_create", "emb_plan_bind_weights", "emb_lookup", "emb_plan_check_errors",
             "emb_plan_serialize", "emb_plan_get_info", "emb_plan_destroy", "emb_plan_text",
-            "emb_status_string", "emb_debug_dedup_tile", "emb_debug_hot_probe", "embx_fill_table"]
+            "emb_status_string", "emb_debug_dedup_tile", "emb_debug_hot_probe", "embx_fill_table",
+            "emb_plan_set_trace"]
 
 
 class EmbxError(RuntimeError):
@@ -75,6 +76,7 @@ _lib.emb_plan_get_info.argtypes = [_vp, ctypes.POINTER(_Info)]
 _lib.emb_plan_destroy.argtypes = [_vp]
 _lib.emb_plan_text.argtypes = [_i32, ctypes.POINTER(_i64), _i32, _i32, ctypes.POINTER(_Stats), _i32, _i32,
                                ctypes.POINTER(_Opts), ctypes.c_char_p, _sz, ctypes.POINTER(_sz)]
+_lib.emb_plan_set_trace.argtypes = [_vp, _vp, _sz, ctypes.POINTER(_sz)]
 _lib.emb_debug_dedup_tile.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
 _lib.emb_debug_hot_probe.argtypes = [_vp, _i32, _vp, _i32, _vp, _vp]
 _lib.embx_fill_table.argtypes = [_vp, _i64, _i64, _i32, _i32, _i32, ctypes.c_uint64, ctypes.c_double,
@@ -222,6 +224,23 @@ class Plan:
     def lookup_ptr(self, indices_ptr: int, offsets_ptr: int, batch: int, out_ptr: int, stream_ptr) -> None:
         """Raw-pointer launch (benchmark loop)."""
         _check(_lib.emb_lookup(self._h, indices_ptr, offsets_ptr, int(batch), out_ptr, stream_ptr), "emb_lookup")
+
+    def set_trace(self, buf) -> int:
+        """Records per-slice timers into device uint64/int64 tensor ``buf`` (None: off).
+        Returns the number of entries the plan needs."""
+        n = _sz(0)
+        if buf is None:
+            _check(_lib.emb_plan_set_trace(self._h, None, 0, ctypes.byref(n)), "emb_plan_set_trace")
+            self._trace = None
+            return int(n.value)
+        _check(_lib.emb_plan_set_trace(self._h, buf.data_ptr(), buf.numel(), ctypes.byref(n)), "emb_plan_set_trace")
+        self._trace = buf
+        return int(n.value)
+
+    def trace_size(self) -> int:
+        n = _sz(0)
+        _lib.emb_plan_set_trace(self._h, None, 0, ctypes.byref(n))
+        return int(n.value)
 
     def check_errors(self, stream=None) -> int:
         n = _i64(0)

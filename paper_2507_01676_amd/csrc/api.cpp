@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <string>
@@ -37,6 +39,13 @@ struct emb_plan {
   int32_t* d_hot_ids = nullptr;
   int32_t* d_counters = nullptr;
   unsigned long long* d_err = nullptr;
+  GatherEntry* d_gq = nullptr;
+  int32_t* d_gq_ptr = nullptr;
+  int32_t* d_gq_chunks = nullptr;
+  GatherEntry* d_gqw = nullptr;
+  int32_t* d_gqw_ptr = nullptr;
+  int32_t* d_gqw_chunks = nullptr;
+  unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
 };
 
 namespace {
@@ -264,10 +273,65 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     d.hash_log2 = x.strat == S_HOT ? p->hot_table_log2[x.t] : 0;
     d.hot_off = x.strat == S_HOT ? p->hot_table_off[x.t] : 0;
     d.counter = x.nchunks > 1 ? ctr_base[x.t] + x.j : 0;
+    // long bags with few of them per slice: a wavefront per bag (not for DEDUP,
+    // whose row source is addressed by tile position)
+    const double s_t = stats[x.t].mean_pooling;
+    const int sw_per_wave = 64 / p->G;
+    const int64_t bags_per_slice = static_cast<int64_t>(max_batch) / x.k;
+    d.mode = (x.strat != S_DEDUP && s_t >= 4.0 * sw_per_wave && bags_per_slice <= 16 * (kBlock / 64)) ? 1 : 0;
+    d.wpf = static_cast<int16_t>(std::min(32767.0, std::max(1.0, std::floor(s_t + 0.5))));
     items.push_back(d);
     wg_ptr[x.wg + 1] += 1;
   }
   for (int w = 0; w < K; ++w) wg_ptr[w + 1] += wg_ptr[w];
+
+  // gather chunk queues per worker, slices in plan order.  SW-mode chunks carry about
+  // W / (4 NSW) expected lookups (W: the worker's SW-mode lookups at the max batch),
+  // at least one full step (8) and at most 32, so that each SW gets several chunks;
+  // wave-mode chunks carry about four wavefront steps of lookups.
+  std::vector<GatherEntry> gq, gqw;
+  std::vector<int32_t> gq_ptr(K + 1, 0), gq_chunks(K, 0), gqw_ptr(K + 1, 0), gqw_chunks(K, 0);
+  {
+    const int nsw = kBlock / p->G;
+    const double wave_chunk = 4.0 * 8.0 * (64 / p->G);
+    auto slice_bags = [&](const DevItem& d) -> int64_t {
+      return (static_cast<int64_t>(d.j + 1) * max_batch) / d.k - (static_cast<int64_t>(d.j) * max_batch) / d.k;
+    };
+    for (int w = 0; w < K; ++w) {
+      double W = 0.0;
+      for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i)
+        if (items[i].strat == S_GATHER && items[i].mode == 0)
+          W += static_cast<double>(slice_bags(items[i])) * std::max(1.0, stats[items[i].table].mean_pooling);
+      const double target = std::min(32.0, std::max(8.0, std::floor(W / (4.0 * nsw))));
+      gq_ptr[w] = static_cast<int32_t>(gq.size());
+      gqw_ptr[w] = static_cast<int32_t>(gqw.size());
+      int64_t base = 0, basew = 0;
+      for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
+        const DevItem& d = items[i];
+        if (d.strat != S_GATHER) continue;
+        const double s_t = std::max(1.0, stats[d.table].mean_pooling);
+        const int32_t cb = static_cast<int32_t>(std::max(1.0, std::floor((d.mode ? wave_chunk : target) / s_t)));
+        const int64_t nb = slice_bags(d);
+        const int64_t nc = (nb + cb - 1) / cb;
+        if (nc == 0) continue;
+        if (d.mode) {
+          gqw.push_back(GatherEntry{i, static_cast<int32_t>(basew), cb, 0});
+          basew += nc;
+        } else {
+          gq.push_back(GatherEntry{i, static_cast<int32_t>(base), cb, 0});
+          base += nc;
+        }
+      }
+      if (base > INT32_MAX || basew > INT32_MAX) {
+        delete p;
+        return EMB_ERR_UNSUPPORTED;
+      }
+      gq_chunks[w] = static_cast<int32_t>(base);
+      gqw_chunks[w] = static_cast<int32_t>(basew);
+    }
+    gq_ptr[K] = static_cast<int32_t>(gq.size());
+    gqw_ptr[K] = static_cast<int32_t>(gqw.size());
+  }
 
   // one metadata allocation
   size_t o_items = 0;
@@ -278,7 +342,13 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   size_t o_ids = align_up(o_slots + h_slots.size() * sizeof(uint16_t), 256);
   size_t o_ctr = align_up(o_ids + h_ids.size() * sizeof(int32_t), 256);
   size_t o_err = align_up(o_ctr + static_cast<size_t>(n_ctr) * sizeof(int32_t), 256);
-  size_t total = align_up(o_err + sizeof(unsigned long long), 256);
+  size_t o_gq = align_up(o_err + sizeof(unsigned long long), 256);
+  size_t o_gqp = align_up(o_gq + gq.size() * sizeof(GatherEntry), 256);
+  size_t o_gqn = align_up(o_gqp + gq_ptr.size() * sizeof(int32_t), 256);
+  size_t o_gqw = align_up(o_gqn + gq_chunks.size() * sizeof(int32_t), 256);
+  size_t o_gqwp = align_up(o_gqw + gqw.size() * sizeof(GatherEntry), 256);
+  size_t o_gqwn = align_up(o_gqwp + gqw_ptr.size() * sizeof(int32_t), 256);
+  size_t total = align_up(o_gqwn + gqw_chunks.size() * sizeof(int32_t), 256);
   if (hipMalloc(&p->d_meta, total) != hipSuccess) {
     delete p;
     return EMB_ERR_OUT_OF_MEMORY;
@@ -296,6 +366,12 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   p->d_hot_ids = reinterpret_cast<int32_t*>(p->d_meta + o_ids);
   p->d_counters = reinterpret_cast<int32_t*>(p->d_meta + o_ctr);
   p->d_err = reinterpret_cast<unsigned long long*>(p->d_meta + o_err);
+  p->d_gq = reinterpret_cast<GatherEntry*>(p->d_meta + o_gq);
+  p->d_gq_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_gqp);
+  p->d_gq_chunks = reinterpret_cast<int32_t*>(p->d_meta + o_gqn);
+  p->d_gqw = reinterpret_cast<GatherEntry*>(p->d_meta + o_gqw);
+  p->d_gqw_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_gqwp);
+  p->d_gqw_chunks = reinterpret_cast<int32_t*>(p->d_meta + o_gqwn);
   std::vector<char> host(total, 0);
   if (!items.empty()) std::memcpy(host.data() + o_items, items.data(), items.size() * sizeof(DevItem));
   std::memcpy(host.data() + o_wg, wg_ptr.data(), wg_ptr.size() * sizeof(int32_t));
@@ -305,6 +381,12 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     std::memcpy(host.data() + o_slots, h_slots.data(), h_slots.size() * sizeof(uint16_t));
     std::memcpy(host.data() + o_ids, h_ids.data(), h_ids.size() * sizeof(int32_t));
   }
+  if (!gq.empty()) std::memcpy(host.data() + o_gq, gq.data(), gq.size() * sizeof(GatherEntry));
+  std::memcpy(host.data() + o_gqp, gq_ptr.data(), gq_ptr.size() * sizeof(int32_t));
+  std::memcpy(host.data() + o_gqn, gq_chunks.data(), gq_chunks.size() * sizeof(int32_t));
+  if (!gqw.empty()) std::memcpy(host.data() + o_gqw, gqw.data(), gqw.size() * sizeof(GatherEntry));
+  std::memcpy(host.data() + o_gqwp, gqw_ptr.data(), gqw_ptr.size() * sizeof(int32_t));
+  std::memcpy(host.data() + o_gqwn, gqw_chunks.data(), gqw_chunks.size() * sizeof(int32_t));
   if (hipMemcpy(p->d_meta, host.data(), total, hipMemcpyHostToDevice) != hipSuccess ||
       (p->d_partials && hipMemset(p->d_partials, 0, part_floats * sizeof(float)) != hipSuccess)) {
     emb_plan_destroy(p);
@@ -361,6 +443,14 @@ emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t*
   a.E = plan->E;
   a.R = plan->R;
   a.lds_rows = plan->lds_rows;
+  a.n_items = static_cast<int32_t>(plan->plan.slices.size());
+  a.trace = plan->d_trace;
+  a.gq = plan->d_gq;
+  a.gq_ptr = plan->d_gq_ptr;
+  a.gq_chunks = plan->d_gq_chunks;
+  a.gqw = plan->d_gqw;
+  a.gqw_ptr = plan->d_gqw_ptr;
+  a.gqw_chunks = plan->d_gqw_chunks;
   return st(launch_lookup(a, plan->G, plan->f16, plan->K, plan->lds_bytes, stream));
 }
 
@@ -372,6 +462,19 @@ emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_ba
   if (v != 0 && hipMemset(plan->d_err, 0, sizeof v) != hipSuccess) return EMB_ERR_DEVICE;
   if (n_bad) *n_bad = static_cast<int64_t>(v);
   return v ? EMB_ERR_INDEX_OUT_OF_RANGE : EMB_OK;
+}
+
+emb_status_t emb_plan_set_trace(emb_plan_t* plan, uint64_t* trace, size_t capacity, size_t* needed) {
+  if (!plan) return EMB_ERR_INVALID_ARGUMENT;
+  const size_t need = static_cast<size_t>(plan->K) * kTraceWorker + 2 * plan->plan.slices.size();
+  if (needed) *needed = need;
+  if (!trace) {
+    plan->d_trace = nullptr;
+    return EMB_OK;
+  }
+  if (capacity < need || (reinterpret_cast<uintptr_t>(trace) & 7u) != 0) return EMB_ERR_INVALID_ARGUMENT;
+  plan->d_trace = reinterpret_cast<unsigned long long*>(trace);
+  return EMB_OK;
 }
 
 emb_status_t emb_plan_serialize(const emb_plan_t* plan, char* buf, size_t cap, size_t* len_out) {

@@ -22,7 +22,8 @@ struct DevItem {
   int32_t hash_log2;    // HOT: log2 of the hash size
   int64_t hot_off;      // HOT: element offset of this table's hash / hot ids
   int32_t counter;      // chunked: combine counter of (table, j)
-  int32_t pad;
+  int16_t mode;         // 0: each sub-wavefront sums whole bags; 1: a wavefront per bag
+  int16_t wpf;          // expected lookups per bag (>= 1): weight of a bag in the gather split
 };
 
 struct DevTable {
@@ -30,6 +31,15 @@ struct DevTable {
   int64_t rows;
   int64_t part_base;    // chunked tables: float offset of the [nchunks, Bmax, E] partial slab
   int32_t nchunks;
+  int32_t pad;
+};
+
+// One gather slice in a worker's chunk queue: the queue's chunks from chunk_base on
+// are runs of `cb` bags of item `item` (counted at the plan's max batch).
+struct GatherEntry {
+  int32_t item;
+  int32_t chunk_base;
+  int32_t cb;
   int32_t pad;
 };
 
@@ -52,7 +62,22 @@ struct LookupArgs {
   int32_t E;
   int32_t R;                    // row bytes
   int32_t lds_rows;             // LDS bytes for rows (the budget L)
+  int32_t n_items;
+  unsigned long long* trace;    // optional timers (see kTraceWorker), nullptr = off
+  const GatherEntry* gq;        // SW-mode gather chunk queues, worker-major
+  const int32_t* gq_ptr;        // [K + 1] entry ranges per worker
+  const int32_t* gq_chunks;     // [K] chunks per worker
+  const GatherEntry* gqw;       // wave-mode gather chunk queues
+  const int32_t* gqw_ptr;
+  const int32_t* gqw_chunks;
 };
+
+// Timer layout (100 MHz real-time counter ticks):
+//   worker w:  trace[w * kTraceWorker + 0]      start
+//              trace[w * kTraceWorker + 1]      end of the staged slices
+//              trace[w * kTraceWorker + 2 + v]  end of wavefront v
+//   slice i:   trace[K * kTraceWorker + 2 i + {0, 1}]  begin / end (staged slices)
+constexpr int kTraceWorker = 2 + kBlock / 64;
 
 // Host-callable launchers (defined in lookup.hip).
 int launch_lookup(const LookupArgs& a, int G, bool f16, int grid, int lds_bytes, void* stream);

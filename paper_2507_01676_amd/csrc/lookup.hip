@@ -5,27 +5,43 @@
 // sub-wavefront (SW) of G = (row bytes)/16 lanes rounded up to a power of two:
 // lane l of a SW covers bytes [16 l, 16 l + 16) of a row, so one SW moves one
 // row per 16-byte load (global_load_dwordx4 from HBM or ds_read_b128 from LDS).
-// A SW walks the lookups of a contiguous run of bags in index order, issuing
-// kU independent row loads before it sums any of them, and keeps one bag's fp32
-// partial sum in registers (4 values per lane for fp32 rows, 8 for fp16 rows).
-// Each bag is therefore summed by one SW in index order: results are bitwise
-// reproducible run to run.
+//
+// Two ways to cover a slice's bags:
+//   SW mode    each SW sums a contiguous run of whole bags, walking their lookups
+//              in index order with kU independent row loads in flight;
+//   wave mode  (long bags, few per slice) the S = 64/G SWs of a wavefront take the
+//              lookups of one bag in turn (SW s: positions s, s+S, ...) and their
+//              partial sums are combined by cross-lane butterflies, in a fixed order.
+// Either way every output element is produced by one fixed sequence of fp32
+// additions: results are bitwise reproducible run to run.
 //
 // Data flows per slice (Sec. II-B, re-targeted at a CU):
 //   LDS    the table, or a row chunk of it (Sec. III-B), is staged into LDS once
 //          per launch; chunk partial sums land in a workspace and the last chunk
-//          worker to finish sums them in chunk order (deterministic stand-in for
+//          worker to finish sums them in chunk order (a deterministic stand-in for
 //          the paper's atomic inter-core accumulation);
 //   HOT    the hottest rows are staged into LDS behind an open-addressing hash of
 //          their ids held in LDS; hits read LDS, misses read HBM;
 //   DEDUP  a tile of up to kTile lookups is bitonic-sorted in LDS, each distinct
 //          row is fetched once into LDS, and the bags read their rows from there;
-//   GATHER rows straight from HBM; the worker's gather slices are flattened and
-//          split evenly over all its SWs.
+//   GATHER rows straight from HBM; a worker's gather slices are flattened and
+//          split over its SWs (or wavefronts) by expected lookups.
+//
+// All pointers carry their address space (1 = global, 3 = LDS) so that every
+// access compiles to a global_* or ds_* instruction, never a flat one.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
 #include "device_types.hpp"
+
+// address spaces exist in the device pass only; the host pass sees plain pointers
+#if defined(__HIP_DEVICE_COMPILE__)
+#define GMEM __attribute__((address_space(1)))
+#define LMEM __attribute__((address_space(3)))
+#else
+#define GMEM
+#define LMEM
+#endif
 
 namespace embx {
 namespace {
@@ -44,6 +60,14 @@ constexpr int kMetaBytes = kMetaScan + 256;
 static_assert(kMetaBytes == kMetaReserve, "LDS metadata layout");
 constexpr int kMetaHashKeys = 0;                      // HOT: int32[H], H <= 4096
 constexpr int kMetaHashSlots = 4096 * 4;              // HOT: uint16[H]
+
+using gchar = GMEM const char;
+using lchar = LMEM char;
+
+template <class T>
+__device__ __forceinline__ GMEM T* as_global(T* p) {
+  return (GMEM T*)p;
+}
 
 template <bool F16>
 struct Acc {
@@ -72,38 +96,38 @@ __device__ __forceinline__ void acc_add(Acc<true>& a, const uint4 r) {
   }
 }
 
-__device__ __forceinline__ void acc_add_f32(Acc<false>& a, const float* p) {
-  const float4 x = *reinterpret_cast<const float4*>(p);
-  a.v[0] += x.x;
-  a.v[1] += x.y;
-  a.v[2] += x.z;
-  a.v[3] += x.w;
+template <bool F16>
+__device__ __forceinline__ void acc_add_f32(Acc<F16>& a, GMEM const float* p) {
+#pragma unroll
+  for (int h = 0; h < (F16 ? 2 : 1); ++h) {
+    const float4 x = *reinterpret_cast<GMEM const float4*>(p + 4 * h);
+    a.v[4 * h + 0] += x.x;
+    a.v[4 * h + 1] += x.y;
+    a.v[4 * h + 2] += x.z;
+    a.v[4 * h + 3] += x.w;
+  }
 }
 
-__device__ __forceinline__ void acc_add_f32(Acc<true>& a, const float* p) {
-  const float4 x = *reinterpret_cast<const float4*>(p);
-  const float4 y = *reinterpret_cast<const float4*>(p + 4);
-  a.v[0] += x.x;
-  a.v[1] += x.y;
-  a.v[2] += x.z;
-  a.v[3] += x.w;
-  a.v[4] += y.x;
-  a.v[5] += y.y;
-  a.v[6] += y.z;
-  a.v[7] += y.w;
+template <bool F16>
+__device__ __forceinline__ void acc_store(GMEM float* p, const Acc<F16>& a) {
+#pragma unroll
+  for (int h = 0; h < (F16 ? 2 : 1); ++h)
+    *reinterpret_cast<GMEM float4*>(p + 4 * h) = make_float4(a.v[4 * h], a.v[4 * h + 1], a.v[4 * h + 2], a.v[4 * h + 3]);
 }
 
-__device__ __forceinline__ void acc_store(float* p, const Acc<false>& a) {
-  *reinterpret_cast<float4*>(p) = make_float4(a.v[0], a.v[1], a.v[2], a.v[3]);
+// sum of the S = 64/G sub-wavefront partials of a wavefront (xor butterflies)
+template <int G, bool F16>
+__device__ __forceinline__ void acc_wave_reduce(Acc<F16>& a) {
+#pragma unroll
+  for (int d = G; d < kWave; d <<= 1) {
+#pragma unroll
+    for (int i = 0; i < (F16 ? 8 : 4); ++i) a.v[i] += __shfl_xor(a.v[i], d);
+  }
 }
 
-__device__ __forceinline__ void acc_store(float* p, const Acc<true>& a) {
-  *reinterpret_cast<float4*>(p) = make_float4(a.v[0], a.v[1], a.v[2], a.v[3]);
-  *reinterpret_cast<float4*>(p + 4) = make_float4(a.v[4], a.v[5], a.v[6], a.v[7]);
-}
-
-__device__ __forceinline__ uint4 ld16(const char* p) { return *reinterpret_cast<const uint4*>(p); }
-__device__ __forceinline__ void st16(char* p, const uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+__device__ __forceinline__ uint4 ldg16(gchar* p) { return *reinterpret_cast<GMEM const uint4*>(p); }
+__device__ __forceinline__ uint4 lds16(const lchar* p) { return *reinterpret_cast<LMEM const uint4*>(p); }
+__device__ __forceinline__ void sts16(lchar* p, const uint4 v) { *reinterpret_cast<LMEM uint4*>(p) = v; }
 __device__ __forceinline__ uint4 zero16() { return make_uint4(0u, 0u, 0u, 0u); }
 
 __device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
@@ -114,63 +138,85 @@ __device__ __forceinline__ int slice_lo(int j, int k, int B) {
 }
 
 // ---------------------------------------------------------------- row sources
+// Every step of a walker issues all of its loads unconditionally (invalid ids read
+// row 0, lanes beyond the row read the row's first 16 bytes) and applies validity
+// only when the values are used.  With no branches around loads, the compiler can
+// keep a step to a single wait on the memory counter.
+
+// Waits until every memory operation this wavefront issued has completed.
+__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
+
+// A run of bags [bs, be) of one table.
+struct Seg {
+  gchar* w;
+  uint64_t rows;
+  GMEM const int64_t* off;   // the table's CSR offsets
+  GMEM float* ob;            // out + table * E (or a chunk's partial-sum slab)
+  int bs, be;
+};
 
 struct RowBase {
-  const char* w;          // table base (HBM)
+  gchar* w;               // table base (HBM)
   uint64_t rows;
   int R;
-  int lane_off;           // 16 * lane-in-SW
+  int lane_c;             // this lane's byte offset in a row (0 for lanes beyond the row)
   bool active;            // this lane holds part of the row
-  bool lead;              // lane 0 of the SW (reports errors)
-  unsigned long long* err;
+  bool count;             // this slice reports out-of-range ids
+  GMEM unsigned long long* err;
 
-  __device__ __forceinline__ uint4 hbm(int64_t ix) const {
-    return active ? ld16(w + ix * R + lane_off) : zero16();
+  __device__ __forceinline__ gchar* row(int32_t ix) const {
+    return w + static_cast<int64_t>(ix > 0 ? ix : 0) * R + lane_c;
   }
   __device__ __forceinline__ void bad() const {
-    if (lead) atomicAdd(err, 1ull);
+    if (count) atomicAdd(err, 1ull);
+  }
+  __device__ __forceinline__ void bind(const Seg& s) {
+    w = s.w;
+    rows = s.rows;
   }
 };
 
 struct FGather : RowBase {
-  __device__ __forceinline__ void probe(const int64_t (&)[kU], int64_t, int, int32_t (&)[kU]) const {}
-  __device__ __forceinline__ uint4 fetch(int64_t ix, int32_t) const {
-    if (static_cast<uint64_t>(ix) < rows) return hbm(ix);
-    bad();
-    return zero16();
+  static constexpr bool kPositional = false;
+  using Raw = uint4;
+  __device__ __forceinline__ void probe(const int32_t (&)[kU], int64_t, int, int32_t (&)[kU]) const {}
+  __device__ __forceinline__ void issue(int32_t ix, int32_t, Raw& r) const { r = ldg16(row(ix)); }
+  __device__ __forceinline__ uint4 take(int32_t ix, int32_t, const Raw& r) const {
+    return (ix >= 0 && active) ? r : zero16();
   }
 };
 
-// rows [r0, r1) of the table resident in LDS at `lds`; others contribute nothing
+// rows [r0, r1) of the table resident in LDS at `lds`; others contribute nothing here
 struct FLds : RowBase {
-  const char* lds;
-  int64_t r0, r1;
-  bool count;             // this slice reports out-of-range ids (chunk 0 only)
-  __device__ __forceinline__ void probe(const int64_t (&)[kU], int64_t, int, int32_t (&)[kU]) const {}
-  __device__ __forceinline__ uint4 fetch(int64_t ix, int32_t) const {
-    if (ix >= r0 && ix < r1) return active ? ld16(lds + (ix - r0) * R + lane_off) : zero16();
-    if (count && static_cast<uint64_t>(ix) >= rows) bad();
-    return zero16();
+  static constexpr bool kPositional = false;
+  using Raw = uint4;
+  const lchar* lds;
+  int32_t r0, r1;
+  __device__ __forceinline__ bool in(int32_t ix) const { return ix >= r0 && ix < r1; }
+  __device__ __forceinline__ void probe(const int32_t (&)[kU], int64_t, int, int32_t (&)[kU]) const {}
+  __device__ __forceinline__ void issue(int32_t ix, int32_t, Raw& r) const {
+    r = lds16(lds + static_cast<int64_t>(in(ix) ? ix - r0 : 0) * R + lane_c);
+  }
+  __device__ __forceinline__ uint4 take(int32_t ix, int32_t, const Raw& r) const {
+    return (in(ix) && active) ? r : zero16();
   }
 };
 
 // open-addressing hash of the hot ids (key -1 = empty slot), linear probing
-__device__ __forceinline__ void hot_probe_batch(const int32_t* keys, const uint16_t* slots, int hb,
-                                                const int64_t (&ix)[kU], int n, uint64_t rows,
-                                                int32_t (&sl)[kU]) {
+__device__ __forceinline__ void hot_probe_batch(const LMEM int32_t* keys, const LMEM uint16_t* slots, int hb,
+                                                const int32_t (&ix)[kU], int n, int32_t (&sl)[kU]) {
   const uint32_t mask = (1u << hb) - 1u;
   uint32_t h[kU];
   int32_t k[kU];
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
-    const bool ok = u < n && static_cast<uint64_t>(ix[u]) < rows;
+    const bool ok = u < n && ix[u] >= 0;
     h[u] = ok ? hot_hash(static_cast<uint32_t>(ix[u]), hb) : 0u;
     k[u] = ok ? keys[h[u]] : -1;
   }
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
-    const int32_t want = static_cast<int32_t>(ix[u]);
-    while (k[u] >= 0 && k[u] != want) {
+    while (k[u] >= 0 && k[u] != ix[u]) {
       h[u] = (h[u] + 1u) & mask;
       k[u] = keys[h[u]];
     }
@@ -178,121 +224,331 @@ __device__ __forceinline__ void hot_probe_batch(const int32_t* keys, const uint1
   }
 }
 
+struct Pair16 {
+  uint4 l, g;
+};
+
+// hot rows in LDS (slot order) behind the id hash; misses read HBM
 struct FHot : RowBase {
-  const char* lds;        // hot rows in slot order
-  const int32_t* keys;
-  const uint16_t* slots;
+  static constexpr bool kPositional = false;
+  using Raw = Pair16;
+  const lchar* lds;
+  const LMEM int32_t* keys;
+  const LMEM uint16_t* slots;
   int hb;
-  __device__ __forceinline__ void probe(const int64_t (&ix)[kU], int64_t, int n, int32_t (&sl)[kU]) const {
-    hot_probe_batch(keys, slots, hb, ix, n, rows, sl);
+  __device__ __forceinline__ void probe(const int32_t (&ix)[kU], int64_t, int n, int32_t (&sl)[kU]) const {
+    hot_probe_batch(keys, slots, hb, ix, n, sl);
   }
-  __device__ __forceinline__ uint4 fetch(int64_t ix, int32_t sl) const {
-    if (static_cast<uint64_t>(ix) >= rows) {
-      bad();
-      return zero16();
-    }
-    if (sl >= 0) return active ? ld16(lds + static_cast<int64_t>(sl) * R + lane_off) : zero16();
-    return hbm(ix);
+  __device__ __forceinline__ void issue(int32_t ix, int32_t sl, Raw& r) const {
+    r.l = lds16(lds + static_cast<int64_t>(sl > 0 ? sl : 0) * R + lane_c);
+    r.g = ldg16(row(sl < 0 ? ix : 0));
+  }
+  __device__ __forceinline__ uint4 take(int32_t ix, int32_t sl, const Raw& r) const {
+    if (ix < 0 || !active) return zero16();
+    return sl >= 0 ? r.l : r.g;
   }
 };
 
+// a tile's distinct rows in LDS (first capd of them, slot order); the rest read HBM
 struct FDedup : RowBase {
-  const char* lds;        // the tile's distinct rows in slot order (first capd of them)
-  const int16_t* inv;     // slot of each tile position, -1 for an invalid id
+  static constexpr bool kPositional = true;   // probes by position in the tile
+  using Raw = Pair16;
+  const lchar* lds;
+  const LMEM int16_t* inv;  // slot of each tile position, -1 for an invalid id
   int64_t P0;             // first lookup of the tile
   int capd;
-  __device__ __forceinline__ void probe(const int64_t (&)[kU], int64_t p, int n, int32_t (&sl)[kU]) const {
+  __device__ __forceinline__ void probe(const int32_t (&)[kU], int64_t p, int n, int32_t (&sl)[kU]) const {
 #pragma unroll
     for (int u = 0; u < kU; ++u) sl[u] = u < n ? static_cast<int32_t>(inv[p + u - P0]) : -1;
   }
-  __device__ __forceinline__ uint4 fetch(int64_t ix, int32_t sl) const {
-    if (static_cast<uint64_t>(ix) >= rows) {
-      bad();
-      return zero16();
-    }
-    if (sl >= 0 && sl < capd) return active ? ld16(lds + static_cast<int64_t>(sl) * R + lane_off) : zero16();
-    return hbm(ix);
+  __device__ __forceinline__ bool in_lds(int32_t sl) const { return sl >= 0 && sl < capd; }
+  __device__ __forceinline__ void issue(int32_t ix, int32_t sl, Raw& r) const {
+    r.l = lds16(lds + static_cast<int64_t>(in_lds(sl) ? sl : 0) * R + lane_c);
+    r.g = ldg16(row(in_lds(sl) ? 0 : ix));
+  }
+  __device__ __forceinline__ uint4 take(int32_t ix, int32_t sl, const Raw& r) const {
+    if (ix < 0 || !active) return zero16();
+    return in_lds(sl) ? r.l : r.g;
   }
 };
 
-// ---------------------------------------------------------------- the bag walker
+// The kU upcoming lookups of a SW are loaded one per lane (IPL per lane when the SW
+// has fewer than kU lanes): position u sits in lane u % G, slot u / G.  Positions past
+// the end read `safe` (a valid position) and are marked invalid; validity is applied
+// when the ids are resolved.  Each lane checks its own ids against the table (an
+// invalid id is counted once, by the lane that loaded it), then the SW broadcasts the
+// validated 32-bit ids with shuffles.
+template <int G>
+struct Ids {
+  static constexpr int IPL = G >= kU ? 1 : kU / G;
+  int64_t raw[IPL];
+  uint32_t ok_bits;
 
-// One SW sums bags [bs, be) of one table (bag b = lookups off[b] .. off[b+1]) into
-// obase + b * ostride.  The SW's lanes cache the ends of the next G bags (one
-// coalesced load per G bags) and read them back with a shuffle.
-template <int G, bool F16, class F>
-__device__ __forceinline__ void walk(const int64_t* __restrict__ indices, const int64_t* __restrict__ off,
-                                     int bs, int be, float* __restrict__ obase, int64_t ostride, int lane_sw,
-                                     const F& f) {
-  if (bs >= be) return;
-  constexpr int NA = F16 ? 8 : 4;
-  int64_t p = off[bs];
-  const int64_t pend = off[be];
-  int wb = bs;
-  int64_t win = off[min(bs + 1 + lane_sw, be)];
-  int b = bs;
-  auto end_of = [&](int bb) -> int64_t {
-    if (bb - wb >= G) {
-      wb = bb;
-      win = off[min(bb + 1 + lane_sw, be)];
+  // positions first + stride * u for u < kU, below end
+  __device__ __forceinline__ void load(GMEM const int64_t* __restrict__ indices, int64_t first, int64_t stride,
+                                       int64_t end, int64_t safe, int lane_sw) {
+    ok_bits = 0;
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) {
+      const int u = lane_sw + j * G;
+      const int64_t pos = first + stride * u;
+      const bool ok = u < kU && pos < end;
+      raw[j] = indices[ok ? pos : safe];
+      ok_bits |= (ok ? 1u : 0u) << j;
     }
-    return __shfl(win, bb - wb, G);
+  }
+
+  template <class F>
+  __device__ __forceinline__ void resolve(const F& f, int lane_sw, int32_t (&ix)[kU]) const {
+    int32_t mine[IPL];
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) {
+      const bool in_range = (ok_bits >> j) & 1u;
+      const bool ok = static_cast<uint64_t>(raw[j]) < f.rows;
+      mine[j] = (in_range && ok) ? static_cast<int32_t>(raw[j]) : -1;
+      if (in_range && !ok) f.bad();
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) ix[u] = G == 1 ? mine[u] : __shfl(mine[u / G], u % G, G);
+  }
+};
+
+// ---------------------------------------------------------------- SW mode
+
+template <int G>
+struct SegPre {   // a segment's first loads, issued one segment ahead
+  int64_t p, pend, win, win_next;
+  __device__ __forceinline__ void issue(const Seg& s, int lane_sw) {
+    p = s.off[s.bs];
+    pend = s.off[s.be];
+    win = s.off[min(s.bs + 1 + lane_sw, s.be)];
+    win_next = s.off[min(s.bs + 1 + G + lane_sw, s.be)];
+  }
+};
+
+struct OneSeg {   // a segment source with a single segment
+  Seg s;
+  bool done;
+  __device__ __forceinline__ bool next(Seg& o) {
+    if (done) return false;
+    o = s;
+    done = true;
+    return true;
+  }
+};
+
+// One SW sums the bags of a sequence of segments (src.next yields them in order) into
+// seg.ob + b * ostride, each bag in index order.  A step: resolve the kU ids loaded by
+// the previous step, issue the kU row loads, the next step's index loads and the
+// offsets window ahead, then wait once and add the rows (storing each bag as it ends).
+// The lanes of the SW hold the ends of 2G bags; the offsets of the next segment are
+// loaded while the current one is walked.
+template <int G, bool F16, class F, class Src>
+__device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indices, int64_t ostride, int lane_sw,
+                                         F& f, Src& src) {
+  constexpr int NA = F16 ? 8 : 4;
+  Seg cur, nxt;
+  if (!src.next(cur)) return;
+  SegPre<G> cs, ns;
+  cs.issue(cur, lane_sw);
+  bool has_nxt = src.next(nxt);
+  if (has_nxt) ns.issue(nxt, lane_sw);
+  while (true) {
+    f.bind(cur);
+    GMEM const int64_t* const off = cur.off;
+    const int be = cur.be;
+    wait_all();
+    const int64_t pend = cs.pend;
+    int64_t p = cs.p;
+    Ids<G> ids;
+    ids.ok_bits = 0;
+    if (p < pend) ids.load(indices, p, 1, pend, p, lane_sw);
+    int wb = cur.bs, b = cur.bs;
+    int64_t win = cs.win, win2 = cs.win_next;
+    wait_all();
+    auto end_of = [&](int bb) -> int64_t {
+      const int d = bb - wb;
+      if (d < G) return __shfl(win, d, G);
+      if (d < 2 * G) return __shfl(win2, d - G, G);
+      return off[min(bb + 1, be)];   // more than G empty bags within one step
+    };
+    int64_t bag_end = end_of(b);
+    Acc<F16> acc;
+    acc_zero(acc);
+    GMEM float* const ob = cur.ob + lane_sw * NA;
+    while (p < pend) {
+      const int n = static_cast<int>(min64(kU, pend - p));
+      int32_t ix[kU];
+      ids.resolve(f, lane_sw, ix);
+      int32_t sl[kU];
+      f.probe(ix, p, n, sl);
+      typename F::Raw raw[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) f.issue(ix[u], sl[u], raw[u]);
+      const int64_t pn = p + n;
+      ids.load(indices, pn, 1, pend, p, lane_sw);
+      win2 = off[min(wb + G + 1 + lane_sw, be)];
+      wait_all();   // the one wait of the step: rows, next ids and offsets window together
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        if (u < n) {
+          while (p + u == bag_end) {
+            if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+            acc_zero(acc);
+            ++b;
+            bag_end = end_of(b);
+          }
+          acc_add(acc, f.take(ix[u], sl[u], raw[u]));
+        }
+      }
+      if (b - wb >= G) {
+        if (b - wb < 2 * G) {
+          wb += G;
+          win = win2;
+        } else {
+          wb = b;
+          win = off[min(b + 1 + lane_sw, be)];
+        }
+      }
+      p = pn;
+    }
+    for (; b < be; ++b) {
+      if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+      acc_zero(acc);
+    }
+    if (!has_nxt) break;
+    cur = nxt;
+    cs = ns;
+    has_nxt = src.next(nxt);
+    if (has_nxt) ns.issue(nxt, lane_sw);
+  }
+}
+
+// SW mode over one range of bags of one table
+template <int G, bool F16, class F>
+__device__ __forceinline__ void walk(GMEM const int64_t* __restrict__ indices, GMEM const int64_t* __restrict__ off,
+                                     int bs, int be, GMEM float* __restrict__ obase, int64_t ostride, int lane_sw,
+                                     F& f) {
+  if (bs >= be) return;
+  OneSeg src;
+  src.s.w = f.w;
+  src.s.rows = f.rows;
+  src.s.off = off;
+  src.s.ob = obase;
+  src.s.bs = bs;
+  src.s.be = be;
+  src.done = false;
+  walk_seq<G, F16>(indices, ostride, lane_sw, f, src);
+}
+
+// ---------------------------------------------------------------- wave mode
+
+__device__ __forceinline__ int64_t lane_i64(int64_t v, int lane) {
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(v & 0xffffffff), lane);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(v >> 32), lane);
+  return (static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+}
+
+// One wavefront sums bags [bs, be) one after the other: a step covers S * kU
+// consecutive lookups of the bag, SW s taking positions s, s + S, ... of it; the S
+// partial sums are combined across lanes when the bag ends and SW 0 stores it.  The
+// wavefront holds the ends of 64 bags in its lanes (the next 64 prefetched every
+// step), and each step issues the next step's index loads (possibly of the next bag)
+// before it waits once and sums its rows.
+template <int G, bool F16, class F>
+__device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indices,
+                                          GMEM const int64_t* __restrict__ off, int bs, int be,
+                                          GMEM float* __restrict__ obase, int64_t ostride, int lane_sw, int sw_w,
+                                          F& f) {
+  static_assert(!F::kPositional, "wave mode needs a position-free row source");
+  constexpr int S = kWave / G;
+  constexpr int NA = F16 ? 8 : 4;
+  if (bs >= be) return;
+  const int lane = threadIdx.x & (kWave - 1);
+  GMEM float* const ob = obase + lane_sw * NA;
+  // win: off[wb + lane]; win_next: off[wb + 64 + lane]
+  int wb = bs;
+  int64_t win = off[min(bs + lane, be)];
+  int64_t win_next = off[min(bs + kWave + lane, be)];
+  wait_all();
+  const int64_t safe = lane_i64(win, 0);     // a valid position whenever the range has lookups
+  const int64_t last = off[be];
+  wait_all();
+  if (last == safe) {                         // only empty bags
+    Acc<F16> z;
+    acc_zero(z);
+    for (int b = bs; b < be; ++b)
+      if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, z);
+    return;
+  }
+  auto off_of = [&](int bb) -> int64_t {   // bb - wb in [0, 128)
+    const int d = bb - wb;
+    return d < kWave ? lane_i64(win, d) : lane_i64(win_next, d - kWave);
   };
-  int64_t bag_end = end_of(b);
+  int b = bs;
+  int64_t qb = off_of(b);
+  int64_t p1 = off_of(b + 1);
+  Ids<G> ids;
+  ids.load(indices, qb + sw_w, S, p1, safe, lane_sw);
+  wait_all();
   Acc<F16> acc;
   acc_zero(acc);
-  float* const ob = obase + lane_sw * NA;
-  while (p < pend) {
-    const int n = static_cast<int>(min64(kU, pend - p));
-    int64_t ix[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) ix[u] = u < n ? indices[p + u] : int64_t(-1);
+  while (b < be) {
+    int32_t ix[kU];
+    ids.resolve(f, lane_sw, ix);
+    const int n = qb + sw_w < p1 ? static_cast<int>(min64(kU, (p1 - qb - sw_w + S - 1) / S)) : 0;
     int32_t sl[kU];
-    f.probe(ix, p, n, sl);
-    uint4 v[kU];
+    f.probe(ix, qb + sw_w, n, sl);
+    typename F::Raw raw[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) v[u] = u < n ? f.fetch(ix[u], sl[u]) : zero16();
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      if (u < n) {
-        while (p + u == bag_end) {
-          if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
-          acc_zero(acc);
-          ++b;
-          bag_end = end_of(b);
-        }
-        acc_add(acc, v[u]);
-      }
+    for (int u = 0; u < kU; ++u) f.issue(ix[u], sl[u], raw[u]);
+    // the next step: more of this bag, or the first step of the next one
+    const bool lastq = qb + S * kU >= p1;
+    const int bn = lastq ? b + 1 : b;
+    if (bn - wb >= kWave) {   // slide the window by 64 bags (the next 64 ends are loaded)
+      wb += kWave;
+      win = win_next;
+      win_next = off[min(wb + kWave + lane, be)];
     }
-    p += n;
-  }
-  for (; b < be; ++b) {
-    if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
-    acc_zero(acc);
+    const int64_t qbn = lastq ? (bn < be ? off_of(bn) : p1) : qb + S * kU;
+    const int64_t p1n = lastq ? (bn < be ? off_of(bn + 1) : p1) : p1;
+    ids.load(indices, qbn + sw_w, S, p1n, safe, lane_sw);
+    wait_all();   // the one wait of the step
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (u < n) acc_add(acc, f.take(ix[u], sl[u], raw[u]));
+    if (lastq) {
+      acc_wave_reduce<G>(acc);
+      if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+      acc_zero(acc);
+    }
+    b = bn;
+    qb = qbn;
+    p1 = p1n;
   }
 }
 
 // ---------------------------------------------------------------- staging
 
-__device__ __forceinline__ void stage_linear(char* dst, const char* src, int64_t bytes, int tid) {
+__device__ __forceinline__ void stage_linear(lchar* dst, gchar* src, int64_t bytes, int tid) {
   const int64_t n16 = bytes >> 4;
   int64_t q = tid;
   for (; q + 3 * kBlock < n16; q += 4 * kBlock) {
-    const uint4 a = ld16(src + q * 16);
-    const uint4 b = ld16(src + (q + kBlock) * 16);
-    const uint4 c = ld16(src + (q + 2 * kBlock) * 16);
-    const uint4 d = ld16(src + (q + 3 * kBlock) * 16);
-    st16(dst + q * 16, a);
-    st16(dst + (q + kBlock) * 16, b);
-    st16(dst + (q + 2 * kBlock) * 16, c);
-    st16(dst + (q + 3 * kBlock) * 16, d);
+    const uint4 a = ldg16(src + q * 16);
+    const uint4 b = ldg16(src + (q + kBlock) * 16);
+    const uint4 c = ldg16(src + (q + 2 * kBlock) * 16);
+    const uint4 d = ldg16(src + (q + 3 * kBlock) * 16);
+    sts16(dst + q * 16, a);
+    sts16(dst + (q + kBlock) * 16, b);
+    sts16(dst + (q + 2 * kBlock) * 16, c);
+    sts16(dst + (q + 3 * kBlock) * 16, d);
   }
-  for (; q < n16; q += kBlock) st16(dst + q * 16, ld16(src + q * 16));
+  for (; q < n16; q += kBlock) sts16(dst + q * 16, ldg16(src + q * 16));
 }
 
 // rows ids[0..n) of the table -> dst rows 0..n (16-byte pieces spread over the workgroup)
-template <class Id>
-__device__ __forceinline__ void stage_rows(char* dst, const char* w, const Id* ids, int n, int R, int tid) {
+template <class IdPtr>
+__device__ __forceinline__ void stage_rows(lchar* dst, gchar* w, IdPtr ids, int n, int R, int tid) {
   const int RP = R >> 4;
   const int total = n * RP;
   int q = tid;
@@ -302,14 +558,14 @@ __device__ __forceinline__ void stage_rows(char* dst, const char* w, const Id* i
     for (int i = 0; i < 4; ++i) {
       const int qq = q + i * kBlock;
       const int s = qq / RP;
-      v[i] = ld16(w + static_cast<int64_t>(ids[s]) * R + (qq - s * RP) * 16);
+      v[i] = ldg16(w + static_cast<int64_t>(ids[s]) * R + (qq - s * RP) * 16);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) st16(dst + static_cast<int64_t>(q + i * kBlock) * 16, v[i]);
+    for (int i = 0; i < 4; ++i) sts16(dst + static_cast<int64_t>(q + i * kBlock) * 16, v[i]);
   }
   for (; q < total; q += kBlock) {
     const int s = q / RP;
-    st16(dst + static_cast<int64_t>(q) * 16, ld16(w + static_cast<int64_t>(ids[s]) * R + (q - s * RP) * 16));
+    sts16(dst + static_cast<int64_t>(q) * 16, ldg16(w + static_cast<int64_t>(ids[s]) * R + (q - s * RP) * 16));
   }
 }
 
@@ -318,11 +574,12 @@ __device__ __forceinline__ void stage_rows(char* dst, const char* w, const Id* i
 // Sorts the tile's (row << 11 | position) keys, then numbers the distinct rows in
 // ascending order: uniq[slot] = row, inv[position] = slot (-1: id out of range).
 // Returns the number of distinct rows.  All threads of the workgroup call it.
-__device__ int dedup_tile(char* meta, const int64_t* __restrict__ idx, int n, uint64_t rows, int tid) {
-  int64_t* K = reinterpret_cast<int64_t*>(meta + kMetaKeys);
-  int16_t* inv = reinterpret_cast<int16_t*>(meta + kMetaInv);
-  int32_t* uniq = reinterpret_cast<int32_t*>(meta + kMetaUniq);
-  int32_t* scan = reinterpret_cast<int32_t*>(meta + kMetaScan);
+__device__ __attribute__((noinline)) int dedup_tile(lchar* meta, GMEM const int64_t* __restrict__ idx, int n,
+                                                    uint64_t rows, int tid) {
+  LMEM int64_t* K = reinterpret_cast<LMEM int64_t*>(meta + kMetaKeys);
+  LMEM int16_t* inv = reinterpret_cast<LMEM int16_t*>(meta + kMetaInv);
+  LMEM int32_t* uniq = reinterpret_cast<LMEM int32_t*>(meta + kMetaUniq);
+  LMEM int32_t* scan = reinterpret_cast<LMEM int32_t*>(meta + kMetaScan);
   int npad = 1;
   while (npad < n) npad <<= 1;
   for (int q = tid; q < npad; q += kBlock) {
@@ -409,187 +666,313 @@ __device__ int dedup_tile(char* meta, const int64_t* __restrict__ idx, int n, ui
 
 // ---------------------------------------------------------------- the worker kernel
 
-template <int G, bool F16>
-__device__ __forceinline__ void combine_chunks(const LookupArgs& a, const DevItem& it, const DevTable& tb, int bs,
-                                               int be, int sw, int lane_sw, bool active) {
-  constexpr int NSW = kBlock / G;
-  constexpr int NA = F16 ? 8 : 4;
-  const int nb = be - bs;
-  const int lo = bs + static_cast<int>((static_cast<int64_t>(nb) * sw) / NSW);
-  const int hi = bs + static_cast<int>((static_cast<int64_t>(nb) * (sw + 1)) / NSW);
-  if (!active) return;
-  const int64_t slab = static_cast<int64_t>(a.Bmax) * a.E;
-  for (int b = lo; b < hi; ++b) {
-    Acc<F16> acc;
-    acc_zero(acc);
-    const float* p = a.partials + tb.part_base + static_cast<int64_t>(b) * a.E + lane_sw * NA;
-    for (int c = 0; c < it.nchunks; ++c) acc_add_f32(acc, p + c * slab);
-    acc_store(a.out + (static_cast<int64_t>(b) * a.T + it.table) * a.E + lane_sw * NA, acc);
+struct Lane {
+  int tid, lane_sw, sw, wave, sw_w;
+  bool active;
+};
+
+template <int G>
+__device__ __forceinline__ Lane lane_of(int R) {
+  Lane l;
+  l.tid = threadIdx.x;
+  l.lane_sw = l.tid & (G - 1);
+  l.sw = l.tid / G;
+  l.wave = l.tid / kWave;
+  l.sw_w = (l.tid & (kWave - 1)) / G;
+  l.active = l.lane_sw * 16 < R;
+  return l;
+}
+
+__device__ __forceinline__ RowBase row_base(const LookupArgs& a, const DevTable& tb, const Lane& l) {
+  RowBase rb;
+  rb.w = as_global(static_cast<const char*>(tb.w));
+  rb.rows = static_cast<uint64_t>(tb.rows);
+  rb.R = a.R;
+  rb.lane_c = l.active ? l.lane_sw * 16 : 0;
+  rb.active = l.active;
+  rb.count = true;
+  rb.err = as_global(a.err);
+  return rb;
+}
+
+// part i of n of [bs, be), by bag count
+__device__ __forceinline__ void split_bags(int bs, int be, int i, int n, int* lo, int* hi) {
+  const int64_t nb = be - bs;
+  *lo = bs + static_cast<int>((nb * i) / n);
+  *hi = bs + static_cast<int>((nb * (i + 1)) / n);
+}
+
+// a staged slice's bags, by SW (SW mode) or by wavefront (wave mode)
+template <int G, bool F16, class F>
+__device__ __forceinline__ void run_slice(const LookupArgs& a, const DevItem& it, const Lane& l, int bs, int be,
+                                          GMEM float* ob, int64_t ost, F& f) {
+  GMEM const int64_t* idx = as_global(a.indices);
+  GMEM const int64_t* off = as_global(a.offsets) + static_cast<int64_t>(it.table) * a.B;
+  int lo, hi;
+  if constexpr (!F::kPositional) {
+    if (it.mode == 1) {
+      split_bags(bs, be, l.wave, kNumWaves, &lo, &hi);
+      walk_wave<G, F16>(idx, off, lo, hi, ob, ost, l.lane_sw, l.sw_w, f);
+      return;
+    }
   }
+  split_bags(bs, be, l.sw, kBlock / G, &lo, &hi);
+  walk<G, F16>(idx, off, lo, hi, ob, ost, l.lane_sw, f);
 }
 
 template <int G, bool F16>
-__global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
-  extern __shared__ __align__(16) char smem[];
-  __shared__ int s_last;
+__device__ __forceinline__ void combine_chunks(const LookupArgs& a, const DevItem& it, const DevTable& tb, int bs,
+                                               int be, const Lane& l) {
+  constexpr int NA = F16 ? 8 : 4;
+  int lo, hi;
+  split_bags(bs, be, l.sw, kBlock / G, &lo, &hi);
+  if (!l.active) return;
+  const int64_t slab = static_cast<int64_t>(a.Bmax) * a.E;
+  GMEM const float* part = as_global(a.partials) + tb.part_base + l.lane_sw * NA;
+  GMEM float* out = as_global(a.out) + static_cast<int64_t>(it.table) * a.E + l.lane_sw * NA;
+  for (int b = lo; b < hi; ++b) {
+    Acc<F16> acc;
+    acc_zero(acc);
+    GMEM const float* p = part + static_cast<int64_t>(b) * a.E;
+    for (int c = 0; c < it.nchunks; ++c) acc_add_f32(acc, p + c * slab);
+    acc_store(out + static_cast<int64_t>(b) * a.T * a.E, acc);
+  }
+}
+
+// LDS slice: the table (or row chunk [r0, r1)) staged into LDS.  A chunk writes
+// partial sums; the last chunk worker of the batch slice sums them in chunk order.
+template <int G, bool F16>
+__device__ __attribute__((noinline)) void lds_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                                   lchar* smem, LMEM int* s_last) {
+  const Lane l = lane_of<G>(a.R);
+  const DevTable tb = a.tables[it.table];
+  stage_linear(smem, as_global(static_cast<const char*>(tb.w)) + it.r0 * a.R, (it.r1 - it.r0) * a.R, l.tid);
+  __syncthreads();
+  FLds f;
+  static_cast<RowBase&>(f) = row_base(a, tb, l);
+  f.lds = smem;
+  f.r0 = static_cast<int32_t>(it.r0);
+  f.r1 = static_cast<int32_t>(it.r1);
+  f.count = it.chunk == 0;
+  if (it.nchunks == 1) {
+    run_slice<G, F16>(a, it, l, bs, be, as_global(a.out) + static_cast<int64_t>(it.table) * a.E,
+                      static_cast<int64_t>(a.T) * a.E, f);
+    return;
+  }
+  run_slice<G, F16>(a, it, l, bs, be,
+                    as_global(a.partials) + tb.part_base + static_cast<int64_t>(it.chunk) * a.Bmax * a.E, a.E, f);
+  __threadfence();
+  __syncthreads();
+  if (l.tid == 0) *s_last = atomicAdd(as_global(a.counters) + it.counter, 1) == it.nchunks - 1;
+  __syncthreads();
+  if (*s_last) {
+    __threadfence();
+    combine_chunks<G, F16>(a, it, tb, bs, be, l);
+    if (l.tid == 0) atomicExch(as_global(a.counters) + it.counter, 0);
+  }
+}
+
+// HOT slice: the C hottest rows and their id hash staged into LDS
+template <int G, bool F16>
+__device__ __attribute__((noinline)) void hot_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                                   lchar* smem) {
+  const Lane l = lane_of<G>(a.R);
+  const DevTable tb = a.tables[it.table];
+  lchar* meta = smem + a.lds_rows;
+  const int H = 1 << it.hash_log2;
+  LMEM int32_t* hk = reinterpret_cast<LMEM int32_t*>(meta + kMetaHashKeys);
+  LMEM uint16_t* hs = reinterpret_cast<LMEM uint16_t*>(meta + kMetaHashSlots);
+  GMEM const int32_t* gk = as_global(a.hot_keys) + it.hot_off;
+  GMEM const uint16_t* gs = as_global(a.hot_slots) + it.hot_off;
+  for (int q = l.tid; q < H; q += kBlock) {
+    hk[q] = gk[q];
+    hs[q] = gs[q];
+  }
+  stage_rows(smem, as_global(static_cast<const char*>(tb.w)), as_global(a.hot_ids) + it.hot_off, it.C, a.R, l.tid);
+  __syncthreads();
+  FHot f;
+  static_cast<RowBase&>(f) = row_base(a, tb, l);
+  f.lds = smem;
+  f.keys = hk;
+  f.slots = hs;
+  f.hb = it.hash_log2;
+  run_slice<G, F16>(a, it, l, bs, be, as_global(a.out) + static_cast<int64_t>(it.table) * a.E,
+                    static_cast<int64_t>(a.T) * a.E, f);
+}
+
+// one bag gathered straight from HBM by one SW
+template <int G, bool F16>
+__device__ __attribute__((noinline)) void gather_one_bag(const LookupArgs& a, const RowBase& rb,
+                                                         GMEM const int64_t* off, int b, GMEM float* ob, int64_t ost,
+                                                         int lane_sw) {
+  FGather fg;
+  static_cast<RowBase&>(fg) = rb;
+  walk<G, F16>(as_global(a.indices), off, b, b + 1, ob, ost, lane_sw, fg);
+}
+
+// DEDUP slice: tiles of whole bags holding at most kTile lookups
+template <int G, bool F16>
+__device__ __attribute__((noinline)) void dedup_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                                     lchar* smem) {
+  const Lane l = lane_of<G>(a.R);
+  const DevTable tb = a.tables[it.table];
+  GMEM const int64_t* idx = as_global(a.indices);
+  GMEM const int64_t* off = as_global(a.offsets) + static_cast<int64_t>(it.table) * a.B;
+  lchar* meta = smem + a.lds_rows;
+  const int capd = a.lds_rows / a.R;
+  FDedup f;
+  static_cast<RowBase&>(f) = row_base(a, tb, l);
+  f.lds = smem;
+  f.inv = reinterpret_cast<LMEM const int16_t*>(meta + kMetaInv);
+  f.capd = capd;
+  GMEM float* const ob = as_global(a.out) + static_cast<int64_t>(it.table) * a.E;
+  const int64_t ost = static_cast<int64_t>(a.T) * a.E;
+  int bcur = bs;
+  while (bcur < be) {
+    const int64_t P0 = off[bcur];
+    const int cand = bcur + 1 + l.tid;
+    const bool ok = cand <= be && off[min(cand, be)] - P0 <= kTile;
+    const int cnt = __syncthreads_count(ok);
+    const int bnext = bcur + cnt;
+    const int64_t n64 = cnt > 0 ? off[bnext] - P0 : -1;
+    if (cnt == 0 || n64 < 0 || n64 > kTile) {
+      // a bag longer than a tile (or malformed offsets): gathered directly
+      if (l.sw == 0) gather_one_bag<G, F16>(a, static_cast<const RowBase&>(f), off, bcur, ob, ost, l.lane_sw);
+      bcur += 1;
+      continue;
+    }
+    const int n = static_cast<int>(n64);
+    const int U = dedup_tile(meta, idx + P0, n, f.rows, l.tid);
+    stage_rows(smem, f.w, reinterpret_cast<const LMEM int32_t*>(meta + kMetaUniq), min(U, capd), a.R, l.tid);
+    __syncthreads();
+    f.P0 = P0;
+    int lo, hi;
+    split_bags(bcur, bnext, l.sw, kBlock / G, &lo, &hi);
+    walk<G, F16>(idx, off, lo, hi, ob, ost, l.lane_sw, f);
+    __syncthreads();   // LDS is rewritten by the next tile
+    bcur = bnext;
+  }
+}
+
+__device__ __forceinline__ unsigned long long now_ticks() { return __builtin_amdgcn_s_memrealtime(); }
+
+// Chunks c = first, first + step, ... of one worker's gather queue (entries
+// [e, e_end), chunk c of entry x = bags [bs + (c - base) cb, + cb) of its slice).
+struct ChunkSrc {
+  const LookupArgs* a;
+  GMEM const GatherEntry* gq;
+  GMEM const DevItem* items;
+  int e, e_end, c, step, nchunks;
+
+  __device__ __forceinline__ bool next(Seg& sg) {
+    while (c < nchunks) {
+      while (e + 1 < e_end && gq[e + 1].chunk_base <= c) ++e;
+      const GatherEntry ge = gq[e];
+      const DevItem it = items[ge.item];
+      const int bs = slice_lo(it.j, it.k, a->B), be = slice_lo(it.j + 1, it.k, a->B);
+      const int c0 = bs + (c - ge.chunk_base) * ge.cb;
+      const int c1 = min(be, c0 + ge.cb);
+      c += step;
+      if (c0 >= c1) continue;
+      const DevTable tb = a->tables[it.table];
+      sg.w = as_global(static_cast<const char*>(tb.w));
+      sg.rows = static_cast<uint64_t>(tb.rows);
+      sg.off = as_global(a->offsets) + static_cast<int64_t>(it.table) * a->B;
+      sg.ob = as_global(a->out) + static_cast<int64_t>(it.table) * a->E;
+      sg.bs = c0;
+      sg.be = c1;
+      return true;
+    }
+    return false;
+  }
+};
+
+// Gather slices.  A worker's gather slices are cut into two queues of chunks (runs of
+// bags of one slice): long-bag slices (wave mode) and the rest (SW mode).  Wavefront v
+// takes wave-mode chunks v, v + 16, ...; SW s takes SW-mode chunks s, s + NSW, ...  The
+// chunks are small, so every SW samples every slice of the worker: the split stays
+// even when per-lookup cost differs between tables (cache-resident vs HBM-bound).
+template <int G, bool F16>
+__device__ __forceinline__ void gather_phase(const LookupArgs& a, GMEM const DevItem* items, const Lane& l, int wg) {
   constexpr int NSW = kBlock / G;
-  const int tid = threadIdx.x;
-  const int lane_sw = tid & (G - 1);
-  const int sw = tid / G;
-  const bool active = lane_sw * 16 < a.R;
+  GMEM const int64_t* idx = as_global(a.indices);
+  const int64_t ost = static_cast<int64_t>(a.T) * a.E;
+  DevTable tb0;
+  tb0.w = nullptr;
+  tb0.rows = 0;
+  const RowBase rb0 = row_base(a, tb0, l);
+  {  // wave mode
+    GMEM const int32_t* gptr = as_global(a.gqw_ptr);
+    ChunkSrc src{&a, as_global(a.gqw), items, gptr[wg], gptr[wg + 1], l.wave, kNumWaves, as_global(a.gqw_chunks)[wg]};
+    Seg sg;
+    while (src.next(sg)) {
+      FGather f;
+      static_cast<RowBase&>(f) = rb0;
+      f.w = sg.w;
+      f.rows = sg.rows;
+      walk_wave<G, F16>(idx, sg.off, sg.bs, sg.be, sg.ob, ost, l.lane_sw, l.sw_w, f);
+    }
+  }
+  {  // SW mode
+    GMEM const int32_t* gptr = as_global(a.gq_ptr);
+    ChunkSrc src{&a, as_global(a.gq), items, gptr[wg], gptr[wg + 1], l.sw, NSW, as_global(a.gq_chunks)[wg]};
+    FGather f;
+    static_cast<RowBase&>(f) = rb0;
+    walk_seq<G, F16>(idx, ost, l.lane_sw, f, src);
+  }
+}
+
+// STAGED = false: the plan has gather slices only (no LDS, no staged-slice code).
+template <int G, bool F16, bool STAGED>
+__global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
+  extern __shared__ __align__(16) char smem_raw[];
+  __shared__ int s_last;
+  const Lane l = lane_of<G>(a.R);
   const int wg = blockIdx.x;
-  const int i0 = a.wg_ptr[wg], i1 = a.wg_ptr[wg + 1];
-  char* const meta = smem + a.lds_rows;
+  GMEM const int32_t* wg_ptr = as_global(a.wg_ptr);
+  GMEM const DevItem* items = as_global(a.items);
+  const int i0 = wg_ptr[wg], i1 = wg_ptr[wg + 1];
+  GMEM unsigned long long* tw = a.trace ? as_global(a.trace) + static_cast<int64_t>(wg) * kTraceWorker : nullptr;
+  GMEM unsigned long long* ti = a.trace ? as_global(a.trace) + static_cast<int64_t>(gridDim.x) * kTraceWorker : nullptr;
+  if (tw && l.tid == 0) tw[0] = now_ticks();
 
   // staged slices first: each needs the whole workgroup and LDS
-  for (int i = i0; i < i1; ++i) {
-    const DevItem it = a.items[i];
-    if (it.strat == 3) continue;
-    const int bs = slice_lo(it.j, it.k, a.B), be = slice_lo(it.j + 1, it.k, a.B);
-    if (bs >= be) continue;
-    const DevTable tb = a.tables[it.table];
-    const int64_t* off = a.offsets + static_cast<int64_t>(it.table) * a.B;
-    RowBase rb;
-    rb.w = static_cast<const char*>(tb.w);
-    rb.rows = static_cast<uint64_t>(tb.rows);
-    rb.R = a.R;
-    rb.lane_off = lane_sw * 16;
-    rb.active = active;
-    rb.lead = lane_sw == 0;
-    rb.err = a.err;
-    const int nb = be - bs;
-    const int lo = bs + static_cast<int>((static_cast<int64_t>(nb) * sw) / NSW);
-    const int hi = bs + static_cast<int>((static_cast<int64_t>(nb) * (sw + 1)) / NSW);
-    __syncthreads();   // the previous slice is done with LDS
-    if (it.strat == 0) {
-      stage_linear(smem, rb.w + it.r0 * a.R, (it.r1 - it.r0) * a.R, tid);
-      __syncthreads();
-      FLds f;
-      static_cast<RowBase&>(f) = rb;
-      f.lds = smem;
-      f.r0 = it.r0;
-      f.r1 = it.r1;
-      f.count = it.chunk == 0;
-      if (it.nchunks > 1) {
-        float* ob = a.partials + tb.part_base + static_cast<int64_t>(it.chunk) * a.Bmax * a.E;
-        walk<G, F16>(a.indices, off, lo, hi, ob, a.E, lane_sw, f);
-        // last chunk worker of this batch slice sums the partials in chunk order
-        __threadfence();
+  if constexpr (STAGED) {
+    lchar* smem = (lchar*)smem_raw;
+    for (int i = i0; i < i1; ++i) {
+      const DevItem it = items[i];
+      if (it.strat == 3) continue;
+      const int bs = slice_lo(it.j, it.k, a.B), be = slice_lo(it.j + 1, it.k, a.B);
+      if (bs >= be) continue;
+      __syncthreads();   // the previous slice is done with LDS
+      if (ti && l.tid == 0) ti[2 * i] = now_ticks();
+      if (it.strat == 0)
+        lds_item<G, F16>(a, it, bs, be, smem, (LMEM int*)&s_last);
+      else if (it.strat == 1)
+        hot_item<G, F16>(a, it, bs, be, smem);
+      else
+        dedup_item<G, F16>(a, it, bs, be, smem);
+      if (ti) {
         __syncthreads();
-        if (tid == 0) s_last = atomicAdd(a.counters + it.counter, 1) == it.nchunks - 1;
-        __syncthreads();
-        if (s_last) {
-          __threadfence();
-          combine_chunks<G, F16>(a, it, tb, bs, be, sw, lane_sw, active);
-          if (tid == 0) atomicExch(a.counters + it.counter, 0);
-        }
-      } else {
-        walk<G, F16>(a.indices, off, lo, hi, a.out + static_cast<int64_t>(it.table) * a.E,
-                     static_cast<int64_t>(a.T) * a.E, lane_sw, f);
-      }
-    } else if (it.strat == 1) {
-      const int H = 1 << it.hash_log2;
-      int32_t* hk = reinterpret_cast<int32_t*>(meta + kMetaHashKeys);
-      uint16_t* hs = reinterpret_cast<uint16_t*>(meta + kMetaHashSlots);
-      for (int q = tid; q < H; q += kBlock) {
-        hk[q] = a.hot_keys[it.hot_off + q];
-        hs[q] = a.hot_slots[it.hot_off + q];
-      }
-      stage_rows(smem, rb.w, a.hot_ids + it.hot_off, it.C, a.R, tid);
-      __syncthreads();
-      FHot f;
-      static_cast<RowBase&>(f) = rb;
-      f.lds = smem;
-      f.keys = hk;
-      f.slots = hs;
-      f.hb = it.hash_log2;
-      walk<G, F16>(a.indices, off, lo, hi, a.out + static_cast<int64_t>(it.table) * a.E,
-                   static_cast<int64_t>(a.T) * a.E, lane_sw, f);
-    } else {
-      // DEDUP: tiles of whole bags holding at most kTile lookups
-      const int capd = a.lds_rows / a.R;
-      FDedup f;
-      static_cast<RowBase&>(f) = rb;
-      f.lds = smem;
-      f.inv = reinterpret_cast<const int16_t*>(meta + kMetaInv);
-      f.capd = capd;
-      FGather fg;
-      static_cast<RowBase&>(fg) = rb;
-      float* const ob = a.out + static_cast<int64_t>(it.table) * a.E;
-      const int64_t ost = static_cast<int64_t>(a.T) * a.E;
-      int bcur = bs;
-      while (bcur < be) {
-        const int64_t P0 = off[bcur];
-        const int cand = bcur + 1 + tid;
-        const bool ok = cand <= be && off[min(cand, be)] - P0 <= kTile;
-        const int cnt = __syncthreads_count(ok);
-        const int bnext = bcur + cnt;
-        const int64_t n64 = cnt > 0 ? off[bnext] - P0 : -1;
-        if (cnt == 0 || n64 < 0 || n64 > kTile) {
-          // a bag longer than a tile (or malformed offsets): gathered directly
-          if (sw == 0) walk<G, F16>(a.indices, off, bcur, bcur + 1, ob, ost, lane_sw, fg);
-          bcur += 1;
-          continue;
-        }
-        const int n = static_cast<int>(n64);
-        const int U = dedup_tile(meta, a.indices + P0, n, rb.rows, tid);
-        stage_rows(smem, rb.w, reinterpret_cast<const int32_t*>(meta + kMetaUniq), min(U, capd), a.R, tid);
-        __syncthreads();
-        f.P0 = P0;
-        const int tb_n = bnext - bcur;
-        const int tlo = bcur + static_cast<int>((static_cast<int64_t>(tb_n) * sw) / NSW);
-        const int thi = bcur + static_cast<int>((static_cast<int64_t>(tb_n) * (sw + 1)) / NSW);
-        walk<G, F16>(a.indices, off, tlo, thi, ob, ost, lane_sw, f);
-        __syncthreads();   // LDS is rewritten by the next tile
-        bcur = bnext;
+        if (l.tid == 0) ti[2 * i + 1] = now_ticks();
       }
     }
   }
-
-  // gather slices: flattened bag list split evenly over the worker's SWs
-  int64_t N = 0;
-  for (int i = i0; i < i1; ++i) {
-    const DevItem& it = a.items[i];
-    if (it.strat != 3) continue;
-    N += slice_lo(it.j + 1, it.k, a.B) - slice_lo(it.j, it.k, a.B);
-  }
-  if (N == 0) return;
-  const int64_t F0 = (N * sw) / NSW, F1 = (N * (sw + 1)) / NSW;
-  if (F0 >= F1) return;
-  int64_t c0 = 0;
-  for (int i = i0; i < i1 && c0 < F1; ++i) {
-    const DevItem it = a.items[i];
-    if (it.strat != 3) continue;
-    const int bs = slice_lo(it.j, it.k, a.B), be = slice_lo(it.j + 1, it.k, a.B);
-    const int64_t nb = be - bs;
-    const int64_t lo = max64(F0, c0), hi = min64(F1, c0 + nb);
-    if (lo < hi) {
-      const DevTable tb = a.tables[it.table];
-      FGather f;
-      f.w = static_cast<const char*>(tb.w);
-      f.rows = static_cast<uint64_t>(tb.rows);
-      f.R = a.R;
-      f.lane_off = lane_sw * 16;
-      f.active = active;
-      f.lead = lane_sw == 0;
-      f.err = a.err;
-      walk<G, F16>(a.indices, a.offsets + static_cast<int64_t>(it.table) * a.B, bs + static_cast<int>(lo - c0),
-                   bs + static_cast<int>(hi - c0), a.out + static_cast<int64_t>(it.table) * a.E,
-                   static_cast<int64_t>(a.T) * a.E, lane_sw, f);
-    }
-    c0 += nb;
-  }
+  if (tw && l.tid == 0) tw[1] = now_ticks();
+  gather_phase<G, F16>(a, items, l, wg);
+  if (tw && (l.tid & (kWave - 1)) == 0) tw[2 + l.wave] = now_ticks();
 }
 
 // ---------------------------------------------------------------- index-handling probes
 
 __global__ void __launch_bounds__(kBlock) dedup_probe_kernel(const int64_t* idx, int n, int32_t* uniq,
                                                              int32_t* inv, int32_t* n_uniq) {
-  extern __shared__ __align__(16) char smem[];
+  extern __shared__ __align__(16) char smem_raw[];
+  lchar* smem = (lchar*)smem_raw;
   const int tid = threadIdx.x;
-  const int U = dedup_tile(smem, idx, n, uint64_t(1) << 31, tid);
-  const int16_t* li = reinterpret_cast<const int16_t*>(smem + kMetaInv);
-  const int32_t* lu = reinterpret_cast<const int32_t*>(smem + kMetaUniq);
+  const int U = dedup_tile(smem, as_global(idx), n, uint64_t(1) << 31, tid);
+  const LMEM int16_t* li = reinterpret_cast<const LMEM int16_t*>(smem + kMetaInv);
+  const LMEM int32_t* lu = reinterpret_cast<const LMEM int32_t*>(smem + kMetaUniq);
   for (int q = tid; q < n; q += kBlock) inv[q] = li[q];
   for (int q = tid; q < U; q += kBlock) uniq[q] = lu[q];
   if (tid == 0) *n_uniq = U;
@@ -597,9 +980,9 @@ __global__ void __launch_bounds__(kBlock) dedup_probe_kernel(const int64_t* idx,
 
 __global__ void __launch_bounds__(256) hot_probe_kernel(const int32_t* gkeys, const uint16_t* gslots, int hb,
                                                         const int64_t* idx, int n, int32_t* slot) {
-  extern __shared__ __align__(16) char smem[];
-  int32_t* hk = reinterpret_cast<int32_t*>(smem);
-  uint16_t* hs = reinterpret_cast<uint16_t*>(smem + (4 << hb));
+  extern __shared__ __align__(16) char smem_raw[];
+  LMEM int32_t* hk = (LMEM int32_t*)smem_raw;
+  LMEM uint16_t* hs = (LMEM uint16_t*)(smem_raw + (4 << hb));
   const int H = 1 << hb;
   for (int q = threadIdx.x; q < H; q += blockDim.x) {
     hk[q] = gkeys[q];
@@ -609,11 +992,14 @@ __global__ void __launch_bounds__(256) hot_probe_kernel(const int32_t* gkeys, co
   const int base = (blockIdx.x * blockDim.x + threadIdx.x) * kU;
   if (base >= n) return;
   const int m = min(kU, n - base);
-  int64_t ix[kU];
+  int32_t ix[kU];
 #pragma unroll
-  for (int u = 0; u < kU; ++u) ix[u] = u < m ? idx[base + u] : int64_t(-1);
+  for (int u = 0; u < kU; ++u) {
+    const int64_t x = u < m ? idx[base + u] : int64_t(-1);
+    ix[u] = (x >= 0 && x < (int64_t(1) << 31)) ? static_cast<int32_t>(x) : -1;
+  }
   int32_t sl[kU];
-  hot_probe_batch(hk, hs, hb, ix, m, uint64_t(1) << 31, sl);
+  hot_probe_batch(hk, hs, hb, ix, m, sl);
 #pragma unroll
   for (int u = 0; u < kU; ++u)
     if (u < m) slot[base + u] = sl[u];
@@ -666,18 +1052,23 @@ __global__ void __launch_bounds__(256) fill_kernel(char* dst, int64_t row_begin,
 
 using KernelFn = void (*)(LookupArgs);
 
-template <bool F16>
+template <bool F16, bool STAGED>
 KernelFn pick(int G) {
   switch (G) {
-    case 1: return &lookup_kernel<1, F16>;
-    case 2: return &lookup_kernel<2, F16>;
-    case 4: return &lookup_kernel<4, F16>;
-    case 8: return &lookup_kernel<8, F16>;
-    case 16: return &lookup_kernel<16, F16>;
-    case 32: return &lookup_kernel<32, F16>;
-    case 64: return &lookup_kernel<64, F16>;
+    case 1: return &lookup_kernel<1, F16, STAGED>;
+    case 2: return &lookup_kernel<2, F16, STAGED>;
+    case 4: return &lookup_kernel<4, F16, STAGED>;
+    case 8: return &lookup_kernel<8, F16, STAGED>;
+    case 16: return &lookup_kernel<16, F16, STAGED>;
+    case 32: return &lookup_kernel<32, F16, STAGED>;
+    case 64: return &lookup_kernel<64, F16, STAGED>;
     default: return nullptr;
   }
+}
+
+KernelFn pick_any(int G, bool f16, bool staged) {
+  if (f16) return staged ? pick<true, true>(G) : pick<true, false>(G);
+  return staged ? pick<false, true>(G) : pick<false, false>(G);
 }
 
 }  // namespace
@@ -685,7 +1076,7 @@ KernelFn pick(int G) {
 int prepare_lookup_kernels(int lds_bytes) {
   for (int G = 1; G <= 64; G <<= 1) {
     for (int f = 0; f < 2; ++f) {
-      KernelFn k = f ? pick<true>(G) : pick<false>(G);
+      KernelFn k = pick_any(G, f != 0, true);
       if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                               lds_bytes) != hipSuccess)
         return 4;
@@ -698,7 +1089,7 @@ int prepare_lookup_kernels(int lds_bytes) {
 }
 
 int launch_lookup(const LookupArgs& a, int G, bool f16, int grid, int lds_bytes, void* stream) {
-  KernelFn k = f16 ? pick<true>(G) : pick<false>(G);
+  KernelFn k = pick_any(G, f16, lds_bytes > 0);
   if (!k) return 2;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kBlock), lds_bytes, static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? 0 : 4;

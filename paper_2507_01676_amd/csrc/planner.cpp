@@ -6,9 +6,11 @@
 //      row chunks of at most floor(min(chunk_max, L) / R) rows if its best unsplit cost
 //      exceeds the sum of the chunk costs;
 //   P3 tau = ceil(total cost / K);
-//   P4 an item above tau is batch-split k ways (symmetric partitioning, Sec. III-A,
-//      applied per item): the smallest k in [2, min(K, B)] whose best cost is at most
-//      max(tau, 2 x fixed cost); the chunks of a table share one k;
+//   P4 a GATHER item is split k = min(K, B) ways (symmetric partitioning, Sec. III-A:
+//      a gather slice stages nothing, so every worker takes 1/k of every such table);
+//      any other item above tau is batch-split k ways: the smallest k in [2, min(K, B)]
+//      whose best cost is at most max(tau, 2 x fixed cost); the chunks of a table share
+//      one k;
 //   P5 (step 2) slices in order (cost desc, s desc, m asc, t, chunk, j), or the paper's
 //      key (s desc, m asc, t, chunk, j) with order_mode 1;
 //   P6 (step 2) each slice to the least-loaded worker, ties to the lowest index;
@@ -333,7 +335,10 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     // P4
     for (auto& g : P.groups) {
       int32_t k = 1;
-      for (const Item& it : g) k = std::max(k, it.cost <= P.tau ? 1 : P.split_k(it));
+      if (g[0].nchunks == 1 && g[0].strat == S_GATHER)
+        k = P.kmax;
+      else
+        for (const Item& it : g) k = std::max(k, it.cost <= P.tau ? 1 : P.split_k(it));
       for (Item& it : g) {
         Best bb = P.item_best(it, k);
         it.strat = bb.strat;

@@ -151,13 +151,30 @@ def test_plan_invariants_hypothesis(seed):
 # ---------------------------------------------------------------- special cases
 
 def test_K_identical_tables_one_per_worker():
+    # staged tables (DEDUP forced) that each cost about tau stay whole: one per worker
     K = 8
     rows = [5_000_000] * K
     stats = [OPL.Stat(1.0)] * K
-    p = OPL.plan_reference(rows, 64, "f32", stats, 2048, K)
+    p = OPL.plan_reference(rows, 64, "f32", stats, 2048, K, OPL.Options(force=[OPL.DEDUP] * K))
     assert sorted(s.wg for s in p.slices) == list(range(K))
-    assert all(s.k == 1 and s.strat == OPL.GATHER for s in p.slices)
+    assert all(s.k == 1 and s.strat == OPL.DEDUP for s in p.slices)
     assert p.lif_milli == 1000
+
+
+def test_gather_tables_are_partitioned_symmetrically():
+    # gather tables are split over all workers: every worker gets one slice of each
+    K, B = 8, 2048
+    rows = [10, 5_000_000, 300_000]
+    stats = [OPL.Stat(1.0), OPL.Stat(8.0), OPL.Stat(2.0)]
+    p = OPL.plan_reference(rows, 64, "f32", stats, B, K, OPL.Options(force=[OPL.GATHER] * 3))
+    assert len(p.slices) == 3 * K
+    for t in range(3):
+        assert sorted(s.wg for s in p.slices if s.t == t) == list(range(K))
+        assert all(s.k == K for s in p.slices if s.t == t)
+    assert p.lif_milli == 1000
+    # fewer samples than workers: k = B
+    p = OPL.plan_reference(rows, 64, "f32", stats, 5, K, OPL.Options(force=[OPL.GATHER] * 3))
+    assert all(s.k == 5 for s in p.slices)
 
 
 def test_one_huge_table_is_split_over_all_workers():
@@ -238,8 +255,9 @@ def test_lif_fallback_makes_trailing_tables_symmetric():
     rows = [1_000_000, 1_000_001]
     stats = [OPL.Stat(1.0), OPL.Stat(1.0)]
     b = OPL.default_beta(256)
-    b[OPL.G0] = 1e9            # a big fixed cost keeps P4 from splitting
-    p = OPL.plan_reference(rows, 64, "f32", stats, 3, 3, OPL.Options(beta=b, lif_milli=1200))
+    b[OPL.D0] = 1e9            # a big fixed cost keeps P4 from splitting
+    p = OPL.plan_reference(rows, 64, "f32", stats, 3, 3,
+                           OPL.Options(beta=b, lif_milli=1200, force=[OPL.DEDUP, OPL.DEDUP]))
     assert p.r_sym >= 1
     sym = [s for s in p.slices if s.t == 1]
     assert sorted(s.wg for s in sym) == [0, 1, 2] and all(s.k == 3 for s in sym)
