@@ -39,12 +39,11 @@ struct emb_plan {
   int32_t* d_hot_ids = nullptr;
   int32_t* d_counters = nullptr;
   unsigned long long* d_err = nullptr;
-  GatherEntry* d_gq = nullptr;
-  int32_t* d_gq_ptr = nullptr;
-  int32_t* d_gq_chunks = nullptr;
-  GatherEntry* d_gqw = nullptr;
-  int32_t* d_gqw_ptr = nullptr;
-  int32_t* d_gqw_chunks = nullptr;
+  std::vector<GatherRun> h_gr;           // gather runs (table pointers patched at bind)
+  GatherRun* d_gr = nullptr;
+  int32_t* d_gr_ptr = nullptr;
+  int32_t* d_gr_info = nullptr;
+  bool staged = false;                   // the plan has LDS / HOT / DEDUP slices
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
 };
 
@@ -284,53 +283,82 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     wg_ptr[x.wg + 1] += 1;
   }
   for (int w = 0; w < K; ++w) wg_ptr[w + 1] += wg_ptr[w];
+  // Gather slices share their worker's SW pool, so for them a bag is long when it
+  // holds more lookups than one SW's share of the worker's gather lookups.
+  for (int w = 0; w < K; ++w) {
+    double Wg = 0.0;
+    for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
+      const DevItem& d = items[i];
+      if (d.strat != S_GATHER) continue;
+      const int64_t nb = (static_cast<int64_t>(d.j + 1) * max_batch) / d.k - (static_cast<int64_t>(d.j) * max_batch) / d.k;
+      Wg += static_cast<double>(nb) * std::max(1.0, stats[d.table].mean_pooling);
+    }
+    for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
+      DevItem& d = items[i];
+      if (d.strat != S_GATHER) continue;
+      const double s_t = stats[d.table].mean_pooling;
+      d.mode = (s_t >= 4.0 * (64 / p->G) && s_t * (kBlock / p->G) > Wg) ? 1 : 0;
+    }
+  }
 
-  // gather chunk queues per worker, slices in plan order.  SW-mode chunks carry about
-  // W / (4 NSW) expected lookups (W: the worker's SW-mode lookups at the max batch),
-  // at least one full step (8) and at most 32, so that each SW gets several chunks;
-  // wave-mode chunks carry about four wavefront steps of lookups.
-  std::vector<GatherEntry> gq, gqw;
-  std::vector<int32_t> gq_ptr(K + 1, 0), gq_chunks(K, 0), gqw_ptr(K + 1, 0), gqw_chunks(K, 0);
+  // gather run queues per worker, slices in plan order: wave-mode runs, then SW-mode
+  // runs.  SW-mode chunks carry about W / (4 NSW) expected lookups (W: the worker's
+  // SW-mode lookups at the max batch), at least one full step (8) and at most 32, so
+  // that each SW gets several chunks; wave-mode chunks carry about four wavefront
+  // steps of lookups, fewer when that leaves some of the 16 wavefronts without one.
+  std::vector<GatherRun>& gr = p->h_gr;
+  std::vector<int32_t> gr_ptr(K + 1, 0), gr_info(4 * static_cast<size_t>(K), 0);
+  int max_runs = 0;
   {
     const int nsw = kBlock / p->G;
+    const int nwaves = kBlock / 64;
     const double wave_chunk = 4.0 * 8.0 * (64 / p->G);
     auto slice_bags = [&](const DevItem& d) -> int64_t {
       return (static_cast<int64_t>(d.j + 1) * max_batch) / d.k - (static_cast<int64_t>(d.j) * max_batch) / d.k;
     };
     for (int w = 0; w < K; ++w) {
-      double W = 0.0;
-      for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i)
-        if (items[i].strat == S_GATHER && items[i].mode == 0)
-          W += static_cast<double>(slice_bags(items[i])) * std::max(1.0, stats[items[i].table].mean_pooling);
-      const double target = std::min(32.0, std::max(8.0, std::floor(W / (4.0 * nsw))));
-      gq_ptr[w] = static_cast<int32_t>(gq.size());
-      gqw_ptr[w] = static_cast<int32_t>(gqw.size());
-      int64_t base = 0, basew = 0;
+      double Ws = 0.0, Ww = 0.0;
       for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
-        const DevItem& d = items[i];
-        if (d.strat != S_GATHER) continue;
-        const double s_t = std::max(1.0, stats[d.table].mean_pooling);
-        const int32_t cb = static_cast<int32_t>(std::max(1.0, std::floor((d.mode ? wave_chunk : target) / s_t)));
-        const int64_t nb = slice_bags(d);
-        const int64_t nc = (nb + cb - 1) / cb;
-        if (nc == 0) continue;
-        if (d.mode) {
-          gqw.push_back(GatherEntry{i, static_cast<int32_t>(basew), cb, 0});
-          basew += nc;
-        } else {
-          gq.push_back(GatherEntry{i, static_cast<int32_t>(base), cb, 0});
-          base += nc;
+        if (items[i].strat != S_GATHER) continue;
+        const double lk = static_cast<double>(slice_bags(items[i])) * std::max(1.0, stats[items[i].table].mean_pooling);
+        (items[i].mode ? Ww : Ws) += lk;
+      }
+      const double target = std::min(32.0, std::max(8.0, std::floor(Ws / (4.0 * nsw))));
+      const double wtarget = std::min(wave_chunk, std::max(1.0, std::floor(Ww / nwaves)));
+      gr_ptr[w] = static_cast<int32_t>(gr.size());
+      int64_t base[2] = {0, 0};
+      int32_t nrun[2] = {0, 0};
+      for (int pass = 1; pass >= 0; --pass) {   // wave mode (1) first
+        for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
+          const DevItem& d = items[i];
+          if (d.strat != S_GATHER || d.mode != pass) continue;
+          const double s_t = std::max(1.0, stats[d.table].mean_pooling);
+          const int32_t cb = static_cast<int32_t>(std::max(1.0, std::floor((pass ? wtarget : target) / s_t)));
+          const int64_t nc = (slice_bags(d) + cb - 1) / cb;
+          if (nc == 0) continue;
+          GatherRun r{};
+          r.w = nullptr;
+          r.rows = rows[d.table];
+          r.table = d.table;
+          r.j = d.j;
+          r.k = d.k;
+          r.cb = cb;
+          r.chunk_base = static_cast<int32_t>(base[pass]);
+          gr.push_back(r);
+          base[pass] += nc;
+          nrun[pass] += 1;
         }
       }
-      if (base > INT32_MAX || basew > INT32_MAX) {
+      if (base[0] > INT32_MAX || base[1] > INT32_MAX || nrun[0] + nrun[1] > kMaxRunsPerWorker) {
         delete p;
         return EMB_ERR_UNSUPPORTED;
       }
-      gq_chunks[w] = static_cast<int32_t>(base);
-      gqw_chunks[w] = static_cast<int32_t>(basew);
+      max_runs = std::max(max_runs, nrun[0] + nrun[1]);
+      gr_info[4 * w + 0] = nrun[1];
+      gr_info[4 * w + 1] = static_cast<int32_t>(base[1]);
+      gr_info[4 * w + 2] = static_cast<int32_t>(base[0]);
     }
-    gq_ptr[K] = static_cast<int32_t>(gq.size());
-    gqw_ptr[K] = static_cast<int32_t>(gqw.size());
+    gr_ptr[K] = static_cast<int32_t>(gr.size());
   }
 
   // one metadata allocation
@@ -342,13 +370,10 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   size_t o_ids = align_up(o_slots + h_slots.size() * sizeof(uint16_t), 256);
   size_t o_ctr = align_up(o_ids + h_ids.size() * sizeof(int32_t), 256);
   size_t o_err = align_up(o_ctr + static_cast<size_t>(n_ctr) * sizeof(int32_t), 256);
-  size_t o_gq = align_up(o_err + sizeof(unsigned long long), 256);
-  size_t o_gqp = align_up(o_gq + gq.size() * sizeof(GatherEntry), 256);
-  size_t o_gqn = align_up(o_gqp + gq_ptr.size() * sizeof(int32_t), 256);
-  size_t o_gqw = align_up(o_gqn + gq_chunks.size() * sizeof(int32_t), 256);
-  size_t o_gqwp = align_up(o_gqw + gqw.size() * sizeof(GatherEntry), 256);
-  size_t o_gqwn = align_up(o_gqwp + gqw_ptr.size() * sizeof(int32_t), 256);
-  size_t total = align_up(o_gqwn + gqw_chunks.size() * sizeof(int32_t), 256);
+  size_t o_gr = align_up(o_err + sizeof(unsigned long long), 256);
+  size_t o_grp = align_up(o_gr + gr.size() * sizeof(GatherRun), 256);
+  size_t o_gri = align_up(o_grp + gr_ptr.size() * sizeof(int32_t), 256);
+  size_t total = align_up(o_gri + gr_info.size() * sizeof(int32_t), 256);
   if (hipMalloc(&p->d_meta, total) != hipSuccess) {
     delete p;
     return EMB_ERR_OUT_OF_MEMORY;
@@ -366,12 +391,9 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   p->d_hot_ids = reinterpret_cast<int32_t*>(p->d_meta + o_ids);
   p->d_counters = reinterpret_cast<int32_t*>(p->d_meta + o_ctr);
   p->d_err = reinterpret_cast<unsigned long long*>(p->d_meta + o_err);
-  p->d_gq = reinterpret_cast<GatherEntry*>(p->d_meta + o_gq);
-  p->d_gq_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_gqp);
-  p->d_gq_chunks = reinterpret_cast<int32_t*>(p->d_meta + o_gqn);
-  p->d_gqw = reinterpret_cast<GatherEntry*>(p->d_meta + o_gqw);
-  p->d_gqw_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_gqwp);
-  p->d_gqw_chunks = reinterpret_cast<int32_t*>(p->d_meta + o_gqwn);
+  p->d_gr = reinterpret_cast<GatherRun*>(p->d_meta + o_gr);
+  p->d_gr_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_grp);
+  p->d_gr_info = reinterpret_cast<int32_t*>(p->d_meta + o_gri);
   std::vector<char> host(total, 0);
   if (!items.empty()) std::memcpy(host.data() + o_items, items.data(), items.size() * sizeof(DevItem));
   std::memcpy(host.data() + o_wg, wg_ptr.data(), wg_ptr.size() * sizeof(int32_t));
@@ -381,18 +403,18 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     std::memcpy(host.data() + o_slots, h_slots.data(), h_slots.size() * sizeof(uint16_t));
     std::memcpy(host.data() + o_ids, h_ids.data(), h_ids.size() * sizeof(int32_t));
   }
-  if (!gq.empty()) std::memcpy(host.data() + o_gq, gq.data(), gq.size() * sizeof(GatherEntry));
-  std::memcpy(host.data() + o_gqp, gq_ptr.data(), gq_ptr.size() * sizeof(int32_t));
-  std::memcpy(host.data() + o_gqn, gq_chunks.data(), gq_chunks.size() * sizeof(int32_t));
-  if (!gqw.empty()) std::memcpy(host.data() + o_gqw, gqw.data(), gqw.size() * sizeof(GatherEntry));
-  std::memcpy(host.data() + o_gqwp, gqw_ptr.data(), gqw_ptr.size() * sizeof(int32_t));
-  std::memcpy(host.data() + o_gqwn, gqw_chunks.data(), gqw_chunks.size() * sizeof(int32_t));
+  if (!gr.empty()) std::memcpy(host.data() + o_gr, gr.data(), gr.size() * sizeof(GatherRun));
+  std::memcpy(host.data() + o_grp, gr_ptr.data(), gr_ptr.size() * sizeof(int32_t));
+  std::memcpy(host.data() + o_gri, gr_info.data(), gr_info.size() * sizeof(int32_t));
   if (hipMemcpy(p->d_meta, host.data(), total, hipMemcpyHostToDevice) != hipSuccess ||
       (p->d_partials && hipMemset(p->d_partials, 0, part_floats * sizeof(float)) != hipSuccess)) {
     emb_plan_destroy(p);
     return EMB_ERR_DEVICE;
   }
-  p->lds_bytes = staged ? static_cast<int>(L) + kMetaReserve : 0;
+  // LDS: the staged slices' rows and metadata, and (after them) the worker's gather runs
+  const int run_bytes = max_runs * static_cast<int>(sizeof(GatherRun));
+  p->staged = staged;
+  p->lds_bytes = std::max(staged ? static_cast<int>(L) + kMetaReserve : 0, run_bytes);
   if (prepare_lookup_kernels(std::max(p->lds_bytes, kMetaReserve)) != 0) {
     emb_plan_destroy(p);
     return EMB_ERR_DEVICE;
@@ -407,8 +429,11 @@ emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights)
     if (!weights[t] || (reinterpret_cast<uintptr_t>(weights[t]) & 15u) != 0) return EMB_ERR_INVALID_ARGUMENT;
   }
   for (int32_t t = 0; t < plan->T; ++t) plan->h_tables[t].w = weights[t];
+  for (GatherRun& r : plan->h_gr) r.w = weights[r.table];
   if (hipMemcpy(plan->d_tables, plan->h_tables.data(), plan->T * sizeof(DevTable), hipMemcpyHostToDevice) !=
-      hipSuccess)
+          hipSuccess ||
+      (!plan->h_gr.empty() && hipMemcpy(plan->d_gr, plan->h_gr.data(), plan->h_gr.size() * sizeof(GatherRun),
+                                        hipMemcpyHostToDevice) != hipSuccess))
     return EMB_ERR_DEVICE;
   plan->bound = true;
   return EMB_OK;
@@ -445,13 +470,10 @@ emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t*
   a.lds_rows = plan->lds_rows;
   a.n_items = static_cast<int32_t>(plan->plan.slices.size());
   a.trace = plan->d_trace;
-  a.gq = plan->d_gq;
-  a.gq_ptr = plan->d_gq_ptr;
-  a.gq_chunks = plan->d_gq_chunks;
-  a.gqw = plan->d_gqw;
-  a.gqw_ptr = plan->d_gqw_ptr;
-  a.gqw_chunks = plan->d_gqw_chunks;
-  return st(launch_lookup(a, plan->G, plan->f16, plan->K, plan->lds_bytes, stream));
+  a.gr = plan->d_gr;
+  a.gr_ptr = plan->d_gr_ptr;
+  a.gr_info = plan->d_gr_info;
+  return st(launch_lookup(a, plan->G, plan->f16, plan->staged, plan->K, plan->lds_bytes, stream));
 }
 
 emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_bad) {

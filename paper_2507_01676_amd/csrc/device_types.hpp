@@ -34,14 +34,20 @@ struct DevTable {
   int32_t pad;
 };
 
-// One gather slice in a worker's chunk queue: the queue's chunks from chunk_base on
-// are runs of `cb` bags of item `item` (counted at the plan's max batch).
-struct GatherEntry {
-  int32_t item;
-  int32_t chunk_base;
+// One gather slice in a worker's queue, self-contained so that a worker can hold its
+// whole queue in LDS: from chunk_base on, the queue's chunks are runs of `cb` bags
+// (counted at the plan's max batch) of batch slice j of k of table `table`.
+struct GatherRun {
+  const void* w;        // the table's rows (set when weights are bound)
+  int64_t rows;
+  int32_t table;
+  int32_t j, k;
   int32_t cb;
-  int32_t pad;
+  int32_t chunk_base;
+  int32_t pad[3];
 };
+static_assert(sizeof(GatherRun) == 48, "GatherRun is staged as three 16-byte pieces");
+constexpr int kMaxRunsPerWorker = 1024;   // a worker's gather runs held in LDS at once
 
 struct LookupArgs {
   const DevItem* items;
@@ -64,12 +70,9 @@ struct LookupArgs {
   int32_t lds_rows;             // LDS bytes for rows (the budget L)
   int32_t n_items;
   unsigned long long* trace;    // optional timers (see kTraceWorker), nullptr = off
-  const GatherEntry* gq;        // SW-mode gather chunk queues, worker-major
-  const int32_t* gq_ptr;        // [K + 1] entry ranges per worker
-  const int32_t* gq_chunks;     // [K] chunks per worker
-  const GatherEntry* gqw;       // wave-mode gather chunk queues
-  const int32_t* gqw_ptr;
-  const int32_t* gqw_chunks;
+  const GatherRun* gr;          // gather runs, worker-major: wave-mode runs first, then SW-mode runs
+  const int32_t* gr_ptr;        // [K + 1] run ranges per worker
+  const int32_t* gr_info;       // [K][4]: wave-mode runs, wave-mode chunks, SW-mode chunks, 0
 };
 
 // Timer layout (100 MHz real-time counter ticks):
@@ -80,7 +83,7 @@ struct LookupArgs {
 constexpr int kTraceWorker = 2 + kBlock / 64;
 
 // Host-callable launchers (defined in lookup.hip).
-int launch_lookup(const LookupArgs& a, int G, bool f16, int grid, int lds_bytes, void* stream);
+int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, int grid, int lds_bytes, void* stream);
 int prepare_lookup_kernels(int lds_bytes);
 int launch_dedup_probe(const int64_t* idx, int n, int32_t* uniq, int32_t* inv, int32_t* n_uniq, void* stream);
 int launch_hot_probe(const int32_t* keys, const uint16_t* slots, int hash_log2, const int64_t* idx, int n,

@@ -856,69 +856,224 @@ __device__ __attribute__((noinline)) void dedup_item(const LookupArgs& a, const 
 
 __device__ __forceinline__ unsigned long long now_ticks() { return __builtin_amdgcn_s_memrealtime(); }
 
-// Chunks c = first, first + step, ... of one worker's gather queue (entries
-// [e, e_end), chunk c of entry x = bags [bs + (c - base) cb, + cb) of its slice).
-struct ChunkSrc {
-  const LookupArgs* a;
-  GMEM const GatherEntry* gq;
-  GMEM const DevItem* items;
-  int e, e_end, c, step, nchunks;
+// A run of bags of one gather run: run e of the worker's queue, bags [bs, be).
+struct SegRef {
+  int e, bs, be;
+};
 
-  __device__ __forceinline__ bool next(Seg& sg) {
+// Chunks c = first, first + step, ... of one worker's gather queue held in LDS (runs
+// [e, e_end); chunk c of run x is bags [bs + (c - chunk_base) cb, + cb) of its slice,
+// clipped to the slice at the runtime batch).  Only LDS is read.
+struct RunQueue {
+  const LMEM GatherRun* r;
+  int e, e_end, c, step, nchunks, B;
+  __device__ __forceinline__ bool next(SegRef& s) {
     while (c < nchunks) {
-      while (e + 1 < e_end && gq[e + 1].chunk_base <= c) ++e;
-      const GatherEntry ge = gq[e];
-      const DevItem it = items[ge.item];
-      const int bs = slice_lo(it.j, it.k, a->B), be = slice_lo(it.j + 1, it.k, a->B);
-      const int c0 = bs + (c - ge.chunk_base) * ge.cb;
-      const int c1 = min(be, c0 + ge.cb);
+      while (e + 1 < e_end && r[e + 1].chunk_base <= c) ++e;
+      const int bs = slice_lo(r[e].j, r[e].k, B), be = slice_lo(r[e].j + 1, r[e].k, B);
+      const int c0 = bs + (c - r[e].chunk_base) * r[e].cb;
+      const int c1 = min(be, c0 + r[e].cb);
       c += step;
-      if (c0 >= c1) continue;
-      const DevTable tb = a->tables[it.table];
-      sg.w = as_global(static_cast<const char*>(tb.w));
-      sg.rows = static_cast<uint64_t>(tb.rows);
-      sg.off = as_global(a->offsets) + static_cast<int64_t>(it.table) * a->B;
-      sg.ob = as_global(a->out) + static_cast<int64_t>(it.table) * a->E;
-      sg.bs = c0;
-      sg.be = c1;
-      return true;
+      if (c0 < c1) {
+        s.e = e;
+        s.bs = c0;
+        s.be = c1;
+        return true;
+      }
     }
     return false;
   }
 };
 
+// A segment's first loads: where its lookups start and end, and the ends of its
+// first G bags (lane i: end of bag bs + i).
+struct SegHead {
+  int64_t p, pend, win;
+  __device__ __forceinline__ void issue(GMEM const int64_t* off, const SegRef& s, int lane_sw) {
+    p = off[s.bs];
+    pend = off[s.be];
+    win = off[min(s.bs + 1 + lane_sw, s.be)];
+  }
+};
+
+// SW mode over the stream of segments a RunQueue yields (gather rows).  Steps run on
+// across segment boundaries without a pause: a segment's head (SegHead) is loaded two
+// segments ahead and its first ids by the last step of the segment before it, so a
+// step's single wait covers everything the next step needs.  Per bag the order of
+// additions is the lookup order, as in walk_seq.
+template <int G, bool F16>
+__device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ indices,
+                                            GMEM const int64_t* __restrict__ offsets, GMEM float* __restrict__ out,
+                                            int E, int B, int64_t ostride, int lane_sw, FGather& f, RunQueue& q) {
+  constexpr int NA = F16 ? 8 : 4;
+  SegRef cur, s1, s2;
+  SegHead h0, h1, h2;
+  auto off_of = [&](const SegRef& s) -> GMEM const int64_t* {
+    return offsets + static_cast<int64_t>(q.r[s.e].table) * B;
+  };
+  if (!q.next(cur)) return;
+  h0.issue(off_of(cur), cur, lane_sw);
+  bool has1 = q.next(s1);
+  if (has1) h1.issue(off_of(s1), s1, lane_sw);
+  bool has2 = has1 && q.next(s2);
+  if (has2) h2.issue(off_of(s2), s2, lane_sw);
+  wait_all();
+
+  GMEM const int64_t* off;
+  GMEM float* ob;
+  int be, wb, b;
+  int64_t p, pend, win, win2;
+  Acc<F16> acc;
+  acc_zero(acc);
+  auto open = [&]() {   // make cur (head h0) the current segment
+    const LMEM GatherRun& g = q.r[cur.e];
+    f.w = as_global(static_cast<const char*>(g.w));
+    f.rows = static_cast<uint64_t>(g.rows);
+    off = offsets + static_cast<int64_t>(g.table) * B;
+    ob = out + static_cast<int64_t>(g.table) * E + lane_sw * NA;
+    be = cur.be;
+    wb = cur.bs;
+    b = cur.bs;
+    p = h0.p;
+    pend = h0.pend;
+    win = h0.win;
+    win2 = off[min(wb + G + 1 + lane_sw, be)];
+  };
+  auto advance = [&]() {
+    cur = s1;
+    h0 = h1;
+    s1 = s2;
+    h1 = h2;
+    has1 = has2;
+    has2 = has1 && q.next(s2);
+    if (has2) h2.issue(off_of(s2), s2, lane_sw);
+  };
+  auto flush = [&]() {   // the bags left in the segment end here (the last one holds acc)
+    for (; b < be; ++b) {
+      if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+      acc_zero(acc);
+    }
+  };
+  auto end_of = [&](int bb) -> int64_t {
+    const int d = bb - wb;
+    if (d < G) return __shfl(win, d, G);
+    if (d < 2 * G) return __shfl(win2, d - G, G);
+    return off[min(bb + 1, be)];   // more than G empty bags within one step
+  };
+  // the first segment with lookups
+  while (true) {
+    open();
+    if (p < pend) break;
+    flush();
+    if (!has1) return;
+    advance();
+  }
+  Ids<G> ids;
+  ids.load(indices, p, 1, pend, p, lane_sw);
+  int64_t bag_end = end_of(b);
+  wait_all();
+  while (true) {
+    const int n = static_cast<int>(min64(kU, pend - p));
+    int32_t ix[kU];
+    ids.resolve(f, lane_sw, ix);
+    uint4 raw[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) f.issue(ix[u], 0, raw[u]);
+    const int64_t pn = p + n;
+    const bool seg_end = pn >= pend;
+    // the next step's ids: more of this segment, or the start of the next one
+    if (!seg_end)
+      ids.load(indices, pn, 1, pend, p, lane_sw);
+    else if (has1)
+      ids.load(indices, h1.p, 1, h1.pend, h1.p, lane_sw);
+    win2 = off[min(wb + G + 1 + lane_sw, be)];
+    wait_all();   // the one wait of the step
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      if (u < n) {
+        while (p + u == bag_end) {
+          if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+          acc_zero(acc);
+          ++b;
+          bag_end = end_of(b);
+        }
+        acc_add(acc, f.take(ix[u], 0, raw[u]));
+      }
+    }
+    if (b - wb >= G) {
+      if (b - wb < 2 * G) {
+        wb += G;
+        win = win2;
+      } else {
+        wb = b;
+        win = off[min(b + 1 + lane_sw, be)];
+      }
+    }
+    p = pn;
+    if (seg_end) {
+      flush();
+      if (!has1) return;
+      bool reload = false;   // the ids in flight belong to an empty segment
+      while (true) {
+        advance();
+        open();
+        if (p < pend) break;
+        flush();
+        reload = true;
+        if (!has1) return;
+      }
+      if (reload) ids.load(indices, p, 1, pend, p, lane_sw);
+      bag_end = end_of(b);
+    }
+  }
+}
+
 // Gather slices.  A worker's gather slices are cut into two queues of chunks (runs of
 // bags of one slice): long-bag slices (wave mode) and the rest (SW mode).  Wavefront v
 // takes wave-mode chunks v, v + 16, ...; SW s takes SW-mode chunks s, s + NSW, ...  The
 // chunks are small, so every SW samples every slice of the worker: the split stays
-// even when per-lookup cost differs between tables (cache-resident vs HBM-bound).
+// even when per-lookup cost differs between tables (cache-resident vs HBM-bound).  The
+// worker's runs are first copied into LDS (`lds`), so that finding a chunk's table and
+// bags costs no memory round trip.
 template <int G, bool F16>
-__device__ __forceinline__ void gather_phase(const LookupArgs& a, GMEM const DevItem* items, const Lane& l, int wg) {
+__device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, const Lane& l, int wg) {
   constexpr int NSW = kBlock / G;
+  GMEM const int32_t* gptr = as_global(a.gr_ptr);
+  const int r0 = gptr[wg], nr = gptr[wg + 1] - r0;
+  GMEM const int32_t* info = as_global(a.gr_info) + 4 * wg;
+  const int n_wave = info[0], wave_chunks = info[1], sw_chunks = info[2];
+  {
+    gchar* src = reinterpret_cast<gchar*>(as_global(a.gr) + r0);
+    for (int q = l.tid; q < 3 * nr; q += kBlock) sts16(lds + 16 * q, ldg16(src + 16 * q));
+  }
+  __syncthreads();
+  const LMEM GatherRun* runs = reinterpret_cast<const LMEM GatherRun*>(lds);
   GMEM const int64_t* idx = as_global(a.indices);
+  GMEM const int64_t* offsets = as_global(a.offsets);
+  GMEM float* out = as_global(a.out);
   const int64_t ost = static_cast<int64_t>(a.T) * a.E;
   DevTable tb0;
   tb0.w = nullptr;
   tb0.rows = 0;
   const RowBase rb0 = row_base(a, tb0, l);
   {  // wave mode
-    GMEM const int32_t* gptr = as_global(a.gqw_ptr);
-    ChunkSrc src{&a, as_global(a.gqw), items, gptr[wg], gptr[wg + 1], l.wave, kNumWaves, as_global(a.gqw_chunks)[wg]};
-    Seg sg;
-    while (src.next(sg)) {
+    RunQueue q{runs, 0, n_wave, l.wave, kNumWaves, wave_chunks, a.B};
+    SegRef s;
+    while (q.next(s)) {
       FGather f;
       static_cast<RowBase&>(f) = rb0;
-      f.w = sg.w;
-      f.rows = sg.rows;
-      walk_wave<G, F16>(idx, sg.off, sg.bs, sg.be, sg.ob, ost, l.lane_sw, l.sw_w, f);
+      const LMEM GatherRun& g = runs[s.e];
+      f.w = as_global(static_cast<const char*>(g.w));
+      f.rows = static_cast<uint64_t>(g.rows);
+      walk_wave<G, F16>(idx, offsets + static_cast<int64_t>(g.table) * a.B, s.bs, s.be,
+                        out + static_cast<int64_t>(g.table) * a.E, ost, l.lane_sw, l.sw_w, f);
     }
   }
   {  // SW mode
-    GMEM const int32_t* gptr = as_global(a.gq_ptr);
-    ChunkSrc src{&a, as_global(a.gq), items, gptr[wg], gptr[wg + 1], l.sw, NSW, as_global(a.gq_chunks)[wg]};
+    RunQueue q{runs, n_wave, nr, l.sw, NSW, sw_chunks, a.B};
     FGather f;
     static_cast<RowBase&>(f) = rb0;
-    walk_seq<G, F16>(idx, ost, l.lane_sw, f, src);
+    walk_stream<G, F16>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
   }
 }
 
@@ -959,7 +1114,8 @@ __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
     }
   }
   if (tw && l.tid == 0) tw[1] = now_ticks();
-  gather_phase<G, F16>(a, items, l, wg);
+  __syncthreads();   // staged slices are done with LDS
+  gather_phase<G, F16>(a, (lchar*)smem_raw, l, wg);
   if (tw && (l.tid & (kWave - 1)) == 0) tw[2 + l.wave] = now_ticks();
 }
 
@@ -1088,8 +1244,8 @@ int prepare_lookup_kernels(int lds_bytes) {
   return 0;
 }
 
-int launch_lookup(const LookupArgs& a, int G, bool f16, int grid, int lds_bytes, void* stream) {
-  KernelFn k = pick_any(G, f16, lds_bytes > 0);
+int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, int grid, int lds_bytes, void* stream) {
+  KernelFn k = pick_any(G, f16, staged);
   if (!k) return 2;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kBlock), lds_bytes, static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? 0 : 4;
