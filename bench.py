@@ -7,10 +7,16 @@ R distinct batches are cycled.  Prints ONE JSON line:
 
   value            lookups/s over the K timed steps (whole job, one GPU)
   queries_per_s    samples/s (the paper's TPS)
-  p99_us           nearest-rank P99 of the per-batch latency (HIP events around each launch)
-  useful_hbm_frac  (lookups x row bytes)/s over the 8 TB/s HBM peak
-  roofline         algorithmic bytes per launch (rows + indices + offsets + output) over the
-                   mean launch duration, against the 8 TB/s HBM peak
+  p99_us           nearest-rank P99 of the per-batch latency (a separate pass with HIP
+                   events around each launch; mean_us is that pass's mean)
+  launch_us        average launch duration over the K timed steps (one HIP event pair on
+                   the launch stream around the back-to-back launches)
+  useful_hbm_frac  (lookups x row bytes) per launch_us over the 8 TB/s HBM peak
+  roofline         algorithmic bytes per launch (rows + indices + offsets + output) over
+                   launch_us, against the 8 TB/s HBM peak; traffic = measured HBM bytes per
+                   launch (profiles/traffic_<workload>.json: FETCH_SIZE and WRITE_SIZE, each
+                   scaled by its reading for a 1 GiB device copy) when the committed counters
+                   were taken on this kernel source, else null
   cpu_baseline     the CPU oracle timed on a bounded sample of the same workload
 
   python bench.py [--config 2] [--steps 200] [--warmup 20]
@@ -174,7 +180,10 @@ def main():
     R = args.batches or (4 if args.config == 5 else 8)
     t0 = time.time()
     log(f"workload {c.cfg_id}: {c.name}; generating {R} batches + statistics")
-    batches = [W.gen_batch(c, i) for i in range(R)]
+    batches = []
+    for i in range(R):
+        batches.append(W.gen_batch(c, i))
+        log(f"batch {i}: {batches[-1].n_lookups} lookups ({time.time() - t0:.1f}s)")
     stats = W.history_stats(c)
     log(f"inputs generated in {time.time() - t0:.1f}s; filling {sum(c.rows) * c.row_bytes / 1e9:.2f} GB of tables")
     dt = torch.float16 if c.dtype == "f16" else torch.float32
@@ -212,18 +221,31 @@ def main():
     assert plan.check_errors() == 0
 
     K = args.steps
+    # per-batch latency (P99): an event pair around each launch
     ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
     ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
     torch.cuda.synchronize()
-    wall0 = time.perf_counter()
     for i in range(K):
         ip, op = ptrs[i % R]
         ev0[i].record(stream)
         plan.lookup_ptr(ip, op, B, outp, sp)
         ev1[i].record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
     lat_ms = [ev0[i].elapsed_time(ev1[i]) for i in range(K)]
+
+    # throughput: the K timed steps back to back, synchronized on both sides; one event
+    # pair on the launch stream gives the average launch duration
+    e_start, e_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e_start.record(stream)
+    for i in range(K):
+        ip, op = ptrs[i % R]
+        plan.lookup_ptr(ip, op, B, outp, sp)
+    e_stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    launch_ms = e_start.elapsed_time(e_stop) / K
     total_lookups = sum(n_look[i % R] for i in range(K))
     mean_ms = sum(lat_ms) / K
 
@@ -231,7 +253,7 @@ def main():
     alg = [W.algorithmic_bytes(c, n_look[i % R])["total"] for i in range(K)]
     alg_mean = sum(alg) / K
     useful_mean = sum(n_look[i % R] for i in range(K)) * R_b / K
-    achieved = alg_mean / (mean_ms * 1e-3) / 1e9
+    achieved = alg_mean / (launch_ms * 1e-3) / 1e9
     src_hash = kernel_source_hash()
     workload = f"workload{c.cfg_id}"
     traffic = load_traffic(workload, src_hash)
@@ -261,10 +283,13 @@ def main():
         "queries_per_s": B * K / wall,
         "p99_us": p99(lat_ms) * 1e3,
         "mean_us": mean_ms * 1e3,
-        "useful_gbps": useful_mean / (mean_ms * 1e-3) / 1e9,
-        "useful_hbm_frac": useful_mean / (mean_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "launch_us": launch_ms * 1e3,
+        "useful_gbps": useful_mean / (launch_ms * 1e-3) / 1e9,
+        "useful_hbm_frac": useful_mean / (launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": traffic,
+                     "traffic_gbps": None if traffic is None else traffic / (launch_ms * 1e-3) / 1e9,
                      "algorithmic_bytes_per_launch": alg_mean, "kernel": "lookup_kernel"},
         "copy_gbps": copy_gbps,
         "plan": {"strategies": info["n_strategy"], "items": info["num_items"], "lif_milli": info["lif_milli"],

@@ -18,6 +18,14 @@ LIB_PATH = os.environ.get("EMBX_LIBRARY") or os.path.join(_HERE, "libembx.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"embx native library missing: {LIB_PATH} (build it with: python paper_2507_01676_amd/build.py)")
 
+# PyTorch ships its own HIP runtime under the same soname as the system one; it must be
+# the one in the process (loaded first), so that torch's device pointers and streams
+# and the library's kernels live in one runtime.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 # ---------------------------------------------------------------- constants (include/embx.h)

@@ -1,0 +1,256 @@
+"""Calibration of the planner's cost model on the device it runs on (Eq. (2)).
+
+The paper prices each table-to-core assignment with a cost linear in the
+table's parameters and fits the coefficients by ordinary least squares on
+measured runs (Sec. III-A).  Here the measured runs are lookups on synthetic
+workloads with every table forced to one strategy and the per-slice timers of
+``emb_plan_set_trace`` switched on; the coefficients are the planner's beta
+vector (picoseconds), in the layout of ``include/embx.h``:
+
+    G0 G1 L0 L1 S I H0 P D0 D1
+
+and each strategy's cost of one slice with lambda lookups is
+
+    GATHER   G0 + G1 lambda
+    LDS      L0 + S mu R + L1 lambda                 (mu rows staged)
+    chunk    L0 + S mu R + I lambda + L1 lambda / c  (one of c row chunks)
+    HOT      H0 + S C R + lambda (P + h L1 + (1 - h) G1)
+    DEDUP    D0 + D1 lambda + G1 u lambda
+
+Shared coefficients are fitted once and then held fixed: GATHER first (G0,
+G1 from each worker's gather-phase time against its gather slices and
+lookups), LDS next (L0, S, L1 from whole-table slices, then I from what they
+leave of the row-chunk slices' times, so that I also carries the chunk
+combine), then HOT (H0, P) and DEDUP (D0, D1) on what their costs leave after
+the shared terms.
+Every fit is ``numpy.linalg.lstsq``.
+
+``fit_beta`` is plain host arithmetic; ``collect`` runs lookups on the current
+device and needs the extension.  ``python -m paper_2507_01676_amd.calibrate``
+runs both on the synthetic workloads and prints the fitted vector.
+"""
+from __future__ import annotations
+
+import json
+import sys
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+G0, G1, L0, L1, S, I, H0, P, D0, D1 = range(10)
+NBETA = 10
+LDS, HOT, DEDUP, GATHER = 0, 1, 2, 3
+TICK_PS = 10_000.0          # the kernel timers count a 100 MHz clock
+
+
+@dataclass
+class SliceSample:
+    """One staged slice (LDS, HOT or DEDUP) and its measured time."""
+    strat: int
+    lam: float              # lookups of the slice in the measured batch
+    mu: float = 0.0         # LDS: rows staged;  HOT: hot rows staged (C)
+    R: int = 0              # row bytes
+    c: int = 1              # LDS: number of row chunks of the table
+    h: float = 0.0          # HOT: fraction of the table's lookups on the staged rows
+    u: float = 1.0          # DEDUP: distinct rows per lookup
+    ps: float = 0.0         # measured time
+
+
+@dataclass
+class WorkerSample:
+    """One worker's gather phase: its gather slices, their lookups and its time."""
+    n_slices: int
+    lam: float
+    ps: float
+
+
+@dataclass
+class Samples:
+    slices: List[SliceSample] = field(default_factory=list)
+    workers: List[WorkerSample] = field(default_factory=list)
+
+
+def _lstsq(A: np.ndarray, y: np.ndarray) -> np.ndarray:
+    x, *_ = np.linalg.lstsq(A, y, rcond=None)
+    return x
+
+
+def fit_beta(s: Samples, base: Optional[Sequence[float]] = None) -> List[float]:
+    """OLS fit of the beta vector; coefficients with no samples keep ``base``'s value."""
+    b = list(base) if base is not None else [0.0] * NBETA
+    if s.workers:
+        A = np.array([[w.n_slices, w.lam] for w in s.workers], dtype=np.float64)
+        y = np.array([w.ps for w in s.workers], dtype=np.float64)
+        b[G0], b[G1] = (float(v) for v in _lstsq(A, y))
+    whole = [x for x in s.slices if x.strat == LDS and x.c == 1]
+    if whole:
+        A = np.array([[1.0, x.mu * x.R, x.lam] for x in whole])
+        y = np.array([x.ps for x in whole])
+        b[L0], b[S], b[L1] = (float(v) for v in _lstsq(A, y))
+    chunks = [x for x in s.slices if x.strat == LDS and x.c > 1]
+    if chunks:
+        # I on what the whole-table terms leave; it absorbs the chunk combine as well
+        A = np.array([[x.lam] for x in chunks])
+        y = np.array([x.ps - b[L0] - b[S] * x.mu * x.R - b[L1] * x.lam / x.c for x in chunks])
+        b[I] = float(_lstsq(A, y)[0])
+    hot = [x for x in s.slices if x.strat == HOT]
+    if hot:
+        A = np.array([[1.0, x.lam] for x in hot])
+        y = np.array([x.ps - b[S] * x.mu * x.R - x.lam * (x.h * b[L1] + (1.0 - x.h) * b[G1]) for x in hot])
+        b[H0], b[P] = (float(v) for v in _lstsq(A, y))
+    dd = [x for x in s.slices if x.strat == DEDUP]
+    if dd:
+        A = np.array([[1.0, x.lam] for x in dd])
+        y = np.array([x.ps - b[G1] * x.u * x.lam for x in dd])
+        b[D0], b[D1] = (float(v) for v in _lstsq(A, y))
+    return b
+
+
+def predict(b: Sequence[float], x) -> float:
+    """The cost model's time for one sample (the same formulas the fit inverts)."""
+    if isinstance(x, WorkerSample):
+        return b[G0] * x.n_slices + b[G1] * x.lam
+    if x.strat == LDS:
+        extra = b[I] * x.lam if x.c > 1 else 0.0
+        return b[L0] + b[S] * x.mu * x.R + extra + b[L1] * x.lam / x.c
+    if x.strat == HOT:
+        return b[H0] + b[S] * x.mu * x.R + x.lam * (b[P] + x.h * b[L1] + (1.0 - x.h) * b[G1])
+    if x.strat == DEDUP:
+        return b[D0] + b[D1] * x.lam + b[G1] * x.u * x.lam
+    raise ValueError(x.strat)
+
+
+# ---------------------------------------------------------------- measurement
+
+def _plan_items(text: str):
+    out = []
+    for ln in text.splitlines():
+        if ln.startswith("item "):
+            f = ln.split()
+            out.append(dict(wg=int(f[1]), t=int(f[2]), strat=int(f[3]), chunk=int(f[4]), nchunks=int(f[5]),
+                            r0=int(f[6]), r1=int(f[7]), k=int(f[8]), j=int(f[9]), C=int(f[10])))
+    return out
+
+
+def measure(plan, indices, offsets, batch: int, out, host_offsets: np.ndarray, stats, R: int,
+            warm: int = 3) -> Samples:
+    """Runs one traced launch of ``plan`` and turns its timers into samples.
+
+    ``host_offsets`` is the batch's CSR offsets on the host (to count each
+    slice's lookups); ``stats`` the per-table statistics the plan was made from.
+    """
+    import torch
+    for _ in range(warm):
+        plan.lookup(indices, offsets, batch, out)
+    n = plan.trace_size()
+    buf = torch.zeros(n, dtype=torch.int64, device=indices.device)
+    plan.set_trace(buf)
+    plan.lookup(indices, offsets, batch, out)
+    torch.cuda.synchronize()
+    plan.set_trace(None)
+    tr = buf.cpu().numpy()
+    info = plan.info()
+    K = info["num_workers"]
+    per = 2 + 1024 // 64
+    tw = tr[:K * per].reshape(K, per)
+    ti = tr[K * per:].reshape(-1, 2)
+    items = _plan_items(plan.serialize())
+    T = len(stats)
+    s = Samples()
+    gcount = np.zeros(K, dtype=np.int64)
+    glam = np.zeros(K, dtype=np.float64)
+    for i, it in enumerate(items):
+        bs, be = it["j"] * batch // it["k"], (it["j"] + 1) * batch // it["k"]
+        t = it["t"]
+        lam = float(host_offsets[t * batch + be] - host_offsets[t * batch + bs])
+        if it["strat"] == GATHER:
+            gcount[it["wg"]] += 1
+            glam[it["wg"]] += lam
+            continue
+        if be <= bs:
+            continue
+        ps = float(ti[i, 1] - ti[i, 0]) * TICK_PS
+        st = stats[t]
+        hot_f = getattr(st, "hot_freq", None)
+        h = float(np.sum(hot_f[:it["C"]])) if (hot_f is not None and it["C"] > 0) else 0.0
+        u = float(getattr(st, "unique_frac", 1.0))
+        mu = float(it["r1"] - it["r0"]) if it["strat"] == LDS else float(it["C"])
+        s.slices.append(SliceSample(it["strat"], lam, mu, R, it["nchunks"], h, u if 0 < u <= 1 else 1.0, ps))
+    gat = (tw[:, 2:].max(axis=1) - tw[:, 1]).astype(np.float64) * TICK_PS
+    for w in range(K):
+        if gcount[w]:
+            s.workers.append(WorkerSample(int(gcount[w]), float(glam[w]), float(gat[w])))
+    return s
+
+
+def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("gather", "lds", "hot", "dedup"),
+            lds_max_bytes: int = 32 << 20, log=print) -> Samples:
+    """Measures the synthetic workloads with each strategy forced on every table."""
+    import torch
+    import workloads as W
+    from . import Plan, fill_table
+    code = {"lds": LDS, "hot": HOT, "dedup": DEDUP, "gather": GATHER}
+    allS = Samples()
+    for cfg in configs:
+        c = W.make_config(cfg)
+        bt = W.gen_batch(c, 0)
+        stats = W.history_stats(c)
+        dt = torch.float16 if c.dtype == "f16" else torch.float32
+        ws = []
+        for t, m in enumerate(c.rows):
+            w = torch.empty((m, c.E), dtype=dt, device="cuda")
+            fill_table(w, t, c.value_seeds[t], c.lo, c.hi)
+            ws.append(w)
+        idx = torch.from_numpy(bt.indices).cuda()
+        off = torch.from_numpy(bt.offsets).cuda()
+        out = torch.empty((c.batch, c.T, c.E), device="cuda")
+        for name in strategies:
+            force = [code[name]] * c.T
+            if name == "lds":
+                # LDS (row chunks) only on the tables of at most lds_max_bytes; the rest
+                # gather, and those gather workers are not samples (their time follows
+                # the staged slices on the same workers)
+                force = [LDS if m * c.row_bytes <= lds_max_bytes else GATHER for m in c.rows]
+            plan = Plan(c.rows, c.E, c.dtype, stats, c.batch, force=force).bind(ws)
+            s = measure(plan, idx, off, c.batch, out, bt.offsets, stats, c.row_bytes)
+            plan.close()
+            if name == "lds":
+                s.workers = []
+            log(f"workload {cfg} {name}: {len(s.slices)} slices, {len(s.workers)} gather workers")
+            allS.slices += s.slices
+            allS.workers += s.workers
+        del ws
+        torch.cuda.empty_cache()
+    return allS
+
+
+def main(argv=None) -> int:
+    import argparse
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--configs", type=int, nargs="+", default=[2, 3, 4])
+    ap.add_argument("--strategies", nargs="+", default=["gather", "lds", "hot", "dedup"])
+    ap.add_argument("--out", default=None, help="write the samples and the fit as JSON")
+    a = ap.parse_args(argv)
+    s = collect(a.configs, a.strategies, log=lambda m: print(m, file=sys.stderr, flush=True))
+    b = fit_beta(s)
+    names = ["G0", "G1", "L0", "L1", "S", "I", "H0", "P", "D0", "D1"]
+    for st, nm in ((LDS, "LDS"), (HOT, "HOT"), (DEDUP, "DEDUP")):
+        xs = [x for x in s.slices if x.strat == st]
+        if xs:
+            err = np.array([predict(b, x) - x.ps for x in xs])
+            print(f"{nm}: {len(xs)} slices, rms residual {np.sqrt(np.mean(err ** 2)) / 1e6:.2f} us", file=sys.stderr)
+    if s.workers:
+        err = np.array([predict(b, x) - x.ps for x in s.workers])
+        print(f"GATHER: {len(s.workers)} workers, rms residual {np.sqrt(np.mean(err ** 2)) / 1e6:.2f} us",
+              file=sys.stderr)
+    print(json.dumps(dict(zip(names, b))))
+    if a.out:
+        with open(a.out, "w") as f:
+            json.dump(dict(beta=dict(zip(names, b)), slices=[x.__dict__ for x in s.slices],
+                           workers=[x.__dict__ for x in s.workers]), f)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -221,18 +221,18 @@ struct Planner {
 
 }  // namespace
 
-std::array<double, B_COUNT> default_beta(int32_t R) {
+std::array<double, B_COUNT> default_beta(int32_t) {
   std::array<double, B_COUNT> b{};
-  b[B_G0] = 200000.0;
-  b[B_G1] = (static_cast<double>(R) * 32.0) / 0.7;
-  b[B_L0] = 200000.0;
-  b[B_L1] = static_cast<double>(R) / 0.3072;
-  b[B_S] = 32.0;
-  b[B_I] = 256.0;
-  b[B_H0] = 200000.0;
-  b[B_P] = 100.0;
-  b[B_D0] = 200000.0;
-  b[B_D1] = 4000.0;
+  b[B_G0] = 131000.0;
+  b[B_G1] = 10900.0;
+  b[B_L0] = 1670000.0;
+  b[B_L1] = 10950.0;
+  b[B_S] = 477.0;
+  b[B_I] = 8280.0;
+  b[B_H0] = 0.0;
+  b[B_P] = 2340.0;
+  b[B_D0] = 21600000.0;
+  b[B_D1] = 29400.0;
   return b;
 }
 

@@ -24,6 +24,16 @@ def _b(R=256):
     return OPL.default_beta(R)
 
 
+def _roofline_beta(R=256):
+    """Coefficients from bandwidths alone (a row at one CU's share of HBM, LDS at
+    128 B/clk), for special cases whose premise is that LDS beats HBM per lookup."""
+    b = [0.0] * OPL.NBETA
+    b[OPL.G0], b[OPL.G1] = 200000.0, R * 32.0 / 0.7
+    b[OPL.L0], b[OPL.L1], b[OPL.S], b[OPL.I] = 200000.0, R / 0.3072, 32.0, 256.0
+    b[OPL.H0], b[OPL.P], b[OPL.D0], b[OPL.D1] = 200000.0, 100.0, 200000.0, 4000.0
+    return b
+
+
 # ---------------------------------------------------------------- cost model cross-checks
 
 def test_cost_formulas_coincide_where_strategies_do():
@@ -189,7 +199,7 @@ def test_one_huge_table_is_split_over_all_workers():
 def test_tiny_tables_with_many_lookups_stay_in_lds():
     rows = [10, 40, 100, 300]
     stats = [OPL.Stat(20.0)] * 4
-    p = OPL.plan_reference(rows, 64, "f32", stats, 4096, 64)
+    p = OPL.plan_reference(rows, 64, "f32", stats, 4096, 64, OPL.Options(beta=_roofline_beta()))
     assert all(s.strat == OPL.LDS for s in p.slices)
 
 
