@@ -43,6 +43,7 @@ struct emb_plan {
   GatherRun* d_gr = nullptr;
   int32_t* d_gr_ptr = nullptr;
   int32_t* d_gr_info = nullptr;
+  const char* d_zero_row = nullptr;      // R zero bytes
   bool staged = false;                   // the plan has LDS / HOT / DEDUP slices
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
 };
@@ -373,7 +374,8 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   size_t o_gr = align_up(o_err + sizeof(unsigned long long), 256);
   size_t o_grp = align_up(o_gr + gr.size() * sizeof(GatherRun), 256);
   size_t o_gri = align_up(o_grp + gr_ptr.size() * sizeof(int32_t), 256);
-  size_t total = align_up(o_gri + gr_info.size() * sizeof(int32_t), 256);
+  size_t o_zero = align_up(o_gri + gr_info.size() * sizeof(int32_t), 256);
+  size_t total = align_up(o_zero + static_cast<size_t>(p->R), 256);
   if (hipMalloc(&p->d_meta, total) != hipSuccess) {
     delete p;
     return EMB_ERR_OUT_OF_MEMORY;
@@ -394,6 +396,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   p->d_gr = reinterpret_cast<GatherRun*>(p->d_meta + o_gr);
   p->d_gr_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_grp);
   p->d_gr_info = reinterpret_cast<int32_t*>(p->d_meta + o_gri);
+  p->d_zero_row = p->d_meta + o_zero;   // zeros: the host image is zero-filled
   std::vector<char> host(total, 0);
   if (!items.empty()) std::memcpy(host.data() + o_items, items.data(), items.size() * sizeof(DevItem));
   std::memcpy(host.data() + o_wg, wg_ptr.data(), wg_ptr.size() * sizeof(int32_t));
@@ -473,6 +476,8 @@ emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t*
   a.gr = plan->d_gr;
   a.gr_ptr = plan->d_gr_ptr;
   a.gr_info = plan->d_gr_info;
+  a.zero_row = plan->d_zero_row;
+  a.one = 1.0f;
   return st(launch_lookup(a, plan->G, plan->f16, plan->staged, plan->K, plan->lds_bytes, stream));
 }
 

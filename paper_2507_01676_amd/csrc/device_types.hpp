@@ -73,6 +73,8 @@ struct LookupArgs {
   const GatherRun* gr;          // gather runs, worker-major: wave-mode runs first, then SW-mode runs
   const int32_t* gr_ptr;        // [K + 1] run ranges per worker
   const int32_t* gr_info;       // [K][4]: wave-mode runs, wave-mode chunks, SW-mode chunks, 0
+  const void* zero_row;         // R zero bytes: the row an invalid id reads in the gather walkers
+  float one;                    // 1.0f, opaque to the compiler (fp16 rows are added as x * one + acc)
 };
 
 // Timer layout (100 MHz real-time counter ticks):

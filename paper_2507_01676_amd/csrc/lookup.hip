@@ -96,6 +96,21 @@ __device__ __forceinline__ void acc_add(Acc<true>& a, const uint4 r) {
   }
 }
 
+// fp16 halves added as x * one + acc with one = 1 at run time (opaque to the compiler):
+// the product is exact and the fma rounds once, so the sum is the same as widening and
+// adding, in one mixed-precision instruction per half instead of two
+__device__ __forceinline__ void acc_add(Acc<true>& a, const uint4 r, float one) {
+  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    a.v[2 * q] = __builtin_fmaf(__half2float(__ushort_as_half(static_cast<unsigned short>(w[q] & 0xffffu))), one,
+                                a.v[2 * q]);
+    a.v[2 * q + 1] = __builtin_fmaf(__half2float(__ushort_as_half(static_cast<unsigned short>(w[q] >> 16))), one,
+                                    a.v[2 * q + 1]);
+  }
+}
+__device__ __forceinline__ void acc_add(Acc<false>& a, const uint4 r, float) { acc_add(a, r); }
+
 template <bool F16>
 __device__ __forceinline__ void acc_add_f32(Acc<F16>& a, GMEM const float* p) {
 #pragma unroll
@@ -163,6 +178,8 @@ struct RowBase {
   bool active;            // this lane holds part of the row
   bool count;             // this slice reports out-of-range ids
   GMEM unsigned long long* err;
+  gchar* zero;            // R zero bytes (+ lane_c): what an invalid id reads in the gather walkers
+  float one;              // 1.0f from the launch arguments (see acc_add)
 
   __device__ __forceinline__ gchar* row(int32_t ix) const {
     return w + static_cast<int64_t>(ix > 0 ? ix : 0) * R + lane_c;
@@ -176,14 +193,16 @@ struct RowBase {
   }
 };
 
+// rows straight from HBM; an invalid id reads the zero row, so a row needs no masking
+// (lanes beyond the row read its first 16 bytes and are never stored)
 struct FGather : RowBase {
   static constexpr bool kPositional = false;
   using Raw = uint4;
   __device__ __forceinline__ void probe(const int32_t (&)[kU], int64_t, int, int32_t (&)[kU]) const {}
-  __device__ __forceinline__ void issue(int32_t ix, int32_t, Raw& r) const { r = ldg16(row(ix)); }
-  __device__ __forceinline__ uint4 take(int32_t ix, int32_t, const Raw& r) const {
-    return (ix >= 0 && active) ? r : zero16();
+  __device__ __forceinline__ void issue(int32_t ix, int32_t, Raw& r) const {
+    r = ldg16(ix >= 0 ? w + static_cast<int64_t>(ix) * R + lane_c : zero + lane_c);
   }
+  __device__ __forceinline__ uint4 take(int32_t, int32_t, const Raw& r) const { return r; }
 };
 
 // rows [r0, r1) of the table resident in LDS at `lds`; others contribute nothing here
@@ -388,17 +407,20 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
       const int64_t pn = p + n;
       ids.load(indices, pn, 1, pend, p, lane_sw);
       win2 = off[min(wb + G + 1 + lane_sw, be)];
+      // the current bag ends before the step's lookup u = rel (rel > kU: not in this step)
+      int rel = static_cast<int>(min64(bag_end - p, kU + 1));
       wait_all();   // the one wait of the step: rows, next ids and offsets window together
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         if (u < n) {
-          while (p + u == bag_end) {
+          while (u == rel) {
             if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
             acc_zero(acc);
             ++b;
             bag_end = end_of(b);
+            rel = static_cast<int>(min64(bag_end - p, kU + 1));
           }
-          acc_add(acc, f.take(ix[u], sl[u], raw[u]));
+          acc_add(acc, f.take(ix[u], sl[u], raw[u]), f.one);
         }
       }
       if (b - wb >= G) {
@@ -516,7 +538,7 @@ __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indic
     wait_all();   // the one wait of the step
 #pragma unroll
     for (int u = 0; u < kU; ++u)
-      if (u < n) acc_add(acc, f.take(ix[u], sl[u], raw[u]));
+      if (u < n) acc_add(acc, f.take(ix[u], sl[u], raw[u]), f.one);
     if (lastq) {
       acc_wave_reduce<G>(acc);
       if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
@@ -692,6 +714,8 @@ __device__ __forceinline__ RowBase row_base(const LookupArgs& a, const DevTable&
   rb.active = l.active;
   rb.count = true;
   rb.err = as_global(a.err);
+  rb.zero = as_global(static_cast<const char*>(a.zero_row));
+  rb.one = a.one;
   return rb;
 }
 
@@ -974,6 +998,8 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
   wait_all();
   while (true) {
     const int n = static_cast<int>(min64(kU, pend - p));
+    // the current bag ends before the step's lookup u = rel (rel > kU: not in this step)
+    int rel = static_cast<int>(min64(bag_end - p, kU + 1));
     int32_t ix[kU];
     ids.resolve(f, lane_sw, ix);
     uint4 raw[kU];
@@ -991,13 +1017,14 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       if (u < n) {
-        while (p + u == bag_end) {
+        while (u == rel) {
           if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
           acc_zero(acc);
           ++b;
           bag_end = end_of(b);
+          rel = static_cast<int>(min64(bag_end - p, kU + 1));
         }
-        acc_add(acc, f.take(ix[u], 0, raw[u]));
+        acc_add(acc, f.take(ix[u], 0, raw[u]), f.one);
       }
     }
     if (b - wb >= G) {
