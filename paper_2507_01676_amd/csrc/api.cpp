@@ -302,13 +302,14 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     }
   }
 
-  // gather run queues per worker, slices in plan order: wave-mode runs, then SW-mode
-  // runs.  SW-mode chunks carry about W / (4 NSW) expected lookups (W: the worker's
+  // gather run queues per worker, slices in plan order: wave-mode runs, then runs of
+  // tables whose bags hold at most one lookup (kChunkSingle bags per chunk: one step
+  // of a SW), then SW-mode runs.  SW-mode chunks carry about W / (4 NSW) expected lookups (W: the worker's
   // SW-mode lookups at the max batch), at least one full step (8) and at most 32, so
   // that each SW gets several chunks; wave-mode chunks carry about four wavefront
   // steps of lookups, fewer when that leaves some of the 16 wavefronts without one.
   std::vector<GatherRun>& gr = p->h_gr;
-  std::vector<int32_t> gr_ptr(K + 1, 0), gr_info(4 * static_cast<size_t>(K), 0);
+  std::vector<int32_t> gr_ptr(K + 1, 0), gr_info(8 * static_cast<size_t>(K), 0);
   int max_runs = 0;
   {
     const int nsw = kBlock / p->G;
@@ -322,19 +323,28 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
       for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
         if (items[i].strat != S_GATHER) continue;
         const double lk = static_cast<double>(slice_bags(items[i])) * std::max(1.0, stats[items[i].table].mean_pooling);
-        (items[i].mode ? Ww : Ws) += lk;
+        if (items[i].mode)
+          Ww += lk;
+        else if (stats[items[i].table].max_pooling > 1)
+          Ws += lk;
       }
       const double target = std::min(32.0, std::max(8.0, std::floor(Ws / (4.0 * nsw))));
       const double wtarget = std::min(wave_chunk, std::max(1.0, std::floor(Ww / nwaves)));
       gr_ptr[w] = static_cast<int32_t>(gr.size());
-      int64_t base[2] = {0, 0};
-      int32_t nrun[2] = {0, 0};
-      for (int pass = 1; pass >= 0; --pass) {   // wave mode (1) first
+      // classes, in queue order: 0 wave mode, 1 single-lookup bags, 2 SW mode
+      auto class_of = [&](const DevItem& d) -> int {
+        if (d.mode) return 0;
+        return stats[d.table].max_pooling <= 1 ? 1 : 2;
+      };
+      int64_t base[3] = {0, 0, 0};
+      int32_t nrun[3] = {0, 0, 0};
+      for (int cls = 0; cls < 3; ++cls) {
         for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
           const DevItem& d = items[i];
-          if (d.strat != S_GATHER || d.mode != pass) continue;
+          if (d.strat != S_GATHER || class_of(d) != cls) continue;
           const double s_t = std::max(1.0, stats[d.table].mean_pooling);
-          const int32_t cb = static_cast<int32_t>(std::max(1.0, std::floor((pass ? wtarget : target) / s_t)));
+          const int32_t cb = cls == 1 ? kChunkSingle
+                                      : static_cast<int32_t>(std::max(1.0, std::floor((cls == 0 ? wtarget : target) / s_t)));
           const int64_t nc = (slice_bags(d) + cb - 1) / cb;
           if (nc == 0) continue;
           GatherRun r{};
@@ -344,20 +354,23 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
           r.j = d.j;
           r.k = d.k;
           r.cb = cb;
-          r.chunk_base = static_cast<int32_t>(base[pass]);
+          r.chunk_base = static_cast<int32_t>(base[cls]);
           gr.push_back(r);
-          base[pass] += nc;
-          nrun[pass] += 1;
+          base[cls] += nc;
+          nrun[cls] += 1;
         }
       }
-      if (base[0] > INT32_MAX || base[1] > INT32_MAX || nrun[0] + nrun[1] > kMaxRunsPerWorker) {
+      if (base[0] > INT32_MAX || base[1] > INT32_MAX || base[2] > INT32_MAX ||
+          nrun[0] + nrun[1] + nrun[2] > kMaxRunsPerWorker) {
         delete p;
         return EMB_ERR_UNSUPPORTED;
       }
-      max_runs = std::max(max_runs, nrun[0] + nrun[1]);
-      gr_info[4 * w + 0] = nrun[1];
-      gr_info[4 * w + 1] = static_cast<int32_t>(base[1]);
-      gr_info[4 * w + 2] = static_cast<int32_t>(base[0]);
+      max_runs = std::max(max_runs, nrun[0] + nrun[1] + nrun[2]);
+      gr_info[8 * w + 0] = nrun[0];
+      gr_info[8 * w + 1] = static_cast<int32_t>(base[0]);
+      gr_info[8 * w + 2] = nrun[1];
+      gr_info[8 * w + 3] = static_cast<int32_t>(base[1]);
+      gr_info[8 * w + 4] = static_cast<int32_t>(base[2]);
     }
     gr_ptr[K] = static_cast<int32_t>(gr.size());
   }

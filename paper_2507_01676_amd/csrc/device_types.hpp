@@ -48,6 +48,7 @@ struct GatherRun {
 };
 static_assert(sizeof(GatherRun) == 48, "GatherRun is staged as three 16-byte pieces");
 constexpr int kMaxRunsPerWorker = 1024;   // a worker's gather runs held in LDS at once
+constexpr int kChunkSingle = 8;           // bags per chunk of a single-lookup-bag run (one SW step)
 
 struct LookupArgs {
   const DevItem* items;
@@ -72,7 +73,8 @@ struct LookupArgs {
   unsigned long long* trace;    // optional timers (see kTraceWorker), nullptr = off
   const GatherRun* gr;          // gather runs, worker-major: wave-mode runs first, then SW-mode runs
   const int32_t* gr_ptr;        // [K + 1] run ranges per worker
-  const int32_t* gr_info;       // [K][4]: wave-mode runs, wave-mode chunks, SW-mode chunks, 0
+  const int32_t* gr_info;       // [K][8]: wave-mode runs, wave-mode chunks, single-lookup runs,
+                                //         single-lookup chunks, SW-mode chunks, 0, 0, 0
   const void* zero_row;         // R zero bytes: the row an invalid id reads in the gather walkers
   float one;                    // 1.0f, opaque to the compiler (fp16 rows are added as x * one + acc)
 };

@@ -58,6 +58,7 @@ constexpr int kMetaUniq = kMetaInv + kTile * 2;       // DEDUP: int32[kTile]
 constexpr int kMetaScan = kMetaUniq + kTile * 4;      // DEDUP: int32[64]
 constexpr int kMetaBytes = kMetaScan + 256;
 static_assert(kMetaBytes == kMetaReserve, "LDS metadata layout");
+static_assert(kChunkSingle == kU, "a single-lookup chunk is one SW step");
 constexpr int kMetaHashKeys = 0;                      // HOT: int32[H], H <= 4096
 constexpr int kMetaHashSlots = 4096 * 4;              // HOT: uint16[H]
 
@@ -492,10 +493,9 @@ __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indic
   int wb = bs;
   int64_t win = off[min(bs + lane, be)];
   int64_t win_next = off[min(bs + kWave + lane, be)];
-  wait_all();
-  const int64_t safe = lane_i64(win, 0);     // a valid position whenever the range has lookups
   const int64_t last = off[be];
   wait_all();
+  const int64_t safe = lane_i64(win, 0);     // a valid position whenever the range has lookups
   if (last == safe) {                         // only empty bags
     Acc<F16> z;
     acc_zero(z);
@@ -1055,8 +1055,146 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
   }
 }
 
-// Gather slices.  A worker's gather slices are cut into two queues of chunks (runs of
-// bags of one slice): long-bag slices (wave mode) and the rest (SW mode).  Wavefront v
+
+// lane l of this SW's 64-bit value (a shuffle within the SW's G lanes)
+__device__ __forceinline__ int64_t lane_i64_sw(int64_t v, int l, int G) {
+  const int lo = __shfl(static_cast<int>(v & 0xffffffff), l, G);
+  const int hi = __shfl(static_cast<int>(v >> 32), l, G);
+  return (static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+}
+
+// ---------------------------------------------------------------- gather: single-lookup bags
+//
+// Tables whose statistics promise bags of at most one lookup (max pooling <= 1) need
+// no pooling: each bag's output is its row (or zeros).  A chunk holds at most kU bags
+// and is one step for its SW: the lanes load the bags' offsets and ids and compute
+// the row addresses (the zero row for an empty bag or an invalid id), the SW loads
+// the kU rows, and each row is stored, widened to fp32, as its bag's output.  A bag
+// that holds more than one lookup after all is summed again, in lookup order, on a
+// slow path.  Chunk heads and ids are loaded one chunk ahead.
+
+template <int G>
+struct SingleHead {   // where each bag of a chunk starts and ends (slot j: bag lane_sw + j G)
+  static constexpr int IPL = G >= kU ? 1 : kU / G;
+  int64_t st[IPL], en[IPL];
+  __device__ __forceinline__ void issue(GMEM const int64_t* off, const SegRef& s, int lane_sw) {
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) {
+      const int b = min(s.bs + lane_sw + j * G, s.be);   // past the chunk: an empty bag at be
+      st[j] = off[b];
+      en[j] = off[min(b + 1, s.be)];
+    }
+  }
+};
+
+template <int G>
+struct SingleIds {
+  static constexpr int IPL = SingleHead<G>::IPL;
+  int64_t raw[IPL];
+  __device__ __forceinline__ void load(GMEM const int64_t* __restrict__ indices, const SingleHead<G>& h) {
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) raw[j] = h.en[j] > h.st[j] ? indices[h.st[j]] : int64_t(0);
+  }
+};
+
+template <int G, bool F16>
+__device__ __forceinline__ void store_row(GMEM float* p, const uint4 r) {
+  if constexpr (F16) {
+    Acc<true> a;
+    const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      a.v[2 * q] = __half2float(__ushort_as_half(static_cast<unsigned short>(w[q] & 0xffffu)));
+      a.v[2 * q + 1] = __half2float(__ushort_as_half(static_cast<unsigned short>(w[q] >> 16)));
+    }
+    acc_store(p, a);
+  } else {
+    *reinterpret_cast<GMEM uint4*>(p) = r;   // fp32 rows are their own output (bit for bit)
+  }
+}
+
+template <int G, bool F16>
+__device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ indices,
+                                            GMEM const int64_t* __restrict__ offsets, GMEM float* __restrict__ out,
+                                            int E, int B, int64_t ostride, int lane_sw, FGather& f, RunQueue& q) {
+  constexpr int NA = F16 ? 8 : 4;
+  constexpr int IPL = SingleHead<G>::IPL;
+  auto off_of = [&](const SegRef& s) -> GMEM const int64_t* {
+    return offsets + static_cast<int64_t>(q.r[s.e].table) * B;
+  };
+  SegRef cur, nxt, nn;
+  if (!q.next(cur)) return;
+  SingleHead<G> h0, h1, h2;
+  SingleIds<G> i0, i1;
+  h0.issue(off_of(cur), cur, lane_sw);
+  bool has1 = q.next(nxt);
+  if (has1) h1.issue(off_of(nxt), nxt, lane_sw);
+  wait_all();
+  i0.load(indices, h0);
+  bool has2 = has1 && q.next(nn);
+  if (has2) h2.issue(off_of(nn), nn, lane_sw);
+  if (has1) i1.load(indices, h1);
+  while (true) {
+    // ---- chunk cur: head h0 and ids i0 have landed (or are in flight)
+    const LMEM GatherRun& g = q.r[cur.e];
+    f.w = as_global(static_cast<const char*>(g.w));
+    f.rows = static_cast<uint64_t>(g.rows);
+    GMEM float* const ob = out + static_cast<int64_t>(g.table) * E + lane_sw * NA;
+    int64_t addr[IPL];
+    bool multi = false;
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) {
+      const bool has = h0.en[j] > h0.st[j];
+      const bool ok = static_cast<uint64_t>(i0.raw[j]) < f.rows;
+      if (has && !ok) f.bad();
+      addr[j] = reinterpret_cast<int64_t>(has && ok ? f.w + i0.raw[j] * f.R : f.zero);
+      multi = multi || h0.en[j] - h0.st[j] > 1;
+    }
+    uint4 raw[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int64_t a = G == 1 ? addr[u] : lane_i64_sw(addr[u / G], u % G, G);
+      raw[u] = ldg16(reinterpret_cast<gchar*>(a) + f.lane_c);
+    }
+    wait_all();   // the one wait of the step
+    const int nb = cur.be - cur.bs;
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (u < nb && f.active) store_row<G, F16>(ob + static_cast<int64_t>(cur.bs + u) * ostride, raw[u]);
+    if (__ballot(multi) != 0) {   // bags of more than one lookup: sum them again in lookup order
+#pragma unroll 1
+      for (int u = 0; u < kU; ++u) {
+        const int64_t s0 = G == 1 ? h0.st[u] : lane_i64_sw(h0.st[u / G], u % G, G);
+        const int64_t e0 = G == 1 ? h0.en[u] : lane_i64_sw(h0.en[u / G], u % G, G);
+        if (u < nb && e0 - s0 > 1) {
+          Acc<F16> acc;
+          acc_zero(acc);
+          for (int64_t k = s0; k < e0; ++k) {
+            const int64_t x = indices[k];
+            const bool ok = static_cast<uint64_t>(x) < f.rows;
+            if (!ok && lane_sw == 0 && k > s0) f.bad();   // the first id was counted with the chunk
+            acc_add(acc, ldg16(ok ? f.w + x * f.R + f.lane_c : f.zero + f.lane_c), f.one);
+          }
+          if (f.active) acc_store(ob + static_cast<int64_t>(cur.bs + u) * ostride, acc);
+        }
+      }
+    }
+    if (!has1) return;
+    cur = nxt;
+    h0 = h1;
+    i0 = i1;
+    nxt = nn;
+    h1 = h2;
+    has1 = has2;
+    has2 = has1 && q.next(nn);
+    if (has2) h2.issue(off_of(nn), nn, lane_sw);
+    if (has1) i1.load(indices, h1);
+  }
+}
+
+// Gather slices.  A worker's gather slices are cut into three queues of chunks (runs
+// of bags of one slice): long-bag slices (wave mode), single-lookup-bag slices, and
+// the rest (SW mode).  Wavefront v
 // takes wave-mode chunks v, v + 16, ...; SW s takes SW-mode chunks s, s + NSW, ...  The
 // chunks are small, so every SW samples every slice of the worker: the split stays
 // even when per-lookup cost differs between tables (cache-resident vs HBM-bound).  The
@@ -1067,8 +1205,9 @@ __device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, co
   constexpr int NSW = kBlock / G;
   GMEM const int32_t* gptr = as_global(a.gr_ptr);
   const int r0 = gptr[wg], nr = gptr[wg + 1] - r0;
-  GMEM const int32_t* info = as_global(a.gr_info) + 4 * wg;
-  const int n_wave = info[0], wave_chunks = info[1], sw_chunks = info[2];
+  GMEM const int32_t* info = as_global(a.gr_info) + 8 * wg;
+  const int n_wave = info[0], wave_chunks = info[1], n_single = info[2], single_chunks = info[3],
+            sw_chunks = info[4];
   {
     gchar* src = reinterpret_cast<gchar*>(as_global(a.gr) + r0);
     for (int q = l.tid; q < 3 * nr; q += kBlock) sts16(lds + 16 * q, ldg16(src + 16 * q));
@@ -1096,8 +1235,14 @@ __device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, co
                         out + static_cast<int64_t>(g.table) * a.E, ost, l.lane_sw, l.sw_w, f);
     }
   }
+  {  // single-lookup bags
+    RunQueue q{runs, n_wave, n_wave + n_single, l.sw, NSW, single_chunks, a.B};
+    FGather f;
+    static_cast<RowBase&>(f) = rb0;
+    walk_single<G, F16>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
+  }
   {  // SW mode
-    RunQueue q{runs, n_wave, nr, l.sw, NSW, sw_chunks, a.B};
+    RunQueue q{runs, n_wave + n_single, nr, l.sw, NSW, sw_chunks, a.B};
     FGather f;
     static_cast<RowBase&>(f) = rb0;
     walk_stream<G, F16>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);

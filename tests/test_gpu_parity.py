@@ -204,3 +204,38 @@ def test_hot_probe_matches_membership(gpu):
         slot = p.hot_probe(t, torch.from_numpy(idx).cuda()).cpu().numpy()
         want = OI.hot_slots(idx, stats[t].hot_rows[:C[t]])
         assert np.array_equal(slot, want)
+
+
+@pytest.mark.parametrize("E,dtype", [(64, "f32"), (128, "f16"), (32, "f32"), (256, "f32")])
+def test_single_lookup_tables_and_a_broken_promise(gpu, E, dtype):
+    """Tables whose statistics promise at most one lookup per bag take their own gather
+    walker; bags that break the promise at run time, empty bags, bag counts that are not
+    a multiple of a chunk and out-of-range ids must still match the oracle exactly."""
+    log(f"single-lookup tables E={E} {dtype}")
+    c = mixed_config(109, E, dtype, B=203, pf_mean=0.9, pf_hi=1)
+    hw = host_tables(c, W.VAL_INTEGER)
+    wd = upload_tables(hw)
+    stats = W.history_stats(c, c.batch)
+    assert all(s.max_pooling == 1 for s in stats)
+    # the promised shape: bags of 0 or 1 lookup
+    batch = W.gen_batch(c, 0)
+    p, got, nbad = run(c, batch, wd, STRATS["gather"])
+    check_full(got, hw, batch, dtype, exact=True)
+    assert nbad == 0
+    # the promise broken: some bags of 2..5 lookups, some empty, a few invalid ids
+    g = np.random.default_rng(7)
+    bags = []
+    for m in c.rows:
+        for b in range(c.batch):
+            n = int(g.choice([0, 1, 1, 1, 2, 5]))
+            bags.append([int(x) for x in g.integers(0, m, size=n)])
+    batch2 = W.batch_from_bags(c.T, c.batch, bags)
+    pos = g.choice(batch2.indices.size, size=9, replace=False)
+    batch2.indices[pos[:3]] = -1
+    batch2.indices[pos[3:6]] = 1 << 35
+    t_of = np.searchsorted(batch2.offsets, pos[6:], side="right") - 1
+    batch2.indices[pos[6:]] = np.asarray(c.rows)[t_of // c.batch]
+    want_bad = OI.range_errors(batch2.indices, batch2.offsets, c.rows, c.batch)
+    _, got2, nbad2 = run(c, batch2, wd, STRATS["gather"])   # the same statistics (max pooling 1)
+    check_full(got2, hw, batch2, dtype, exact=True)
+    assert nbad2 == want_bad == 9
