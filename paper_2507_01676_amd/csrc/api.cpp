@@ -39,10 +39,10 @@ struct emb_plan {
   int32_t* d_hot_ids = nullptr;
   int32_t* d_counters = nullptr;
   unsigned long long* d_err = nullptr;
-  std::vector<GatherRun> h_gr;           // gather runs (table pointers patched at bind)
+  std::vector<GatherRun> h_gr;           // worker slots: header + runs (table pointers patched at bind)
+  std::vector<std::pair<size_t, int32_t>> h_gr_runs;   // (record, table) of every run
+  int32_t gr_slot = 1;                   // records per worker slot
   GatherRun* d_gr = nullptr;
-  int32_t* d_gr_ptr = nullptr;
-  int32_t* d_gr_info = nullptr;
   const char* d_zero_row = nullptr;      // R zero bytes
   bool staged = false;                   // the plan has LDS / HOT / DEDUP slices
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
@@ -308,8 +308,9 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   // SW-mode lookups at the max batch), at least one full step (8) and at most 32, so
   // that each SW gets several chunks; wave-mode chunks carry about four wavefront
   // steps of lookups, fewer when that leaves some of the 16 wavefronts without one.
-  std::vector<GatherRun>& gr = p->h_gr;
-  std::vector<int32_t> gr_ptr(K + 1, 0), gr_info(8 * static_cast<size_t>(K), 0);
+  std::vector<GatherRun> gr;                       // runs, worker-major
+  std::vector<int32_t> gr_ptr(K + 1, 0);
+  std::vector<GatherSlotHeader> gr_head(K);
   int max_runs = 0;
   {
     const int nsw = kBlock / p->G;
@@ -366,13 +367,27 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
         return EMB_ERR_UNSUPPORTED;
       }
       max_runs = std::max(max_runs, nrun[0] + nrun[1] + nrun[2]);
-      gr_info[8 * w + 0] = nrun[0];
-      gr_info[8 * w + 1] = static_cast<int32_t>(base[0]);
-      gr_info[8 * w + 2] = nrun[1];
-      gr_info[8 * w + 3] = static_cast<int32_t>(base[1]);
-      gr_info[8 * w + 4] = static_cast<int32_t>(base[2]);
+      GatherSlotHeader& hd = gr_head[w];
+      std::memset(&hd, 0, sizeof hd);
+      hd.n_wave = nrun[0];
+      hd.wave_chunks = static_cast<int32_t>(base[0]);
+      hd.n_single = nrun[1];
+      hd.single_chunks = static_cast<int32_t>(base[1]);
+      hd.sw_chunks = static_cast<int32_t>(base[2]);
+      hd.n_runs = nrun[0] + nrun[1] + nrun[2];
     }
     gr_ptr[K] = static_cast<int32_t>(gr.size());
+  }
+  // fixed-size slots, so that a worker fetches its header and runs in one round trip
+  p->gr_slot = max_runs + 1;
+  p->h_gr.assign(static_cast<size_t>(K) * p->gr_slot, GatherRun{});
+  for (int w = 0; w < K; ++w) {
+    const size_t s0 = static_cast<size_t>(w) * p->gr_slot;
+    std::memcpy(&p->h_gr[s0], &gr_head[w], sizeof(GatherSlotHeader));
+    for (int32_t i = gr_ptr[w]; i < gr_ptr[w + 1]; ++i) {
+      p->h_gr[s0 + 1 + (i - gr_ptr[w])] = gr[i];
+      p->h_gr_runs.emplace_back(s0 + 1 + (i - gr_ptr[w]), gr[i].table);
+    }
   }
 
   // one metadata allocation
@@ -385,9 +400,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   size_t o_ctr = align_up(o_ids + h_ids.size() * sizeof(int32_t), 256);
   size_t o_err = align_up(o_ctr + static_cast<size_t>(n_ctr) * sizeof(int32_t), 256);
   size_t o_gr = align_up(o_err + sizeof(unsigned long long), 256);
-  size_t o_grp = align_up(o_gr + gr.size() * sizeof(GatherRun), 256);
-  size_t o_gri = align_up(o_grp + gr_ptr.size() * sizeof(int32_t), 256);
-  size_t o_zero = align_up(o_gri + gr_info.size() * sizeof(int32_t), 256);
+  size_t o_zero = align_up(o_gr + p->h_gr.size() * sizeof(GatherRun), 256);
   size_t total = align_up(o_zero + static_cast<size_t>(p->R), 256);
   if (hipMalloc(&p->d_meta, total) != hipSuccess) {
     delete p;
@@ -407,8 +420,6 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   p->d_counters = reinterpret_cast<int32_t*>(p->d_meta + o_ctr);
   p->d_err = reinterpret_cast<unsigned long long*>(p->d_meta + o_err);
   p->d_gr = reinterpret_cast<GatherRun*>(p->d_meta + o_gr);
-  p->d_gr_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_grp);
-  p->d_gr_info = reinterpret_cast<int32_t*>(p->d_meta + o_gri);
   p->d_zero_row = p->d_meta + o_zero;   // zeros: the host image is zero-filled
   std::vector<char> host(total, 0);
   if (!items.empty()) std::memcpy(host.data() + o_items, items.data(), items.size() * sizeof(DevItem));
@@ -419,16 +430,14 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     std::memcpy(host.data() + o_slots, h_slots.data(), h_slots.size() * sizeof(uint16_t));
     std::memcpy(host.data() + o_ids, h_ids.data(), h_ids.size() * sizeof(int32_t));
   }
-  if (!gr.empty()) std::memcpy(host.data() + o_gr, gr.data(), gr.size() * sizeof(GatherRun));
-  std::memcpy(host.data() + o_grp, gr_ptr.data(), gr_ptr.size() * sizeof(int32_t));
-  std::memcpy(host.data() + o_gri, gr_info.data(), gr_info.size() * sizeof(int32_t));
+  std::memcpy(host.data() + o_gr, p->h_gr.data(), p->h_gr.size() * sizeof(GatherRun));
   if (hipMemcpy(p->d_meta, host.data(), total, hipMemcpyHostToDevice) != hipSuccess ||
       (p->d_partials && hipMemset(p->d_partials, 0, part_floats * sizeof(float)) != hipSuccess)) {
     emb_plan_destroy(p);
     return EMB_ERR_DEVICE;
   }
   // LDS: the staged slices' rows and metadata, and (after them) the worker's gather runs
-  const int run_bytes = max_runs * static_cast<int>(sizeof(GatherRun));
+  const int run_bytes = p->gr_slot * static_cast<int>(sizeof(GatherRun));
   p->staged = staged;
   p->lds_bytes = std::max(staged ? static_cast<int>(L) + kMetaReserve : 0, run_bytes);
   if (prepare_lookup_kernels(std::max(p->lds_bytes, kMetaReserve)) != 0) {
@@ -445,7 +454,7 @@ emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights)
     if (!weights[t] || (reinterpret_cast<uintptr_t>(weights[t]) & 15u) != 0) return EMB_ERR_INVALID_ARGUMENT;
   }
   for (int32_t t = 0; t < plan->T; ++t) plan->h_tables[t].w = weights[t];
-  for (GatherRun& r : plan->h_gr) r.w = weights[r.table];
+  for (const auto& rt : plan->h_gr_runs) plan->h_gr[rt.first].w = weights[rt.second];
   if (hipMemcpy(plan->d_tables, plan->h_tables.data(), plan->T * sizeof(DevTable), hipMemcpyHostToDevice) !=
           hipSuccess ||
       (!plan->h_gr.empty() && hipMemcpy(plan->d_gr, plan->h_gr.data(), plan->h_gr.size() * sizeof(GatherRun),
@@ -487,8 +496,7 @@ emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t*
   a.n_items = static_cast<int32_t>(plan->plan.slices.size());
   a.trace = plan->d_trace;
   a.gr = plan->d_gr;
-  a.gr_ptr = plan->d_gr_ptr;
-  a.gr_info = plan->d_gr_info;
+  a.gr_slot = plan->gr_slot;
   a.zero_row = plan->d_zero_row;
   a.one = 1.0f;
   return st(launch_lookup(a, plan->G, plan->f16, plan->staged, plan->K, plan->lds_bytes, stream));

@@ -47,6 +47,15 @@ struct GatherRun {
   int32_t pad[3];
 };
 static_assert(sizeof(GatherRun) == 48, "GatherRun is staged as three 16-byte pieces");
+// The first record of a worker's slot: how its runs split into queues.
+struct GatherSlotHeader {
+  int32_t n_wave, wave_chunks;       // wave-mode runs and their chunks
+  int32_t n_single, single_chunks;   // single-lookup-bag runs and their chunks
+  int32_t sw_chunks;                 // SW-mode chunks (the remaining runs)
+  int32_t n_runs;
+  int32_t pad[6];
+};
+static_assert(sizeof(GatherSlotHeader) == sizeof(GatherRun), "a slot header takes one run record");
 constexpr int kMaxRunsPerWorker = 1024;   // a worker's gather runs held in LDS at once
 constexpr int kChunkSingle = 8;           // bags per chunk of a single-lookup-bag run (one SW step)
 
@@ -71,10 +80,9 @@ struct LookupArgs {
   int32_t lds_rows;             // LDS bytes for rows (the budget L)
   int32_t n_items;
   unsigned long long* trace;    // optional timers (see kTraceWorker), nullptr = off
-  const GatherRun* gr;          // gather runs, worker-major: wave-mode runs first, then SW-mode runs
-  const int32_t* gr_ptr;        // [K + 1] run ranges per worker
-  const int32_t* gr_info;       // [K][8]: wave-mode runs, wave-mode chunks, single-lookup runs,
-                                //         single-lookup chunks, SW-mode chunks, 0, 0, 0
+  const GatherRun* gr;          // worker slots of gr_slot records: a GatherSlotHeader, then the
+                                // worker's runs (wave mode, single-lookup bags, SW mode)
+  int32_t gr_slot;
   const void* zero_row;         // R zero bytes: the row an invalid id reads in the gather walkers
   float one;                    // 1.0f, opaque to the compiler (fp16 rows are added as x * one + acc)
 };

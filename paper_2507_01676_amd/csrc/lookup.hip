@@ -1203,16 +1203,15 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
 template <int G, bool F16>
 __device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, const Lane& l, int wg) {
   constexpr int NSW = kBlock / G;
-  GMEM const int32_t* gptr = as_global(a.gr_ptr);
-  const int r0 = gptr[wg], nr = gptr[wg + 1] - r0;
-  GMEM const int32_t* info = as_global(a.gr_info) + 8 * wg;
-  const int n_wave = info[0], wave_chunks = info[1], n_single = info[2], single_chunks = info[3],
-            sw_chunks = info[4];
-  {
-    gchar* src = reinterpret_cast<gchar*>(as_global(a.gr) + r0);
-    for (int q = l.tid; q < 3 * nr; q += kBlock) sts16(lds + 16 * q, ldg16(src + 16 * q));
+  {   // the worker's slot: a header record, then its runs
+    gchar* src = reinterpret_cast<gchar*>(as_global(a.gr) + static_cast<int64_t>(wg) * a.gr_slot);
+    for (int q = l.tid; q < 3 * a.gr_slot; q += kBlock) sts16(lds + 16 * q, ldg16(src + 16 * q));
   }
   __syncthreads();
+  const LMEM GatherSlotHeader* hd = reinterpret_cast<const LMEM GatherSlotHeader*>(lds);
+  const int n_wave = hd->n_wave, wave_chunks = hd->wave_chunks, n_single = hd->n_single,
+            single_chunks = hd->single_chunks, sw_chunks = hd->sw_chunks, nr = hd->n_runs;
+  lds += sizeof(GatherRun);
   const LMEM GatherRun* runs = reinterpret_cast<const LMEM GatherRun*>(lds);
   GMEM const int64_t* idx = as_global(a.indices);
   GMEM const int64_t* offsets = as_global(a.offsets);
