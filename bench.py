@@ -7,8 +7,11 @@ R distinct batches are cycled.  Prints ONE JSON line:
 
   value            lookups/s over the K timed steps (whole job, one GPU)
   queries_per_s    samples/s (the paper's TPS)
-  p99_us           nearest-rank P99 of the per-batch latency (a separate pass with HIP
-                   events around each launch; mean_us is that pass's mean)
+  p99_us           nearest-rank P99 of the per-batch latency (a separate pass of 1000
+                   batches, 200 for workload 5, with HIP events around each launch;
+                   mean_us is that pass's mean)
+  cold_cache       the same latency with L2 and MALL flushed (a 512 MiB write) before
+                   each batch, outside the timed region
   launch_us        average launch duration over the K timed steps (one HIP event pair on
                    the launch stream around the back-to-back launches)
   useful_hbm_frac  (lookups x row bytes) per launch_us over the 8 TB/s HBM peak
@@ -159,6 +162,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG, help="workload 1..5")
     ap.add_argument("--batches", type=int, default=0, help="distinct resident batches (default 8, 4 for workload 5)")
+    ap.add_argument("--p99-batches", type=int, default=0, help="latency pass length (default 1000; 200 for workload 5)")
+    ap.add_argument("--cold-batches", type=int, default=20, help="batches timed after a cache-flushing write (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-copy", action="store_true")
@@ -221,17 +226,39 @@ def main():
     assert plan.check_errors() == 0
 
     K = args.steps
-    # per-batch latency (P99): an event pair around each launch
-    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    # per-batch latency (P99): an event pair around each launch, over N batches
+    N = args.p99_batches or (200 if args.config == 5 else 1000)
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(N)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(N)]
     torch.cuda.synchronize()
-    for i in range(K):
+    for i in range(N):
         ip, op = ptrs[i % R]
         ev0[i].record(stream)
         plan.lookup_ptr(ip, op, B, outp, sp)
         ev1[i].record(stream)
     torch.cuda.synchronize()
-    lat_ms = [ev0[i].elapsed_time(ev1[i]) for i in range(K)]
+    lat_ms = [ev0[i].elapsed_time(ev1[i]) for i in range(N)]
+
+    # cold caches: before each of these batches a 512 MiB buffer is written (outside the
+    # timed region), which evicts the tables' rows from L2 and the MALL
+    cold = None
+    if args.cold_batches > 0:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        c0 = [torch.cuda.Event(enable_timing=True) for _ in range(args.cold_batches)]
+        c1 = [torch.cuda.Event(enable_timing=True) for _ in range(args.cold_batches)]
+        for i in range(args.cold_batches):
+            flush.fill_(i & 0xFF)
+            ip, op = ptrs[i % R]
+            c0[i].record(stream)
+            plan.lookup_ptr(ip, op, B, outp, sp)
+            c1[i].record(stream)
+        torch.cuda.synchronize()
+        cl = [c0[i].elapsed_time(c1[i]) for i in range(args.cold_batches)]
+        cmean = sum(cl) / len(cl)
+        cuse = sum(n_look[i % R] for i in range(args.cold_batches)) * c.row_bytes / len(cl)
+        cold = {"batches": len(cl), "mean_us": cmean * 1e3, "p99_us": p99(cl) * 1e3,
+                "useful_gbps": cuse / (cmean * 1e-3) / 1e9}
+        del flush
 
     # throughput: the K timed steps back to back, synchronized on both sides; one event
     # pair on the launch stream gives the average launch duration
@@ -247,7 +274,7 @@ def main():
     wall = time.perf_counter() - wall0
     launch_ms = e_start.elapsed_time(e_stop) / K
     total_lookups = sum(n_look[i % R] for i in range(K))
-    mean_ms = sum(lat_ms) / K
+    mean_ms = sum(lat_ms) / len(lat_ms)
 
     R_b = c.row_bytes
     alg = [W.algorithmic_bytes(c, n_look[i % R])["total"] for i in range(K)]
@@ -291,6 +318,8 @@ def main():
                      "traffic": traffic,
                      "traffic_gbps": None if traffic is None else traffic / (launch_ms * 1e-3) / 1e9,
                      "algorithmic_bytes_per_launch": alg_mean, "kernel": "lookup_kernel"},
+        "p99_batches": len(lat_ms),
+        "cold_cache": cold,
         "copy_gbps": copy_gbps,
         "plan": {"strategies": info["n_strategy"], "items": info["num_items"], "lif_milli": info["lif_milli"],
                  "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms},
