@@ -331,6 +331,31 @@ struct Ids {
 #pragma unroll
     for (int u = 0; u < kU; ++u) ix[u] = G == 1 ? mine[u] : __shfl(mine[u / G], u % G, G);
   }
+
+  // The row address of each of the kU lookups, for this lane's 16 bytes of the row:
+  // the lane that loaded an id checks it and forms the row's address once (the zero
+  // row for an invalid id or a position past the end), and the SW shares the 64-bit
+  // addresses by shuffles.
+  __device__ __forceinline__ void resolve_addr(const RowBase& f, int lane_sw, gchar* (&a)[kU]) const {
+    int64_t mine[IPL];
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) {
+      const bool in_range = (ok_bits >> j) & 1u;
+      const bool ok = static_cast<uint64_t>(raw[j]) < f.rows;
+      if (in_range && !ok) f.bad();
+      mine[j] = reinterpret_cast<int64_t>(in_range && ok ? f.w + raw[j] * f.R : f.zero);
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      int64_t v = mine[u / G];
+      if constexpr (G > 1) {
+        const int lo = __shfl(static_cast<int>(v & 0xffffffff), u % G, G);
+        const int hi = __shfl(static_cast<int>(v >> 32), u % G, G);
+        v = (static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+      }
+      a[u] = reinterpret_cast<gchar*>(v) + f.lane_c;
+    }
+  }
 };
 
 // ---------------------------------------------------------------- SW mode
@@ -945,6 +970,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
 
   GMEM const int64_t* off;
   GMEM float* ob;
+  GMEM float* obb;   // bag b's output (this lane's part)
   int be, wb, b;
   int64_t p, pend, win, win2;
   Acc<F16> acc;
@@ -958,6 +984,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     be = cur.be;
     wb = cur.bs;
     b = cur.bs;
+    obb = ob + static_cast<int64_t>(b) * ostride;
     p = h0.p;
     pend = h0.pend;
     win = h0.win;
@@ -973,8 +1000,8 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     if (has2) h2.issue(off_of(s2), s2, lane_sw);
   };
   auto flush = [&]() {   // the bags left in the segment end here (the last one holds acc)
-    for (; b < be; ++b) {
-      if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+    for (; b < be; ++b, obb += ostride) {
+      if (f.active) acc_store(obb, acc);
       acc_zero(acc);
     }
   };
@@ -1000,11 +1027,11 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     const int n = static_cast<int>(min64(kU, pend - p));
     // the current bag ends before the step's lookup u = rel (rel > kU: not in this step)
     int rel = static_cast<int>(min64(bag_end - p, kU + 1));
-    int32_t ix[kU];
-    ids.resolve(f, lane_sw, ix);
+    gchar* ra[kU];
+    ids.resolve_addr(f, lane_sw, ra);
     uint4 raw[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) f.issue(ix[u], 0, raw[u]);
+    for (int u = 0; u < kU; ++u) raw[u] = ldg16(ra[u]);
     const int64_t pn = p + n;
     const bool seg_end = pn >= pend;
     // the next step's ids: more of this segment, or the start of the next one
@@ -1018,13 +1045,14 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     for (int u = 0; u < kU; ++u) {
       if (u < n) {
         while (u == rel) {
-          if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+          if (f.active) acc_store(obb, acc);
           acc_zero(acc);
           ++b;
+          obb += ostride;
           bag_end = end_of(b);
           rel = static_cast<int>(min64(bag_end - p, kU + 1));
         }
-        acc_add(acc, f.take(ix[u], 0, raw[u]), f.one);
+        acc_add(acc, raw[u], f.one);
       }
     }
     if (b - wb >= G) {
