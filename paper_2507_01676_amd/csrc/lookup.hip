@@ -244,14 +244,12 @@ __device__ __forceinline__ void hot_probe_batch(const LMEM int32_t* keys, const 
   }
 }
 
-struct Pair16 {
-  uint4 l, g;
-};
-
-// hot rows in LDS (slot order) behind the id hash; misses read HBM
+// hot rows in LDS (slot order) behind the id hash; misses read HBM.  Each lane loads
+// its row piece from one place only (LDS on a hit, HBM on a miss, the zero row for an
+// invalid id), into one register.
 struct FHot : RowBase {
   static constexpr bool kPositional = false;
-  using Raw = Pair16;
+  using Raw = uint4;
   const lchar* lds;
   const LMEM int32_t* keys;
   const LMEM uint16_t* slots;
@@ -260,19 +258,18 @@ struct FHot : RowBase {
     hot_probe_batch(keys, slots, hb, ix, n, sl);
   }
   __device__ __forceinline__ void issue(int32_t ix, int32_t sl, Raw& r) const {
-    r.l = lds16(lds + static_cast<int64_t>(sl > 0 ? sl : 0) * R + lane_c);
-    r.g = ldg16(row(sl < 0 ? ix : 0));
+    if (sl >= 0)
+      r = lds16(lds + static_cast<int64_t>(sl) * R + lane_c);
+    else
+      r = ldg16(ix >= 0 ? w + static_cast<int64_t>(ix) * R + lane_c : zero + lane_c);
   }
-  __device__ __forceinline__ uint4 take(int32_t ix, int32_t sl, const Raw& r) const {
-    if (ix < 0 || !active) return zero16();
-    return sl >= 0 ? r.l : r.g;
-  }
+  __device__ __forceinline__ uint4 take(int32_t, int32_t, const Raw& r) const { return r; }
 };
 
 // a tile's distinct rows in LDS (first capd of them, slot order); the rest read HBM
 struct FDedup : RowBase {
   static constexpr bool kPositional = true;   // probes by position in the tile
-  using Raw = Pair16;
+  using Raw = uint4;
   const lchar* lds;
   const LMEM int16_t* inv;  // slot of each tile position, -1 for an invalid id
   int64_t P0;             // first lookup of the tile
@@ -283,13 +280,12 @@ struct FDedup : RowBase {
   }
   __device__ __forceinline__ bool in_lds(int32_t sl) const { return sl >= 0 && sl < capd; }
   __device__ __forceinline__ void issue(int32_t ix, int32_t sl, Raw& r) const {
-    r.l = lds16(lds + static_cast<int64_t>(in_lds(sl) ? sl : 0) * R + lane_c);
-    r.g = ldg16(row(in_lds(sl) ? 0 : ix));
+    if (in_lds(sl))
+      r = lds16(lds + static_cast<int64_t>(sl) * R + lane_c);
+    else
+      r = ldg16(ix >= 0 ? w + static_cast<int64_t>(ix) * R + lane_c : zero + lane_c);
   }
-  __device__ __forceinline__ uint4 take(int32_t ix, int32_t sl, const Raw& r) const {
-    if (ix < 0 || !active) return zero16();
-    return in_lds(sl) ? r.l : r.g;
-  }
+  __device__ __forceinline__ uint4 take(int32_t, int32_t, const Raw& r) const { return r; }
 };
 
 // The kU upcoming lookups of a SW are loaded one per lane (IPL per lane when the SW
