@@ -97,7 +97,8 @@ typedef struct {
   int32_t order_mode;       /* 0 = longest first with the paper's keys as tie-breaks;
                                1 = the paper's order (s desc, m asc)                             */
   int64_t chunk_max_bytes;  /* max row-chunk bytes (Sec. III-B); <= 0 -> lds_budget_bytes      */
-  const double* beta;       /* host, EMB_BETA_COUNT coefficients; NULL -> built-in MI355X fit     */
+  const double* beta;       /* host, EMB_BETA_COUNT finite non-negative coefficients (picoseconds);
+                               NULL -> built-in MI355X fit; a negative one is an invalid argument  */
   const int32_t* force_strategy; /* host, T entries of emb_strategy_t, or NULL (all AUTO)        */
   int32_t num_workers;      /* > 0 overrides K (must not exceed 65535)                          */
   int32_t reserved;

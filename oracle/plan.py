@@ -290,7 +290,9 @@ def _validate(rows, E, dtype, stats, B, K, opts: Options):
     if opts.order_mode not in (0, 1):
         raise PlanError("order_mode")
     beta = list(opts.beta) if opts.beta is not None else default_beta(R)
-    if len(beta) != NBETA or not all(math.isfinite(x) for x in beta):
+    # the coefficients price times: a negative one can make a slice cost less than
+    # nothing, and least-loaded placement would then pile such slices onto one worker
+    if len(beta) != NBETA or not all(math.isfinite(x) and x >= 0.0 for x in beta):
         raise PlanError("beta")
     force = list(opts.force) if opts.force is not None else [AUTO] * T
     if len(force) != T or any(f not in (AUTO, LDS, HOT, DEDUP, GATHER) for f in force):

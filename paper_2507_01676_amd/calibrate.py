@@ -23,11 +23,15 @@ lookups), LDS next (L0, S, L1 from whole-table slices, then I from what they
 leave of the row-chunk slices' times, so that I also carries the chunk
 combine), then HOT (H0, P) and DEDUP (D0, D1) on what their costs leave after
 the shared terms.
-Every fit is ``numpy.linalg.lstsq``.
+Every fit is ``numpy.linalg.lstsq``, constrained to non-negative coefficients
+(an active-set NNLS) when the unconstrained solution has a negative one: the
+coefficients are times, and the planner refuses negative ones.
 
 ``fit_beta`` is plain host arithmetic; ``collect`` runs lookups on the current
 device and needs the extension.  ``python -m paper_2507_01676_amd.calibrate``
-runs both on the synthetic workloads and prints the fitted vector.
+runs both on the synthetic workloads and prints the fitted vector; with
+``--report`` it re-plans the workloads with that vector and sets each plan's
+predicted makespan beside the measured one.
 """
 from __future__ import annotations
 
@@ -72,8 +76,17 @@ class Samples:
 
 
 def _lstsq(A: np.ndarray, y: np.ndarray) -> np.ndarray:
+    """Least squares with non-negative coefficients (the planner refuses negative ones):
+    the unconstrained OLS solution when it is non-negative, else the best fit over the
+    columns that stay free (scipy's active-set NNLS), columns scaled to unit norm."""
     x, *_ = np.linalg.lstsq(A, y, rcond=None)
-    return x
+    if np.all(x >= 0.0):
+        return x
+    from scipy.optimize import nnls
+    norm = np.linalg.norm(A, axis=0)
+    norm[norm == 0.0] = 1.0
+    z, _ = nnls(A / norm, y)
+    return z / norm
 
 
 def fit_beta(s: Samples, base: Optional[Sequence[float]] = None) -> List[float]:
@@ -225,12 +238,69 @@ def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("ga
     return allS
 
 
+def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=print) -> List[Dict]:
+    """Re-plans each workload with ``beta`` and sets the plan's predicted makespan (the
+    most loaded worker, in the cost model's units) beside the measured one: the slowest
+    worker's span from the kernel timers and the mean launch time of back-to-back
+    launches."""
+    import torch
+    import workloads as W
+    from . import Plan, fill_table
+    rows_out = []
+    for cfg in configs:
+        c = W.make_config(cfg)
+        bt = W.gen_batch(c, 0)
+        stats = W.history_stats(c)
+        dt = torch.float16 if c.dtype == "f16" else torch.float32
+        ws = []
+        for t, m in enumerate(c.rows):
+            w = torch.empty((m, c.E), dtype=dt, device="cuda")
+            fill_table(w, t, c.value_seeds[t], c.lo, c.hi)
+            ws.append(w)
+        plan = Plan(c.rows, c.E, c.dtype, stats, c.batch, beta=list(beta)).bind(ws)
+        idx = torch.from_numpy(bt.indices).cuda()
+        off = torch.from_numpy(bt.offsets).cuda()
+        out = torch.empty((c.batch, c.T, c.E), device="cuda")
+        for _ in range(5):
+            plan.lookup(idx, off, c.batch, out)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(50):
+            plan.lookup(idx, off, c.batch, out)
+        b.record()
+        torch.cuda.synchronize()
+        launch_us = a.elapsed_time(b) * 1e3 / 50
+        n = plan.trace_size()
+        buf = torch.zeros(n, dtype=torch.int64, device="cuda")
+        plan.set_trace(buf)
+        plan.lookup(idx, off, c.batch, out)
+        torch.cuda.synchronize()
+        plan.set_trace(None)
+        info = plan.info()
+        K = info["num_workers"]
+        per = 2 + 1024 // 64
+        tw = buf.cpu().numpy()[:K * per].reshape(K, per)
+        span_us = float((tw[:, 2:].max() - tw[:, 0].min()) * TICK_PS / 1e6)
+        r = dict(workload=cfg, strategies=info["n_strategy"], lif_milli=info["lif_milli"],
+                 predicted_us=info["max_load_ps"] / 1e6, measured_span_us=span_us, launch_us=launch_us)
+        log(f"workload {cfg}: plan {r['strategies']} lif {r['lif_milli']}; predicted makespan "
+            f"{r['predicted_us']:.1f} us, measured worker span {span_us:.1f} us, launch {launch_us:.1f} us")
+        rows_out.append(r)
+        plan.close()
+        del ws
+        torch.cuda.empty_cache()
+    return rows_out
+
+
 def main(argv=None) -> int:
     import argparse
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--configs", type=int, nargs="+", default=[2, 3, 4])
     ap.add_argument("--strategies", nargs="+", default=["gather", "lds", "hot", "dedup"])
     ap.add_argument("--out", default=None, help="write the samples and the fit as JSON")
+    ap.add_argument("--report", type=int, nargs="*", default=None,
+                    help="re-plan these workloads with the fitted beta and compare predicted and measured makespans")
     a = ap.parse_args(argv)
     s = collect(a.configs, a.strategies, log=lambda m: print(m, file=sys.stderr, flush=True))
     b = fit_beta(s)
@@ -245,9 +315,12 @@ def main(argv=None) -> int:
         print(f"GATHER: {len(s.workers)} workers, rms residual {np.sqrt(np.mean(err ** 2)) / 1e6:.2f} us",
               file=sys.stderr)
     print(json.dumps(dict(zip(names, b))))
+    rep = None
+    if a.report is not None:
+        rep = report(b, a.report or (1, 2, 3, 4), log=lambda m: print(m, file=sys.stderr, flush=True))
     if a.out:
         with open(a.out, "w") as f:
-            json.dump(dict(beta=dict(zip(names, b)), slices=[x.__dict__ for x in s.slices],
+            json.dump(dict(beta=dict(zip(names, b)), report=rep, slices=[x.__dict__ for x in s.slices],
                            workers=[x.__dict__ for x in s.workers]), f)
     return 0
 

@@ -263,7 +263,7 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
   if (in.order_mode != 0 && in.order_mode != 1) return fail(1, "order_mode");
   P.b = in.has_beta ? in.beta : default_beta(static_cast<int32_t>(P.R));
   for (double x : P.b)
-    if (!std::isfinite(x)) return fail(1, "beta");
+    if (!std::isfinite(x) || x < 0.0) return fail(1, "beta");   // negative times would pile slices on one worker
   if (!in.force.empty() && static_cast<int32_t>(in.force.size()) != T) return fail(1, "force_strategy");
   for (int32_t f : in.force)
     if (f < S_AUTO || f > S_GATHER) return fail(1, "force_strategy");

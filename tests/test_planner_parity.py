@@ -103,3 +103,10 @@ def test_cpp_planner_rejects_what_the_oracle_rejects():
             OPL.plan_reference(rows, E, dt, stats, 8, 4)
         with pytest.raises(embx.EmbxError):
             embx.plan_text(rows, E, dt, [dict(mean_pooling=x.mean_pooling) for x in stats], 8, 4)
+    # a negative coefficient (here the HOT intercept) is refused by both
+    beta = OPL.default_beta(256)
+    beta[OPL.H0] = -1.0
+    with pytest.raises(OPL.PlanError):
+        OPL.plan_reference([10, 20], 64, "f32", [OPL.Stat(1.0)] * 2, 8, 4, OPL.Options(beta=beta))
+    with pytest.raises(embx.EmbxError):
+        embx.plan_text([10, 20], 64, "f32", [dict(mean_pooling=1.0)] * 2, 8, 4, beta=beta)
