@@ -101,7 +101,9 @@ typedef struct {
                                NULL -> built-in MI355X fit; a negative one is an invalid argument  */
   const int32_t* force_strategy; /* host, T entries of emb_strategy_t, or NULL (all AUTO)        */
   int32_t num_workers;      /* > 0 overrides K (must not exceed 65535)                          */
-  int32_t reserved;
+  int32_t sym_max_gather;   /* GATHER tables are split over all workers (symmetric partitioning,
+                               Sec. III-A) while the plan has at most this many of them, else
+                               placed by cost like the rest (Sec. III-B); 0 -> 64, < 0 -> never */
 } emb_plan_options_t;
 
 typedef struct emb_plan emb_plan_t;   /* opaque */

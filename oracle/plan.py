@@ -28,10 +28,13 @@ budget for rows):
       cost exceeds the sum of the chunk costs (the speed-up exceeds the number
       of chunks); chunks use the LDS strategy.
   P3  tau = ceil(sum of item costs / K), the ideal per-worker load.
-  P4  an item whose best strategy is GATHER is split k = min(K, B) ways
-      (symmetric partitioning, Sec. III-A: a gather slice stages nothing, so
-      every worker takes 1/k of every such table and the mix of cache-resident
-      and HBM-bound tables is the same on every worker).  Any other item
+  P4  while the plan has at most sym_max unchunked GATHER items (default 64),
+      each is split k = min(K, B) ways (symmetric partitioning, Sec. III-A: a
+      gather slice stages nothing, so every worker takes 1/k of every such
+      table and the mix of cache-resident and HBM-bound tables is the same on
+      every worker); with more of them, T x K slices would swamp the launch, and
+      they are split like the others, which leaves small tables whole and
+      places them asymmetrically (Sec. III-B).  Any other item
       costing more than tau is batch-split k ways (the paper's optional
       replication): the smallest k in [2, min(K, B)] whose best cost is at most
       max(tau, 2 x its fixed cost); all chunks of one table share one k.  A
@@ -69,6 +72,7 @@ NBETA = 10
 MAX_HOT = 4096          # hot rows a table's statistics may list
 MAX_HOT_SLOTS = 2048    # hot rows one HOT item stages at most
 MAX_CHUNKS = 65536
+SYM_MAX_DEFAULT = 64    # GATHER tables split over all workers while the plan has at most this many
 
 
 class PlanError(ValueError):
@@ -119,6 +123,7 @@ class Options:
     order_mode: int = 0
     beta: Optional[Sequence[float]] = None
     force: Optional[Sequence[int]] = None
+    sym_max: int = 0                  # 0 -> SYM_MAX_DEFAULT; < 0: GATHER items never split symmetrically
 
 
 @dataclass
@@ -153,11 +158,12 @@ class Plan:
     sum_ps: int = 0
     lif_milli: int = 0
     r_sym: int = 0
+    sym_max: int = SYM_MAX_DEFAULT
 
     def text(self) -> str:
         lines = ["embx-plan v1",
                  f"T {self.T} E {self.E} dtype {self.dtype} R {self.R} K {self.K} L {self.L} B {self.B} "
-                 f"theta {self.theta} order {self.order_mode}"]
+                 f"theta {self.theta} order {self.order_mode} symmax {self.sym_max}"]
         for s in sorted(self.slices, key=lambda x: (x.wg, x.seq)):
             lines.append(f"item {s.wg} {s.t} {s.strat} {s.chunk} {s.nchunks} {s.r0} {s.r1} {s.k} {s.j} {s.C} {s.cost}")
         lines.append(f"end max {self.max_ps} sum {self.sum_ps} lif {self.lif_milli} sym {self.r_sym}")
@@ -365,8 +371,11 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
             return LDS, c, f
         return tb.best(b, k)
 
+    sym_max = opts.sym_max if opts.sym_max != 0 else SYM_MAX_DEFAULT
+    n_gather = sum(1 for g in groups if g[0].nchunks == 1 and g[0].strat == GATHER)
+    sym_gather = sym_max > 0 and n_gather <= sym_max
     for g in groups:
-        if g[0].nchunks == 1 and g[0].strat == GATHER:
+        if sym_gather and g[0].nchunks == 1 and g[0].strat == GATHER:
             ks = [kmax]
         else:
             ks = [1 if it.cost <= tau else split_k(it) for it in g]
@@ -442,6 +451,7 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
             _, best_r, best_slices, best_loads = cand
 
     plan = Plan(T, E, dtype, R, K, L, B, opts.lif_milli, opts.order_mode)
+    plan.sym_max = sym_max
     plan.slices = best_slices
     plan.max_ps = max(best_loads)
     plan.sum_ps = sum(best_loads)

@@ -59,7 +59,7 @@ class _Opts(ctypes.Structure):
     _fields_ = [("wg_per_cu", ctypes.c_int32), ("lds_budget_bytes", ctypes.c_int32), ("lif_milli", ctypes.c_int32),
                 ("order_mode", ctypes.c_int32), ("chunk_max_bytes", ctypes.c_int64),
                 ("beta", ctypes.POINTER(ctypes.c_double)), ("force_strategy", ctypes.POINTER(ctypes.c_int32)),
-                ("num_workers", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("num_workers", ctypes.c_int32), ("sym_max_gather", ctypes.c_int32)]
 
 
 class _Info(ctypes.Structure):
@@ -152,6 +152,7 @@ class _Marshal:
         o.order_mode = int(opts.get("order_mode", 0))
         o.chunk_max_bytes = int(opts.get("chunk_max_bytes", 0))
         o.num_workers = int(opts.get("num_workers", 0))
+        o.sym_max_gather = int(opts.get("sym_max", 0))
         beta = opts.get("beta")
         if beta is not None:
             b = np.ascontiguousarray(np.asarray(beta, dtype=np.float64))

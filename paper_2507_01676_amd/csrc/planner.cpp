@@ -333,9 +333,14 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     P.tau = static_cast<int64_t>((total1 + P.K - 1) / P.K);
 
     // P4
+    const int32_t sym_max = in.sym_max != 0 ? in.sym_max : kSymMaxDefault;
+    int32_t n_gather = 0;
+    for (const auto& g : P.groups) n_gather += (g[0].nchunks == 1 && g[0].strat == S_GATHER) ? 1 : 0;
+    const bool sym_gather = sym_max > 0 && n_gather <= sym_max;
+    out->sym_max = sym_max;
     for (auto& g : P.groups) {
       int32_t k = 1;
-      if (g[0].nchunks == 1 && g[0].strat == S_GATHER)
+      if (sym_gather && g[0].nchunks == 1 && g[0].strat == S_GATHER)
         k = P.kmax;
       else
         for (const Item& it : g) k = std::max(k, it.cost <= P.tau ? 1 : P.split_k(it));
@@ -429,8 +434,8 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
 std::string plan_text(const PlanOut& p) {
   std::string s = "embx-plan v1\n";
   char buf[512];
-  std::snprintf(buf, sizeof buf, "T %d E %d dtype %s R %d K %d L %lld B %d theta %d order %d\n", p.T, p.E,
-                p.f16 ? "f16" : "f32", p.R, p.K, static_cast<long long>(p.L), p.B, p.theta, p.order_mode);
+  std::snprintf(buf, sizeof buf, "T %d E %d dtype %s R %d K %d L %lld B %d theta %d order %d symmax %d\n", p.T, p.E,
+                p.f16 ? "f16" : "f32", p.R, p.K, static_cast<long long>(p.L), p.B, p.theta, p.order_mode, p.sym_max);
   s += buf;
   for (const PSlice& x : p.slices) {
     std::snprintf(buf, sizeof buf, "item %d %d %d %d %d %lld %lld %d %d %d %lld\n", x.wg, x.t, x.strat, x.chunk,

@@ -239,3 +239,27 @@ def test_single_lookup_tables_and_a_broken_promise(gpu, E, dtype):
     _, got2, nbad2 = run(c, batch2, wd, STRATS["gather"])   # the same statistics (max pooling 1)
     check_full(got2, hw, batch2, dtype, exact=True)
     assert nbad2 == want_bad == 9
+
+
+def test_many_tables_placed_whole(gpu):
+    """300 tables (more than the planner splits over all workers): small tables are placed
+    whole on single workers (the asymmetric mapping), large ones split; bit-exact on
+    integer tables, single- and multi-lookup bags mixed."""
+    log("300 tables, asymmetric placement")
+    g = np.random.default_rng(12)
+    rows = [int(x) for x in np.exp(g.uniform(np.log(10), np.log(50000), size=300))]
+    tabs = []
+    for t, m in enumerate(rows):
+        if t % 3 == 0:
+            tabs.append(W.TableSpec(m, "poisson", 3.0, 0, 9, "zipf", 1.1))
+        else:
+            tabs.append(W.TableSpec(m, "poisson", 1.0, 1, 1, "uniform", 1.0))
+    c = W.Config(110, "many tables E64 f32", 64, "f32", -1.0, 1.0, 256, tabs)
+    c.value_seeds = [W.value_seed(110, t) for t in range(c.T)]
+    batch = W.gen_batch(c, 0)
+    hw = host_tables(c, W.VAL_INTEGER)
+    p, got, nbad = run(c, batch, upload_tables(hw))
+    check_full(got, hw, batch, "f32", exact=True)
+    assert nbad == 0
+    ks = [int(ln.split()[8]) for ln in p.serialize().splitlines() if ln.startswith("item ")]
+    assert ks.count(1) > 100 and max(ks) <= p.info()["num_workers"]

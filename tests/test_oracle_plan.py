@@ -309,3 +309,34 @@ def test_lpt_bound_is_tight_on_the_classic_instance():
     p = OPL.plan_reference(rows, 64, "f32", stats, 1, 2, OPL.Options(beta=b, lif_milli=10 ** 9))
     assert sorted(s.cost for s in p.slices) == [2, 2, 2, 3, 3]
     assert p.max_ps == 7 and _opt_makespan([2, 2, 2, 3, 3], 2) == 6
+
+
+def test_many_gather_tables_are_placed_whole_not_split_over_all_workers():
+    # 200 small gather tables on 64 workers: T x K slices would swamp a launch, so past
+    # sym_max tables they are priced and split like any item; small ones stay whole and
+    # are spread over the workers by least-loaded placement (the asymmetric mapping)
+    g = np.random.default_rng(11)
+    rows = [int(x) for x in g.integers(1000, 100000, size=200)]
+    stats = [OPL.Stat(1.0) for _ in rows]
+    b = OPL.default_beta(256)
+    b[OPL.L0] = b[OPL.H0] = b[OPL.D0] = 1e12      # only GATHER is affordable
+    p = OPL.plan_reference(rows, 64, "f32", stats, 512, 64, OPL.Options(beta=b))
+    assert all(s.strat == OPL.GATHER for s in p.slices)
+    assert p.sym_max == OPL.SYM_MAX_DEFAULT
+    assert len(p.slices) < 200 * 64 // 4
+    whole = [s for s in p.slices if s.k == 1]
+    assert len(whole) >= 150
+    assert len({s.wg for s in whole}) == 64          # every worker gets whole tables
+    # each table is covered exactly once per bag
+    for t in range(200):
+        ks = {s.k for s in p.slices if s.t == t}
+        assert len(ks) == 1
+        assert sorted(s.j for s in p.slices if s.t == t) == list(range(ks.pop()))
+    # at or below sym_max every gather table is split over all workers
+    p2 = OPL.plan_reference(rows, 64, "f32", stats, 512, 64, OPL.Options(beta=b, sym_max=200))
+    assert all(s.k == 64 for s in p2.slices)
+    # a negative sym_max leaves every split to P4's cost rule (the LIF fallback, P7, could
+    # still make trailing tables symmetric: switched off here)
+    p3 = OPL.plan_reference(rows[:10], 64, "f32", stats[:10], 512, 64,
+                            OPL.Options(beta=b, sym_max=-1, lif_milli=10 ** 9))
+    assert all(s.k < 64 for s in p3.slices)

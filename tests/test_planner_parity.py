@@ -43,7 +43,7 @@ def _both(rows, E, dtype, stats, B, K, opts: OPL.Options):
            for s in stats]
     got = embx.plan_text(rows, E, dtype, cst, B, K, lds_budget=opts.lds_budget, lif_milli=opts.lif_milli,
                          chunk_max_bytes=opts.chunk_max_bytes, order_mode=opts.order_mode, beta=opts.beta,
-                         force=opts.force)
+                         force=opts.force, sym_max=opts.sym_max)
     return got, want
 
 
@@ -110,3 +110,14 @@ def test_cpp_planner_rejects_what_the_oracle_rejects():
         OPL.plan_reference([10, 20], 64, "f32", [OPL.Stat(1.0)] * 2, 8, 4, OPL.Options(beta=beta))
     with pytest.raises(embx.EmbxError):
         embx.plan_text([10, 20], 64, "f32", [dict(mean_pooling=1.0)] * 2, 8, 4, beta=beta)
+
+
+@pytest.mark.parametrize("T,sym_max", [(150, 0), (150, 200), (40, -1), (300, 64)])
+def test_cpp_planner_equals_oracle_with_many_tables(T, sym_max):
+    g = np.random.default_rng(T + sym_max)
+    rows = [int(x) for x in np.exp(g.uniform(np.log(10), np.log(2e6), size=T))]
+    stats = [OPL.Stat(float(g.choice([1.0, 1.0, 4.0, 20.0]))) for _ in range(T)]
+    opts = OPL.Options(sym_max=sym_max)
+    got, want = _both(rows, 64, "f32", stats, 1024, 128, opts)
+    assert got == want
+    assert f"symmax {sym_max if sym_max else OPL.SYM_MAX_DEFAULT}" in want
