@@ -280,7 +280,6 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     const int sw_per_wave = 64 / p->G;
     const int64_t bags_per_slice = static_cast<int64_t>(max_batch) / x.k;
     d.mode = (x.strat != S_DEDUP && s_t >= 4.0 * sw_per_wave && bags_per_slice <= 16 * (kBlock / 64)) ? 1 : 0;
-    d.wpf = static_cast<int16_t>(std::min(32767.0, std::max(1.0, std::floor(s_t + 0.5))));
     items.push_back(d);
     wg_ptr[x.wg + 1] += 1;
   }
@@ -494,7 +493,6 @@ emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t*
   a.E = plan->E;
   a.R = plan->R;
   a.lds_rows = plan->lds_rows;
-  a.n_items = static_cast<int32_t>(plan->plan.slices.size());
   a.trace = plan->d_trace;
   a.gr = plan->d_gr;
   a.gr_slot = plan->gr_slot;

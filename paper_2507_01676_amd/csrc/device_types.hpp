@@ -22,8 +22,7 @@ struct DevItem {
   int32_t hash_log2;    // HOT: log2 of the hash size
   int64_t hot_off;      // HOT: element offset of this table's hash / hot ids
   int32_t counter;      // chunked: combine counter of (table, j)
-  int16_t mode;         // 0: each sub-wavefront sums whole bags; 1: a wavefront per bag
-  int16_t wpf;          // expected lookups per bag (>= 1): weight of a bag in the gather split
+  int32_t mode;         // 0: each sub-wavefront sums whole bags; 1: a wavefront per bag
 };
 
 struct DevTable {
@@ -78,7 +77,6 @@ struct LookupArgs {
   int32_t E;
   int32_t R;                    // row bytes
   int32_t lds_rows;             // LDS bytes for rows (the budget L)
-  int32_t n_items;
   unsigned long long* trace;    // optional timers (see kTraceWorker), nullptr = off
   const GatherRun* gr;          // worker slots of gr_slot records: a GatherSlotHeader, then the
                                 // worker's runs (wave mode, single-lookup bags, SW mode)

@@ -24,8 +24,12 @@
 //          their ids held in LDS; hits read LDS, misses read HBM;
 //   DEDUP  a tile of up to kTile lookups is bitonic-sorted in LDS, each distinct
 //          row is fetched once into LDS, and the bags read their rows from there;
-//   GATHER rows straight from HBM; a worker's gather slices are flattened and
-//          split over its SWs (or wavefronts) by expected lookups.
+//   GATHER rows straight from HBM.  A worker's gather slices are flattened into
+//          three queues of small chunks: long bags (wave mode), bags of at most
+//          one lookup (a chunk of kU bags is one SW step and each row is its
+//          bag's output), and the rest (SW mode, walked as one stream across
+//          chunks).  Invalid ids read a row of zeros; fp16 halves are added with
+//          a mixed-precision fma.
 //
 // All pointers carry their address space (1 = global, 3 = LDS) so that every
 // access compiles to a global_* or ds_* instruction, never a flat one.
@@ -88,15 +92,6 @@ __device__ __forceinline__ void acc_add(Acc<false>& a, const uint4 r) {
   a.v[3] += __uint_as_float(r.w);
 }
 
-__device__ __forceinline__ void acc_add(Acc<true>& a, const uint4 r) {
-  const uint32_t w[4] = {r.x, r.y, r.z, r.w};
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    a.v[2 * q] += __half2float(__ushort_as_half(static_cast<unsigned short>(w[q] & 0xffffu)));
-    a.v[2 * q + 1] += __half2float(__ushort_as_half(static_cast<unsigned short>(w[q] >> 16)));
-  }
-}
-
 // fp16 halves added as x * one + acc with one = 1 at run time (opaque to the compiler):
 // the product is exact and the fma rounds once, so the sum is the same as widening and
 // adding, in one mixed-precision instruction per half instead of two
@@ -147,7 +142,6 @@ __device__ __forceinline__ void sts16(lchar* p, const uint4 v) { *reinterpret_ca
 __device__ __forceinline__ uint4 zero16() { return make_uint4(0u, 0u, 0u, 0u); }
 
 __device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
-__device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 
 __device__ __forceinline__ int slice_lo(int j, int k, int B) {
   return static_cast<int>((static_cast<int64_t>(j) * B) / k);
@@ -179,12 +173,8 @@ struct RowBase {
   bool active;            // this lane holds part of the row
   bool count;             // this slice reports out-of-range ids
   GMEM unsigned long long* err;
-  gchar* zero;            // R zero bytes (+ lane_c): what an invalid id reads in the gather walkers
+  gchar* zero;            // R zero bytes (+ lane_c): what an invalid id (or a position past the end) reads
   float one;              // 1.0f from the launch arguments (see acc_add)
-
-  __device__ __forceinline__ gchar* row(int32_t ix) const {
-    return w + static_cast<int64_t>(ix > 0 ? ix : 0) * R + lane_c;
-  }
   __device__ __forceinline__ void bad() const {
     if (count) atomicAdd(err, 1ull);
   }
@@ -268,7 +258,7 @@ struct FHot : RowBase {
 
 // a tile's distinct rows in LDS (first capd of them, slot order); the rest read HBM
 struct FDedup : RowBase {
-  static constexpr bool kPositional = true;   // probes by position in the tile
+  [[maybe_unused]] static constexpr bool kPositional = true;   // probes by position in the tile
   using Raw = uint4;
   const lchar* lds;
   const LMEM int16_t* inv;  // slot of each tile position, -1 for an invalid id
