@@ -936,6 +936,14 @@ struct SegHead {
 // segments ahead and its first ids by the last step of the segment before it, so a
 // step's single wait covers everything the next step needs.  Per bag the order of
 // additions is the lookup order, as in walk_seq.
+//
+// Lane i of the SW holds the end of bag b + i (`win`, reloaded every step), so at the
+// start of a step each lane knows whether its bag ends inside the step and before which
+// of the kU lookups; an OR over the SW's lanes gives the step's mask of bag ends, and
+// the additions then run straight through with one masked store per bag end.  A step
+// in which a bag ends empty, or whose bag ends run past the G-bag window, takes a
+// slower path that reads each bag's end as it gets there (the whole wavefront takes
+// it if one of its SWs needs it).
 template <int G, bool F16>
 __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ indices,
                                             GMEM const int64_t* __restrict__ offsets, GMEM float* __restrict__ out,
@@ -955,10 +963,9 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
   wait_all();
 
   GMEM const int64_t* off;
-  GMEM float* ob;
   GMEM float* obb;   // bag b's output (this lane's part)
-  int be, wb, b;
-  int64_t p, pend, win, win2;
+  int be, b;
+  int64_t p, pend, win;
   Acc<F16> acc;
   acc_zero(acc);
   auto open = [&]() {   // make cur (head h0) the current segment
@@ -966,15 +973,12 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     f.w = as_global(static_cast<const char*>(g.w));
     f.rows = static_cast<uint64_t>(g.rows);
     off = offsets + static_cast<int64_t>(g.table) * B;
-    ob = out + static_cast<int64_t>(g.table) * E + lane_sw * NA;
     be = cur.be;
-    wb = cur.bs;
     b = cur.bs;
-    obb = ob + static_cast<int64_t>(b) * ostride;
+    obb = out + static_cast<int64_t>(g.table) * E + lane_sw * NA + static_cast<int64_t>(b) * ostride;
     p = h0.p;
     pend = h0.pend;
     win = h0.win;
-    win2 = off[min(wb + G + 1 + lane_sw, be)];
   };
   auto advance = [&]() {
     cur = s1;
@@ -991,12 +995,6 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
       acc_zero(acc);
     }
   };
-  auto end_of = [&](int bb) -> int64_t {
-    const int d = bb - wb;
-    if (d < G) return __shfl(win, d, G);
-    if (d < 2 * G) return __shfl(win2, d - G, G);
-    return off[min(bb + 1, be)];   // more than G empty bags within one step
-  };
   // the first segment with lookups
   while (true) {
     open();
@@ -1007,12 +1005,18 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
   }
   Ids<G> ids;
   ids.load(indices, p, 1, pend, p, lane_sw);
-  int64_t bag_end = end_of(b);
   wait_all();
   while (true) {
     const int n = static_cast<int>(min64(kU, pend - p));
-    // the current bag ends before the step's lookup u = rel (rel > kU: not in this step)
-    int rel = static_cast<int>(min64(bag_end - p, kU + 1));
+    // lane i: does bag b + i end inside this step, before lookup d?
+    const int64_t du = win - p;
+    const bool here = du < n;
+    const int d = here ? static_cast<int>(du) : 31;
+    uint32_t fm = here ? 1u << d : 0u;
+#pragma unroll
+    for (int x = 1; x < G; x <<= 1) fm |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(fm), x, G));
+    const bool empty_here = here && lane_sw > 0 && __shfl_up(d, 1, G) == d;
+    const bool fast = !__any(empty_here || (here && lane_sw == G - 1));
     gchar* ra[kU];
     ids.resolve_addr(f, lane_sw, ra);
     uint4 raw[kU];
@@ -1025,30 +1029,39 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
       ids.load(indices, pn, 1, pend, p, lane_sw);
     else if (has1)
       ids.load(indices, h1.p, 1, h1.pend, h1.p, lane_sw);
-    win2 = off[min(wb + G + 1 + lane_sw, be)];
-    wait_all();   // the one wait of the step
+    if (fast) {
+      const int m = __popc(fm);   // bags that end in this step
+      win = off[min(b + m + 1 + lane_sw, be)];
+      wait_all();   // the one wait of the step
+      // (a lane outside the row stores nothing and keeps no output pointer: its bag
+      // count b follows from m alone)
+      const uint32_t fs = f.active ? fm : 0u;
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      if (u < n) {
-        while (u == rel) {
+      for (int u = 0; u < kU; ++u) {   // lookups past the end read the zero row
+        if ((fs >> u) & 1u) {
+          acc_store(obb, acc);
+          acc_zero(acc);
+          obb += ostride;
+        }
+        acc_add(acc, raw[u], f.one);
+      }
+      b += m;
+    } else {
+      wait_all();
+      int64_t e = off[min(b + 1, be)];   // end of bag b
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        while (u < n && e == p + u) {
           if (f.active) acc_store(obb, acc);
           acc_zero(acc);
           ++b;
           obb += ostride;
-          bag_end = end_of(b);
-          rel = static_cast<int>(min64(bag_end - p, kU + 1));
+          e = off[min(b + 1, be)];
         }
         acc_add(acc, raw[u], f.one);
       }
-    }
-    if (b - wb >= G) {
-      if (b - wb < 2 * G) {
-        wb += G;
-        win = win2;
-      } else {
-        wb = b;
-        win = off[min(b + 1 + lane_sw, be)];
-      }
+      win = off[min(b + 1 + lane_sw, be)];
+      wait_all();
     }
     p = pn;
     if (seg_end) {
@@ -1063,8 +1076,10 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
         reload = true;
         if (!has1) return;
       }
-      if (reload) ids.load(indices, p, 1, pend, p, lane_sw);
-      bag_end = end_of(b);
+      if (reload) {
+        ids.load(indices, p, 1, pend, p, lane_sw);
+        wait_all();
+      }
     }
   }
 }
