@@ -153,8 +153,14 @@ __device__ __forceinline__ int slice_lo(int j, int k, int B) {
 // only when the values are used.  With no branches around loads, the compiler can
 // keep a step to a single wait on the memory counter.
 
-// Waits until every memory operation this wavefront issued has completed.
-__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
+// Waits for every memory operation in flight.  The empty asm with a memory clobber
+// keeps the compiler from moving loads written before the wait to after it (the
+// waitcnt builtin alone does not order memory operations): a load sunk past the
+// wait would be issued late and waited for on its own.
+__device__ __forceinline__ void wait_all() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0);
+}
 
 // A run of bags [bs, be) of one table.
 struct Seg {
@@ -931,6 +937,32 @@ struct SegHead {
   }
 };
 
+// OR of x over the G lanes of this SW.  Within a row of 16 lanes the exchanges are DPP
+// lane moves (no LDS round trip): swap neighbours, swap pairs, mirror the half rows,
+// mirror the row; wider SWs add shuffles across rows.
+template <int G>
+__device__ __forceinline__ uint32_t sw_or(uint32_t x) {
+  if constexpr (G >= 2) x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0xB1, 0xF, 0xF, true));
+  if constexpr (G >= 4) x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x4E, 0xF, 0xF, true));
+  if constexpr (G >= 8) x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x141, 0xF, 0xF, true));
+  if constexpr (G >= 16) x |= static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x140, 0xF, 0xF, true));
+  if constexpr (G >= 32) x |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 16));
+  if constexpr (G >= 64) x |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 32));
+  return x;
+}
+
+// number of lanes of this SW whose flag is set (lane_sw: this lane's index in the SW)
+template <int G>
+__device__ __forceinline__ int sw_count(bool flag, int lane_sw) {
+  const uint64_t bal = __ballot(flag);
+  if constexpr (G == 64) {
+    return __popcll(bal);
+  } else {
+    const int base = static_cast<int>(__lane_id()) - lane_sw;
+    return __popcll((bal >> base) & ((uint64_t(1) << G) - 1));
+  }
+}
+
 // SW mode over the stream of segments a RunQueue yields (gather rows).  Steps run on
 // across segment boundaries without a pause: a segment's head (SegHead) is loaded two
 // segments ahead and its first ids by the last step of the segment before it, so a
@@ -980,14 +1012,23 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     pend = h0.pend;
     win = h0.win;
   };
+  // The head of segment s2 is loaded with the next step's loads (h2_due), so that the
+  // step's single wait covers it and the loop's entry never waits on a load (a wait
+  // there would also wait for the bag stores of the step before).
+  bool h2_due = false;
   auto advance = [&]() {
+    if (h2_due) {   // two segments opened without a step between them
+      h2.issue(off_of(s2), s2, lane_sw);
+      h2_due = false;
+      wait_all();
+    }
     cur = s1;
     h0 = h1;
     s1 = s2;
     h1 = h2;
     has1 = has2;
     has2 = has1 && q.next(s2);
-    if (has2) h2.issue(off_of(s2), s2, lane_sw);
+    h2_due = has2;
   };
   auto flush = [&]() {   // the bags left in the segment end here (the last one holds acc)
     for (; b < be; ++b, obb += ostride) {
@@ -1012,11 +1053,10 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     const int64_t du = win - p;
     const bool here = du < n;
     const int d = here ? static_cast<int>(du) : 31;
-    uint32_t fm = here ? 1u << d : 0u;
-#pragma unroll
-    for (int x = 1; x < G; x <<= 1) fm |= static_cast<uint32_t>(__shfl_xor(static_cast<int>(fm), x, G));
-    const bool empty_here = here && lane_sw > 0 && __shfl_up(d, 1, G) == d;
-    const bool fast = !__any(empty_here || (here && lane_sw == G - 1));
+    const uint32_t fm = sw_or<G>(here ? 1u << d : 0u);
+    // the fast path needs one bag per marked lookup (no empty bag ends in the step) and
+    // the step's last bag end inside the window
+    const bool fast = !__any(__popc(fm) != sw_count<G>(here, lane_sw) || (here && lane_sw == G - 1));
     gchar* ra[kU];
     ids.resolve_addr(f, lane_sw, ra);
     uint4 raw[kU];
@@ -1029,6 +1069,10 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
       ids.load(indices, pn, 1, pend, p, lane_sw);
     else if (has1)
       ids.load(indices, h1.p, 1, h1.pend, h1.p, lane_sw);
+    if (h2_due) {
+      h2.issue(off_of(s2), s2, lane_sw);
+      h2_due = false;
+    }
     if (fast) {
       const int m = __popc(fm);   // bags that end in this step
       win = off[min(b + m + 1 + lane_sw, be)];
