@@ -170,3 +170,137 @@ def test_planted_mistakes_are_caught(mistake):
     want = np.stack([A[t] @ weights[t].astype(np.float64) for t in range(T)], axis=1)
     assert np.allclose(ref, want, rtol=1e-6, atol=1e-6)
     assert not np.allclose(bad, want, rtol=1e-6, atol=1e-6)
+
+
+# ---- mean pooling and per-lookup weights (Sec. II-B: sum or average)
+
+def _psw(seed, n):
+    return np.random.default_rng(seed).uniform(-2.0, 2.0, size=n).astype(np.float32)
+
+
+def _dense_weighted(bt, rows, T, B, psw):
+    """A_t[b, r] = sum of the weights of the lookups of row r in bag (t, b); n[t][b] = bag length."""
+    A = [np.zeros((B, rows[t]), dtype=np.float64) for t in range(T)]
+    n = np.zeros((T, B), dtype=np.int64)
+    for t in range(T):
+        for b in range(B):
+            lo, hi = bt.offsets[t * B + b], bt.offsets[t * B + b + 1]
+            n[t, b] = hi - lo
+            for k in range(lo, hi):
+                A[t][b, bt.indices[k]] += 1.0 if psw is None else float(psw[k])
+    return A, n
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("weighted", [False, True])
+def test_mean_and_weights_match_dense_matrices(seed, weighted):
+    T, B = 3, 6
+    weights, bt, rows = _rand_case(300 + seed, T=T, B=B)
+    psw = _psw(seed, bt.indices.size) if weighted else None
+    pooling = ["mean", "sum", "mean"]
+    ref, mag, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, pooling=pooling, psw=psw)
+    A, n = _dense_weighted(bt, rows, T, B, psw)
+    for t in range(T):
+        want = A[t] @ weights[t].astype(np.float64)
+        wmag = np.abs(A[t]) @ np.abs(weights[t].astype(np.float64)) if not weighted else None
+        if pooling[t] == "mean":
+            want = want / np.maximum(n[t], 1)[:, None]
+        assert np.allclose(ref[:, t, :], want, rtol=1e-6, atol=1e-6)
+        if wmag is not None:
+            wmag = wmag / (np.maximum(n[t], 1)[:, None] if pooling[t] == "mean" else 1)
+            assert np.allclose(mag[:, t, :], wmag, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_mean_and_weights_match_torch_embedding_bag(seed):
+    T, B = 3, 7
+    weights, bt, rows = _rand_case(400 + seed, T=T, B=B, maxpf=6)
+    psw = _psw(10 + seed, bt.indices.size)
+    mean, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, pooling="mean")
+    wsum, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, psw=psw)
+    for t in range(T):
+        lo = int(bt.offsets[t * B])
+        hi = int(bt.offsets[t * B + B])
+        idx = torch.from_numpy(bt.indices[lo:hi].copy())
+        off = torch.from_numpy((bt.offsets[t * B: t * B + B] - lo).copy())
+        w = torch.from_numpy(weights[t].astype(np.float64))
+        got_mean = torch.nn.functional.embedding_bag(idx, w, off, mode="mean").numpy()
+        got_w = torch.nn.functional.embedding_bag(idx, w, off, mode="sum",
+                                                  per_sample_weights=torch.from_numpy(psw[lo:hi].astype(np.float64))).numpy()
+        assert np.allclose(mean[:, t, :], got_mean, rtol=1e-6, atol=1e-6)
+        assert np.allclose(wsum[:, t, :], got_w, rtol=1e-6, atol=1e-6)
+
+
+def test_mean_and_weights_match_python_loops_with_fp16_and_bad_indices():
+    T, B = 2, 5
+    weights, bt, rows = _rand_case(17, T=T, B=B, E=16, dtype=np.float16)
+    bt.indices[0] = -4
+    bt.indices[-1] = rows[1]
+    psw = _psw(3, bt.indices.size)
+    for pooling in ("sum", "mean", ["mean", "sum"]):
+        ref, _, bad = OP.pool_reference(weights, bt.indices, bt.offsets, B, pooling=pooling, psw=psw)
+        loops, bad2 = OP.pool_loops(weights, bt.indices, bt.offsets, B, pooling=pooling, psw=psw)
+        assert bad == bad2 >= 1
+        assert np.array_equal(ref, np.array(loops, dtype=np.float64).astype(np.float32))
+
+
+def test_mean_and_weight_invariants():
+    T, B = 3, 6
+    weights, bt, rows = _rand_case(500, T=T, B=B)
+    s, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B)
+    # unit weights change nothing; weight 2 doubles every sum exactly (a power of two)
+    ones = np.ones(bt.indices.size, np.float32)
+    s1, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, psw=ones)
+    s2, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, psw=2 * ones)
+    assert np.array_equal(s1, s) and np.array_equal(s2, 2 * s)
+    # weights are linear: w1 + w2 gives the sum of the two weighted sums
+    a, b = _psw(1, bt.indices.size), _psw(2, bt.indices.size)
+    ra, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, psw=a)
+    rb, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, psw=b)
+    rab, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, psw=a.astype(np.float64) + b)
+    assert np.allclose(rab, ra.astype(np.float64) + rb, rtol=1e-5, atol=1e-5)
+    # a bag of k copies of one row averages to that row, bit for bit; empty bags stay +0.0
+    wd = W.table_rows_block(0, 0, 5, 8, "f32", seed=3, mode=W.VAL_INTEGER)
+    bt2 = W.batch_from_bags(1, 3, [[4] * 6, [], [1, 3]])
+    m, _, _ = OP.pool_reference([wd], bt2.indices, bt2.offsets, 3, pooling="mean")
+    assert np.array_equal(m[0, 0], wd[4])
+    assert np.all(m[1, 0] == 0) and not np.any(np.signbit(m[1, 0]))
+    assert np.array_equal(m[2, 0], ((wd[1].astype(np.float64) + wd[3]) / 2).astype(np.float32))
+    # one-hot table under mean pooling: the bag's histogram over its length
+    E = 16
+    bags = [[1, 1, 5], [0], [15, 2, 2, 2]]
+    bt3 = W.batch_from_bags(1, 3, bags)
+    h, _, _ = OP.pool_reference([np.eye(E, dtype=np.float32)], bt3.indices, bt3.offsets, 3, pooling="mean")
+    for b, bag in enumerate(bags):
+        want = np.bincount(np.array(bag), minlength=E) / len(bag)
+        assert np.array_equal(h[b, 0], want.astype(np.float32))
+    # an out-of-range id adds nothing but still counts in the mean's divisor
+    bt4 = W.batch_from_bags(1, 1, [[2, 99]])
+    q, _, bad = OP.pool_reference([wd], bt4.indices, bt4.offsets, 1, pooling="mean")
+    assert bad == 1 and np.array_equal(q[0, 0], (wd[2].astype(np.float64) / 2).astype(np.float32))
+
+
+@pytest.mark.parametrize("mistake", ["divide_by_n_plus_1", "ignore_weights", "weights_of_next_lookup",
+                                     "mean_before_weights_sum"])
+def test_planted_mistakes_in_mean_and_weights_are_caught(mistake):
+    """A plausible slip (planted here, on the CPU) fails the dense-matrix pin."""
+    T, B = 3, 6
+    weights, bt, rows = _rand_case(88, T=T, B=B, allow_empty=False)
+    psw = _psw(8, bt.indices.size)
+    A, n = _dense_weighted(bt, rows, T, B, psw)
+    want = np.stack([(A[t] @ weights[t].astype(np.float64)) / n[t][:, None] for t in range(T)], axis=1)
+    ref, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, pooling="mean", psw=psw)
+    assert np.allclose(ref, want, rtol=1e-6, atol=1e-6)
+    if mistake == "divide_by_n_plus_1":
+        bad = ref * (n.T / (n.T + 1))[:, :, None]
+    elif mistake == "ignore_weights":
+        bad, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, pooling="mean")
+    elif mistake == "weights_of_next_lookup":
+        bad, _, _ = OP.pool_reference(weights, bt.indices, bt.offsets, B, pooling="mean", psw=np.roll(psw, 1))
+    else:   # the mean of the weights times the mean of the rows
+        bad = np.zeros_like(ref)
+        for t in range(T):
+            for b in range(B):
+                lo, hi = bt.offsets[t * B + b], bt.offsets[t * B + b + 1]
+                bad[b, t] = psw[lo:hi].mean() * weights[t][bt.indices[lo:hi]].astype(np.float64).mean(axis=0)
+    assert not np.allclose(bad, want, rtol=1e-6, atol=1e-6)
