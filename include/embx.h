@@ -10,6 +10,10 @@
  *
  *     out[b, t, :] = sum over k in bag(t, b) of  W_t[indices[k], :]
  *
+ * Sec. II-B also names averaging: a table may be mean-pooled (the bag's sum over
+ * its length n_bt), and each lookup may carry a weight w_k that scales its row
+ * (emb_lookup_weighted): out[b, t, :] = (1 or 1/n_bt) * sum of w_k W_t[indices[k], :].
+ *
  * Planning follows Sec. III: a linear cost model (Eq. (2)) scores each table
  * under four per-core data flows and a greedy algorithm maps tables, row chunks
  * and batch slices asymmetrically onto the GPU's workers (Sec. III-B steps 1-4,
@@ -42,6 +46,11 @@ typedef enum {
 } emb_status_t;
 
 typedef enum { EMB_DTYPE_F32 = 0, EMB_DTYPE_F16 = 1 } emb_dtype_t;
+
+/* Reduction of a table's bags (Sec. II-B): the sum, or the sum over the bag length
+ * (an empty bag gives +0.0 either way; an out-of-range index adds nothing but counts
+ * in the length). */
+typedef enum { EMB_POOL_SUM = 0, EMB_POOL_MEAN = 1 } emb_pooling_t;
 
 /* Per-table data flows (Sec. II-B mapped onto a CU):
  *   LDS    -- the table, or a row chunk of it (Sec. III-B), staged into LDS and read from there
@@ -104,6 +113,8 @@ typedef struct {
   int32_t sym_max_gather;   /* GATHER tables are split over all workers (symmetric partitioning,
                                Sec. III-A) while the plan has at most this many of them, else
                                placed by cost like the rest (Sec. III-B); 0 -> 64, < 0 -> never */
+  const int32_t* pooling;   /* host, T entries of emb_pooling_t, or NULL (all SUM); does not change
+                               the placement, only each bag's final scaling                       */
 } emb_plan_options_t;
 
 typedef struct emb_plan emb_plan_t;   /* opaque */
@@ -144,6 +155,15 @@ emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights)
  * Calls on one plan must not overlap (the chunk workspace is per plan). */
 emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets,
                         int32_t batch, float* out, void* stream);
+
+/* emb_lookup with per-lookup weights (per-sample weights): weights is device fp32
+ * [offsets[T*batch]], 4-byte aligned, aligned element for element with indices; lookup k
+ * adds weights[k] * W_t[indices[k], :] to its bag, computed as one fused multiply-add per
+ * element in fp32 (before the division of a mean-pooled table).  A weight of an
+ * out-of-range index is ignored.  NULL weights is an invalid argument.  Same launch, stream
+ * and overlap rules as emb_lookup. */
+emb_status_t emb_lookup_weighted(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets,
+                                 const float* weights, int32_t batch, float* out, void* stream);
 
 /* Synchronizes `stream`, returns the number of out-of-range indices seen since the last
  * call in *n_bad (may be NULL) and resets the counter; EMB_ERR_INDEX_OUT_OF_RANGE if any. */

@@ -34,10 +34,12 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_OUT_OF_MEMORY, ERR_DEVICE, ERR_NO
 DTYPE_F32, DTYPE_F16 = 0, 1
 STRAT_AUTO, STRAT_LDS, STRAT_HOT, STRAT_DEDUP, STRAT_GATHER = -1, 0, 1, 2, 3
 STRATEGY_NAMES = {0: "LDS", 1: "HOT", 2: "DEDUP", 3: "GATHER"}
+POOL_SUM, POOL_MEAN = 0, 1
+POOLING_CODES = {"sum": POOL_SUM, "mean": POOL_MEAN}
 BETA_COUNT = 10
 MAX_HOT_STATS = 4096
 
-EXPORTED = ["emb_plan_create", "emb_plan_bind_weights", "emb_lookup", "emb_plan_check_errors",
+EXPORTED = ["emb_plan_create", "emb_plan_bind_weights", "emb_lookup", "emb_lookup_weighted", "emb_plan_check_errors",
             "emb_plan_serialize", "emb_plan_get_info", "emb_plan_destroy", "emb_plan_text",
             "emb_status_string", "emb_debug_dedup_tile", "emb_debug_hot_probe", "embx_fill_table",
             "emb_plan_set_trace"]
@@ -59,7 +61,8 @@ class _Opts(ctypes.Structure):
     _fields_ = [("wg_per_cu", ctypes.c_int32), ("lds_budget_bytes", ctypes.c_int32), ("lif_milli", ctypes.c_int32),
                 ("order_mode", ctypes.c_int32), ("chunk_max_bytes", ctypes.c_int64),
                 ("beta", ctypes.POINTER(ctypes.c_double)), ("force_strategy", ctypes.POINTER(ctypes.c_int32)),
-                ("num_workers", ctypes.c_int32), ("sym_max_gather", ctypes.c_int32)]
+                ("num_workers", ctypes.c_int32), ("sym_max_gather", ctypes.c_int32),
+                ("pooling", ctypes.POINTER(ctypes.c_int32))]
 
 
 class _Info(ctypes.Structure):
@@ -78,6 +81,7 @@ _lib.emb_plan_create.argtypes = [ctypes.POINTER(_vp), _i32, ctypes.POINTER(_i64)
                                  ctypes.POINTER(_Stats), _i32, ctypes.POINTER(_Opts)]
 _lib.emb_plan_bind_weights.argtypes = [_vp, ctypes.POINTER(_vp)]
 _lib.emb_lookup.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp]
+_lib.emb_lookup_weighted.argtypes = [_vp, _vp, _vp, _vp, _i32, _vp, _vp]
 _lib.emb_plan_check_errors.argtypes = [_vp, _vp, ctypes.POINTER(_i64)]
 _lib.emb_plan_serialize.argtypes = [_vp, ctypes.c_char_p, _sz, ctypes.POINTER(_sz)]
 _lib.emb_plan_get_info.argtypes = [_vp, ctypes.POINTER(_Info)]
@@ -165,6 +169,14 @@ class _Marshal:
             assert f.size == T
             self.keep.append(f)
             o.force_strategy = f.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        pooling = opts.get("pooling")
+        if pooling is not None:
+            if isinstance(pooling, (str, int)):
+                pooling = [pooling] * T
+            pc = np.ascontiguousarray(np.asarray([POOLING_CODES.get(x, x) for x in pooling], dtype=np.int32))
+            assert pc.size == T
+            self.keep.append(pc)
+            o.pooling = pc.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
         self.opts = o
 
 
@@ -219,20 +231,32 @@ class Plan:
         self._weights = list(weights)
         return self
 
-    def lookup(self, indices, offsets, batch: int, out=None, stream=None):
+    def lookup(self, indices, offsets, batch: int, out=None, stream=None, weights=None):
+        """One batch (emb_lookup); with ``weights`` (fp32 device tensor aligned with
+        ``indices``) each lookup's row is scaled by its weight (emb_lookup_weighted)."""
         import torch
         if out is None:
             out = torch.empty((batch, self.T, self.E), dtype=torch.float32, device=indices.device)
         assert indices.dtype == torch.int64 and offsets.dtype == torch.int64 and out.dtype == torch.float32
         assert out.is_contiguous() and out.numel() >= batch * self.T * self.E
         assert offsets.numel() >= self.T * batch + 1
-        _check(_lib.emb_lookup(self._h, indices.data_ptr(), offsets.data_ptr(), int(batch), out.data_ptr(),
-                               _stream_ptr(stream)), "emb_lookup")
+        if weights is None:
+            _check(_lib.emb_lookup(self._h, indices.data_ptr(), offsets.data_ptr(), int(batch), out.data_ptr(),
+                                   _stream_ptr(stream)), "emb_lookup")
+        else:
+            assert weights.dtype == torch.float32 and weights.is_contiguous() and weights.numel() >= indices.numel()
+            _check(_lib.emb_lookup_weighted(self._h, indices.data_ptr(), offsets.data_ptr(), weights.data_ptr(),
+                                            int(batch), out.data_ptr(), _stream_ptr(stream)), "emb_lookup_weighted")
         return out
 
-    def lookup_ptr(self, indices_ptr: int, offsets_ptr: int, batch: int, out_ptr: int, stream_ptr) -> None:
-        """Raw-pointer launch (benchmark loop)."""
-        _check(_lib.emb_lookup(self._h, indices_ptr, offsets_ptr, int(batch), out_ptr, stream_ptr), "emb_lookup")
+    def lookup_ptr(self, indices_ptr: int, offsets_ptr: int, batch: int, out_ptr: int, stream_ptr,
+                   weights_ptr: int = 0) -> None:
+        """Raw-pointer launch (benchmark loop); weights_ptr != 0 -> emb_lookup_weighted."""
+        if weights_ptr:
+            _check(_lib.emb_lookup_weighted(self._h, indices_ptr, offsets_ptr, weights_ptr, int(batch), out_ptr,
+                                            stream_ptr), "emb_lookup_weighted")
+        else:
+            _check(_lib.emb_lookup(self._h, indices_ptr, offsets_ptr, int(batch), out_ptr, stream_ptr), "emb_lookup")
 
     def set_trace(self, buf) -> int:
         """Records per-slice timers into device uint64/int64 tensor ``buf`` (None: off).

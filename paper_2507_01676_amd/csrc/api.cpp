@@ -46,6 +46,7 @@ struct emb_plan {
   const char* d_zero_row = nullptr;      // R zero bytes
   bool staged = false;                   // the plan has LDS / HOT / DEDUP slices
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
+  std::vector<int32_t> mean;             // per table: 1 = mean pooling
 };
 
 namespace {
@@ -173,8 +174,16 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   PlanIn in;
   emb_status_t s = to_plan_in(num_tables, rows, embedding_dim, dtype, stats, max_batch, K, opts, L, &in);
   if (s != EMB_OK) return s;
+  std::vector<int32_t> mean(num_tables, 0);
+  if (opts && opts->pooling) {
+    for (int32_t t = 0; t < num_tables; ++t) {
+      if (opts->pooling[t] != EMB_POOL_SUM && opts->pooling[t] != EMB_POOL_MEAN) return EMB_ERR_INVALID_ARGUMENT;
+      mean[t] = opts->pooling[t] == EMB_POOL_MEAN ? 1 : 0;
+    }
+  }
   emb_plan* p = new (std::nothrow) emb_plan();
   if (!p) return EMB_ERR_OUT_OF_MEMORY;
+  p->mean = mean;
   std::string err;
   const int rc = build_plan(in, &p->plan, &err);
   if (rc != 0) {
@@ -274,6 +283,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     d.hash_log2 = x.strat == S_HOT ? p->hot_table_log2[x.t] : 0;
     d.hot_off = x.strat == S_HOT ? p->hot_table_off[x.t] : 0;
     d.counter = x.nchunks > 1 ? ctr_base[x.t] + x.j : 0;
+    d.mean = mean[x.t];
     // long bags with few of them per slice: a wavefront per bag (not for DEDUP,
     // whose row source is addressed by tile position)
     const double s_t = stats[x.t].mean_pooling;
@@ -356,6 +366,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
           r.k = d.k;
           r.cb = cb;
           r.chunk_base = static_cast<int32_t>(base[cls]);
+          r.mean = mean[d.table];
           gr.push_back(r);
           base[cls] += nc;
           nrun[cls] += 1;
@@ -464,15 +475,17 @@ emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights)
   return EMB_OK;
 }
 
-emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets, int32_t batch, float* out,
-                        void* stream) {
+namespace {
+
+emb_status_t lookup_impl(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets, const float* weights,
+                         bool weighted, int32_t batch, float* out, void* stream) {
   if (!plan) return EMB_ERR_INVALID_ARGUMENT;
   if (batch < 0 || batch > plan->Bmax) return EMB_ERR_INVALID_ARGUMENT;
   if (!plan->bound) return EMB_ERR_NOT_BOUND;
   if (batch == 0) return EMB_OK;
-  if (!indices || !offsets || !out) return EMB_ERR_INVALID_ARGUMENT;
+  if (!indices || !offsets || !out || (weighted && !weights)) return EMB_ERR_INVALID_ARGUMENT;
   if ((reinterpret_cast<uintptr_t>(out) & 15u) != 0 || (reinterpret_cast<uintptr_t>(indices) & 7u) != 0 ||
-      (reinterpret_cast<uintptr_t>(offsets) & 7u) != 0)
+      (reinterpret_cast<uintptr_t>(offsets) & 7u) != 0 || (reinterpret_cast<uintptr_t>(weights) & 3u) != 0)
     return EMB_ERR_INVALID_ARGUMENT;
   LookupArgs a;
   a.items = plan->d_items;
@@ -498,7 +511,20 @@ emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t*
   a.gr_slot = plan->gr_slot;
   a.zero_row = plan->d_zero_row;
   a.one = 1.0f;
-  return st(launch_lookup(a, plan->G, plan->f16, plan->staged, plan->K, plan->lds_bytes, stream));
+  a.weights = weighted ? weights : nullptr;
+  return st(launch_lookup(a, plan->G, plan->f16, plan->staged, weighted, plan->K, plan->lds_bytes, stream));
+}
+
+}  // namespace
+
+emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets, int32_t batch, float* out,
+                        void* stream) {
+  return lookup_impl(plan, indices, offsets, nullptr, false, batch, out, stream);
+}
+
+emb_status_t emb_lookup_weighted(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets,
+                                 const float* weights, int32_t batch, float* out, void* stream) {
+  return lookup_impl(plan, indices, offsets, weights, true, batch, out, stream);
 }
 
 emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_bad) {

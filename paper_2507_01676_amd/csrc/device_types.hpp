@@ -23,6 +23,8 @@ struct DevItem {
   int64_t hot_off;      // HOT: element offset of this table's hash / hot ids
   int32_t counter;      // chunked: combine counter of (table, j)
   int32_t mode;         // 0: each sub-wavefront sums whole bags; 1: a wavefront per bag
+  int32_t mean;         // 1: the table's bags are averaged (sum over the bag length)
+  int32_t pad;
 };
 
 struct DevTable {
@@ -43,7 +45,8 @@ struct GatherRun {
   int32_t j, k;
   int32_t cb;
   int32_t chunk_base;
-  int32_t pad[3];
+  int32_t mean;         // 1: the table's bags are averaged
+  int32_t pad[2];
 };
 static_assert(sizeof(GatherRun) == 48, "GatherRun is staged as three 16-byte pieces");
 // The first record of a worker's slot: how its runs split into queues.
@@ -82,7 +85,8 @@ struct LookupArgs {
                                 // worker's runs (wave mode, single-lookup bags, SW mode)
   int32_t gr_slot;
   const void* zero_row;         // R zero bytes: the row an invalid id reads in the gather walkers
-  float one;                    // 1.0f, opaque to the compiler (fp16 rows are added as x * one + acc)
+  float one;                    // 1.0f, opaque to the compiler (rows are added as x * one + acc)
+  const float* weights;         // per-lookup weights aligned with indices (weighted launches), else nullptr
 };
 
 // Timer layout (100 MHz real-time counter ticks):
@@ -93,7 +97,8 @@ struct LookupArgs {
 constexpr int kTraceWorker = 2 + kBlock / 64;
 
 // Host-callable launchers (defined in lookup.hip).
-int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, int grid, int lds_bytes, void* stream);
+int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
+                  void* stream);
 int prepare_lookup_kernels(int lds_bytes);
 int launch_dedup_probe(const int64_t* idx, int n, int32_t* uniq, int32_t* inv, int32_t* n_uniq, void* stream);
 int launch_hot_probe(const int32_t* keys, const uint16_t* slots, int hash_log2, const int64_t* idx, int n,

@@ -85,27 +85,38 @@ __device__ __forceinline__ void acc_zero(Acc<F16>& a) {
   for (int i = 0; i < (F16 ? 8 : 4); ++i) a.v[i] = 0.0f;
 }
 
-__device__ __forceinline__ void acc_add(Acc<false>& a, const uint4 r) {
-  a.v[0] += __uint_as_float(r.x);
-  a.v[1] += __uint_as_float(r.y);
-  a.v[2] += __uint_as_float(r.z);
-  a.v[3] += __uint_as_float(r.w);
+// A row is added as x * wt + acc, one rounding per element: wt is the lookup's weight, or
+// 1 at run time (opaque to the compiler) without weights, where the product is exact and
+// the result is the plain sum bit for bit.  fp16 halves take one mixed-precision
+// instruction each (no separate widening).
+__device__ __forceinline__ void acc_add(Acc<false>& a, const uint4 r, float wt) {
+  a.v[0] = __builtin_fmaf(__uint_as_float(r.x), wt, a.v[0]);
+  a.v[1] = __builtin_fmaf(__uint_as_float(r.y), wt, a.v[1]);
+  a.v[2] = __builtin_fmaf(__uint_as_float(r.z), wt, a.v[2]);
+  a.v[3] = __builtin_fmaf(__uint_as_float(r.w), wt, a.v[3]);
 }
 
-// fp16 halves added as x * one + acc with one = 1 at run time (opaque to the compiler):
-// the product is exact and the fma rounds once, so the sum is the same as widening and
-// adding, in one mixed-precision instruction per half instead of two
-__device__ __forceinline__ void acc_add(Acc<true>& a, const uint4 r, float one) {
+__device__ __forceinline__ void acc_add(Acc<true>& a, const uint4 r, float wt) {
   const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    a.v[2 * q] = __builtin_fmaf(__half2float(__ushort_as_half(static_cast<unsigned short>(w[q] & 0xffffu))), one,
+    a.v[2 * q] = __builtin_fmaf(__half2float(__ushort_as_half(static_cast<unsigned short>(w[q] & 0xffffu))), wt,
                                 a.v[2 * q]);
-    a.v[2 * q + 1] = __builtin_fmaf(__half2float(__ushort_as_half(static_cast<unsigned short>(w[q] >> 16))), one,
+    a.v[2 * q + 1] = __builtin_fmaf(__half2float(__ushort_as_half(static_cast<unsigned short>(w[q] >> 16))), wt,
                                     a.v[2 * q + 1]);
   }
 }
-__device__ __forceinline__ void acc_add(Acc<false>& a, const uint4 r, float) { acc_add(a, r); }
+
+// A mean-pooled bag: its sum times the reciprocal of its length (bags of 0 or 1 lookups
+// are left as they are).
+template <bool F16>
+__device__ __forceinline__ void acc_mean(Acc<F16>& a, int64_t len) {
+  if (len > 1) {
+    const float s = 1.0f / static_cast<float>(len);
+#pragma unroll
+    for (int i = 0; i < (F16 ? 8 : 4); ++i) a.v[i] *= s;
+  }
+}
 
 template <bool F16>
 __device__ __forceinline__ void acc_add_f32(Acc<F16>& a, GMEM const float* p) {
@@ -169,6 +180,7 @@ struct Seg {
   GMEM const int64_t* off;   // the table's CSR offsets
   GMEM float* ob;            // out + table * E (or a chunk's partial-sum slab)
   int bs, be;
+  bool mean;                 // average each bag (never for a chunk's partial sums)
 };
 
 struct RowBase {
@@ -181,6 +193,7 @@ struct RowBase {
   GMEM unsigned long long* err;
   gchar* zero;            // R zero bytes (+ lane_c): what an invalid id (or a position past the end) reads
   float one;              // 1.0f from the launch arguments (see acc_add)
+  GMEM const float* wts;  // per-lookup weights (weighted launches)
   __device__ __forceinline__ void bad() const {
     if (count) atomicAdd(err, 1ull);
   }
@@ -289,16 +302,20 @@ struct FDedup : RowBase {
 // the end read `safe` (a valid position) and are marked invalid; validity is applied
 // when the ids are resolved.  Each lane checks its own ids against the table (an
 // invalid id is counted once, by the lane that loaded it), then the SW broadcasts the
-// validated 32-bit ids with shuffles.
-template <int G>
+// validated 32-bit ids with shuffles.  With W, each position's weight is loaded with
+// its id (weight 0 for a position past the end or an invalid id, so that it adds
+// nothing whatever the weight).
+template <int G, bool W = false>
 struct Ids {
   static constexpr int IPL = G >= kU ? 1 : kU / G;
   int64_t raw[IPL];
+  float wr[W ? IPL : 1];
   uint32_t ok_bits;
 
   // positions first + stride * u for u < kU, below end
   __device__ __forceinline__ void load(GMEM const int64_t* __restrict__ indices, int64_t first, int64_t stride,
-                                       int64_t end, int64_t safe, int lane_sw) {
+                                       int64_t end, int64_t safe, int lane_sw,
+                                       GMEM const float* __restrict__ wts = nullptr) {
     ok_bits = 0;
 #pragma unroll
     for (int j = 0; j < IPL; ++j) {
@@ -306,6 +323,7 @@ struct Ids {
       const int64_t pos = first + stride * u;
       const bool ok = u < kU && pos < end;
       raw[j] = indices[ok ? pos : safe];
+      if constexpr (W) wr[j] = wts[ok ? pos : safe];
       ok_bits |= (ok ? 1u : 0u) << j;
     }
   }
@@ -348,6 +366,24 @@ struct Ids {
       a[u] = reinterpret_cast<gchar*>(v) + f.lane_c;
     }
   }
+
+  // the weight of each of the kU lookups (the run-time 1 without weights)
+  __device__ __forceinline__ void weights(const RowBase& f, float (&wt)[kU]) const {
+    if constexpr (!W) {
+#pragma unroll
+      for (int u = 0; u < kU; ++u) wt[u] = f.one;
+    } else {
+      float mine[IPL];
+#pragma unroll
+      for (int j = 0; j < IPL; ++j) {
+        const bool in_range = (ok_bits >> j) & 1u;
+        const bool ok = static_cast<uint64_t>(raw[j]) < f.rows;
+        mine[j] = in_range && ok ? wr[j] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) wt[u] = G == 1 ? mine[u] : __shfl(mine[u / G], u % G, G);
+    }
+  }
 };
 
 // ---------------------------------------------------------------- SW mode
@@ -380,7 +416,7 @@ struct OneSeg {   // a segment source with a single segment
 // offsets window ahead, then wait once and add the rows (storing each bag as it ends).
 // The lanes of the SW hold the ends of 2G bags; the offsets of the next segment are
 // loaded while the current one is walked.
-template <int G, bool F16, class F, class Src>
+template <int G, bool F16, bool W, class F, class Src>
 __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indices, int64_t ostride, int lane_sw,
                                          F& f, Src& src) {
   constexpr int NA = F16 ? 8 : 4;
@@ -394,12 +430,14 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
     f.bind(cur);
     GMEM const int64_t* const off = cur.off;
     const int be = cur.be;
+    const bool mean = cur.mean;
     wait_all();
     const int64_t pend = cs.pend;
     int64_t p = cs.p;
-    Ids<G> ids;
+    int64_t bstart = p;   // where bag b starts
+    Ids<G, W> ids;
     ids.ok_bits = 0;
-    if (p < pend) ids.load(indices, p, 1, pend, p, lane_sw);
+    if (p < pend) ids.load(indices, p, 1, pend, p, lane_sw, f.wts);
     int wb = cur.bs, b = cur.bs;
     int64_t win = cs.win, win2 = cs.win_next;
     wait_all();
@@ -417,13 +455,15 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
       const int n = static_cast<int>(min64(kU, pend - p));
       int32_t ix[kU];
       ids.resolve(f, lane_sw, ix);
+      float wt[kU];
+      ids.weights(f, wt);
       int32_t sl[kU];
       f.probe(ix, p, n, sl);
       typename F::Raw raw[kU];
 #pragma unroll
       for (int u = 0; u < kU; ++u) f.issue(ix[u], sl[u], raw[u]);
       const int64_t pn = p + n;
-      ids.load(indices, pn, 1, pend, p, lane_sw);
+      ids.load(indices, pn, 1, pend, p, lane_sw, f.wts);
       win2 = off[min(wb + G + 1 + lane_sw, be)];
       // the current bag ends before the step's lookup u = rel (rel > kU: not in this step)
       int rel = static_cast<int>(min64(bag_end - p, kU + 1));
@@ -432,13 +472,15 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
       for (int u = 0; u < kU; ++u) {
         if (u < n) {
           while (u == rel) {
+            if (mean) acc_mean(acc, bag_end - bstart);
+            bstart = bag_end;
             if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
             acc_zero(acc);
             ++b;
             bag_end = end_of(b);
             rel = static_cast<int>(min64(bag_end - p, kU + 1));
           }
-          acc_add(acc, f.take(ix[u], sl[u], raw[u]), f.one);
+          acc_add(acc, f.take(ix[u], sl[u], raw[u]), wt[u]);
         }
       }
       if (b - wb >= G) {
@@ -452,7 +494,9 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
       }
       p = pn;
     }
-    for (; b < be; ++b) {
+    for (; b < be; ++b) {   // the bags left end at pend (the first one holds acc)
+      if (mean) acc_mean(acc, pend - bstart);
+      bstart = pend;
       if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
       acc_zero(acc);
     }
@@ -465,10 +509,10 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
 }
 
 // SW mode over one range of bags of one table
-template <int G, bool F16, class F>
+template <int G, bool F16, bool W, class F>
 __device__ __forceinline__ void walk(GMEM const int64_t* __restrict__ indices, GMEM const int64_t* __restrict__ off,
                                      int bs, int be, GMEM float* __restrict__ obase, int64_t ostride, int lane_sw,
-                                     F& f) {
+                                     bool mean, F& f) {
   if (bs >= be) return;
   OneSeg src;
   src.s.w = f.w;
@@ -477,8 +521,9 @@ __device__ __forceinline__ void walk(GMEM const int64_t* __restrict__ indices, G
   src.s.ob = obase;
   src.s.bs = bs;
   src.s.be = be;
+  src.s.mean = mean;
   src.done = false;
-  walk_seq<G, F16>(indices, ostride, lane_sw, f, src);
+  walk_seq<G, F16, W>(indices, ostride, lane_sw, f, src);
 }
 
 // ---------------------------------------------------------------- wave mode
@@ -495,11 +540,11 @@ __device__ __forceinline__ int64_t lane_i64(int64_t v, int lane) {
 // wavefront holds the ends of 64 bags in its lanes (the next 64 prefetched every
 // step), and each step issues the next step's index loads (possibly of the next bag)
 // before it waits once and sums its rows.
-template <int G, bool F16, class F>
+template <int G, bool F16, bool W, class F>
 __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indices,
                                           GMEM const int64_t* __restrict__ off, int bs, int be,
                                           GMEM float* __restrict__ obase, int64_t ostride, int lane_sw, int sw_w,
-                                          F& f) {
+                                          bool mean, F& f) {
   static_assert(!F::kPositional, "wave mode needs a position-free row source");
   constexpr int S = kWave / G;
   constexpr int NA = F16 ? 8 : 4;
@@ -527,14 +572,17 @@ __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indic
   int b = bs;
   int64_t qb = off_of(b);
   int64_t p1 = off_of(b + 1);
-  Ids<G> ids;
-  ids.load(indices, qb + sw_w, S, p1, safe, lane_sw);
+  int64_t bstart = qb;   // where bag b starts
+  Ids<G, W> ids;
+  ids.load(indices, qb + sw_w, S, p1, safe, lane_sw, f.wts);
   wait_all();
   Acc<F16> acc;
   acc_zero(acc);
   while (b < be) {
     int32_t ix[kU];
     ids.resolve(f, lane_sw, ix);
+    float wt[kU];
+    ids.weights(f, wt);
     const int n = qb + sw_w < p1 ? static_cast<int>(min64(kU, (p1 - qb - sw_w + S - 1) / S)) : 0;
     int32_t sl[kU];
     f.probe(ix, qb + sw_w, n, sl);
@@ -551,15 +599,17 @@ __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indic
     }
     const int64_t qbn = lastq ? (bn < be ? off_of(bn) : p1) : qb + S * kU;
     const int64_t p1n = lastq ? (bn < be ? off_of(bn + 1) : p1) : p1;
-    ids.load(indices, qbn + sw_w, S, p1n, safe, lane_sw);
+    ids.load(indices, qbn + sw_w, S, p1n, safe, lane_sw, f.wts);
     wait_all();   // the one wait of the step
 #pragma unroll
     for (int u = 0; u < kU; ++u)
-      if (u < n) acc_add(acc, f.take(ix[u], sl[u], raw[u]), f.one);
+      if (u < n) acc_add(acc, f.take(ix[u], sl[u], raw[u]), wt[u]);
     if (lastq) {
       acc_wave_reduce<G>(acc);
+      if (mean) acc_mean(acc, p1 - bstart);
       if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
       acc_zero(acc);
+      bstart = qbn;
     }
     b = bn;
     qb = qbn;
@@ -733,6 +783,7 @@ __device__ __forceinline__ RowBase row_base(const LookupArgs& a, const DevTable&
   rb.err = as_global(a.err);
   rb.zero = as_global(static_cast<const char*>(a.zero_row));
   rb.one = a.one;
+  rb.wts = as_global(a.weights);
   return rb;
 }
 
@@ -744,21 +795,21 @@ __device__ __forceinline__ void split_bags(int bs, int be, int i, int n, int* lo
 }
 
 // a staged slice's bags, by SW (SW mode) or by wavefront (wave mode)
-template <int G, bool F16, class F>
+template <int G, bool F16, bool W, class F>
 __device__ __forceinline__ void run_slice(const LookupArgs& a, const DevItem& it, const Lane& l, int bs, int be,
-                                          GMEM float* ob, int64_t ost, F& f) {
+                                          GMEM float* ob, int64_t ost, bool mean, F& f) {
   GMEM const int64_t* idx = as_global(a.indices);
   GMEM const int64_t* off = as_global(a.offsets) + static_cast<int64_t>(it.table) * a.B;
   int lo, hi;
   if constexpr (!F::kPositional) {
     if (it.mode == 1) {
       split_bags(bs, be, l.wave, kNumWaves, &lo, &hi);
-      walk_wave<G, F16>(idx, off, lo, hi, ob, ost, l.lane_sw, l.sw_w, f);
+      walk_wave<G, F16, W>(idx, off, lo, hi, ob, ost, l.lane_sw, l.sw_w, mean, f);
       return;
     }
   }
   split_bags(bs, be, l.sw, kBlock / G, &lo, &hi);
-  walk<G, F16>(idx, off, lo, hi, ob, ost, l.lane_sw, f);
+  walk<G, F16, W>(idx, off, lo, hi, ob, ost, l.lane_sw, mean, f);
 }
 
 template <int G, bool F16>
@@ -771,18 +822,20 @@ __device__ __forceinline__ void combine_chunks(const LookupArgs& a, const DevIte
   const int64_t slab = static_cast<int64_t>(a.Bmax) * a.E;
   GMEM const float* part = as_global(a.partials) + tb.part_base + l.lane_sw * NA;
   GMEM float* out = as_global(a.out) + static_cast<int64_t>(it.table) * a.E + l.lane_sw * NA;
+  GMEM const int64_t* off = as_global(a.offsets) + static_cast<int64_t>(it.table) * a.B;
   for (int b = lo; b < hi; ++b) {
     Acc<F16> acc;
     acc_zero(acc);
     GMEM const float* p = part + static_cast<int64_t>(b) * a.E;
     for (int c = 0; c < it.nchunks; ++c) acc_add_f32(acc, p + c * slab);
+    if (it.mean) acc_mean(acc, off[b + 1] - off[b]);
     acc_store(out + static_cast<int64_t>(b) * a.T * a.E, acc);
   }
 }
 
 // LDS slice: the table (or row chunk [r0, r1)) staged into LDS.  A chunk writes
 // partial sums; the last chunk worker of the batch slice sums them in chunk order.
-template <int G, bool F16>
+template <int G, bool F16, bool W>
 __device__ __attribute__((noinline)) void lds_item(const LookupArgs& a, const DevItem& it, int bs, int be,
                                                    lchar* smem, LMEM int* s_last) {
   const Lane l = lane_of<G>(a.R);
@@ -796,12 +849,14 @@ __device__ __attribute__((noinline)) void lds_item(const LookupArgs& a, const De
   f.r1 = static_cast<int32_t>(it.r1);
   f.count = it.chunk == 0;
   if (it.nchunks == 1) {
-    run_slice<G, F16>(a, it, l, bs, be, as_global(a.out) + static_cast<int64_t>(it.table) * a.E,
-                      static_cast<int64_t>(a.T) * a.E, f);
+    run_slice<G, F16, W>(a, it, l, bs, be, as_global(a.out) + static_cast<int64_t>(it.table) * a.E,
+                         static_cast<int64_t>(a.T) * a.E, it.mean != 0, f);
     return;
   }
-  run_slice<G, F16>(a, it, l, bs, be,
-                    as_global(a.partials) + tb.part_base + static_cast<int64_t>(it.chunk) * a.Bmax * a.E, a.E, f);
+  // a chunk's partial sums are never averaged: the combine divides the total
+  run_slice<G, F16, W>(a, it, l, bs, be,
+                       as_global(a.partials) + tb.part_base + static_cast<int64_t>(it.chunk) * a.Bmax * a.E, a.E,
+                       false, f);
   __threadfence();
   __syncthreads();
   if (l.tid == 0) *s_last = atomicAdd(as_global(a.counters) + it.counter, 1) == it.nchunks - 1;
@@ -814,7 +869,7 @@ __device__ __attribute__((noinline)) void lds_item(const LookupArgs& a, const De
 }
 
 // HOT slice: the C hottest rows and their id hash staged into LDS
-template <int G, bool F16>
+template <int G, bool F16, bool W>
 __device__ __attribute__((noinline)) void hot_item(const LookupArgs& a, const DevItem& it, int bs, int be,
                                                    lchar* smem) {
   const Lane l = lane_of<G>(a.R);
@@ -837,22 +892,22 @@ __device__ __attribute__((noinline)) void hot_item(const LookupArgs& a, const De
   f.keys = hk;
   f.slots = hs;
   f.hb = it.hash_log2;
-  run_slice<G, F16>(a, it, l, bs, be, as_global(a.out) + static_cast<int64_t>(it.table) * a.E,
-                    static_cast<int64_t>(a.T) * a.E, f);
+  run_slice<G, F16, W>(a, it, l, bs, be, as_global(a.out) + static_cast<int64_t>(it.table) * a.E,
+                       static_cast<int64_t>(a.T) * a.E, it.mean != 0, f);
 }
 
 // one bag gathered straight from HBM by one SW
-template <int G, bool F16>
+template <int G, bool F16, bool W>
 __device__ __attribute__((noinline)) void gather_one_bag(const LookupArgs& a, const RowBase& rb,
                                                          GMEM const int64_t* off, int b, GMEM float* ob, int64_t ost,
-                                                         int lane_sw) {
+                                                         int lane_sw, bool mean) {
   FGather fg;
   static_cast<RowBase&>(fg) = rb;
-  walk<G, F16>(as_global(a.indices), off, b, b + 1, ob, ost, lane_sw, fg);
+  walk<G, F16, W>(as_global(a.indices), off, b, b + 1, ob, ost, lane_sw, mean, fg);
 }
 
 // DEDUP slice: tiles of whole bags holding at most kTile lookups
-template <int G, bool F16>
+template <int G, bool F16, bool W>
 __device__ __attribute__((noinline)) void dedup_item(const LookupArgs& a, const DevItem& it, int bs, int be,
                                                      lchar* smem) {
   const Lane l = lane_of<G>(a.R);
@@ -878,7 +933,8 @@ __device__ __attribute__((noinline)) void dedup_item(const LookupArgs& a, const 
     const int64_t n64 = cnt > 0 ? off[bnext] - P0 : -1;
     if (cnt == 0 || n64 < 0 || n64 > kTile) {
       // a bag longer than a tile (or malformed offsets): gathered directly
-      if (l.sw == 0) gather_one_bag<G, F16>(a, static_cast<const RowBase&>(f), off, bcur, ob, ost, l.lane_sw);
+      if (l.sw == 0)
+        gather_one_bag<G, F16, W>(a, static_cast<const RowBase&>(f), off, bcur, ob, ost, l.lane_sw, it.mean != 0);
       bcur += 1;
       continue;
     }
@@ -889,7 +945,7 @@ __device__ __attribute__((noinline)) void dedup_item(const LookupArgs& a, const 
     f.P0 = P0;
     int lo, hi;
     split_bags(bcur, bnext, l.sw, kBlock / G, &lo, &hi);
-    walk<G, F16>(idx, off, lo, hi, ob, ost, l.lane_sw, f);
+    walk<G, F16, W>(idx, off, lo, hi, ob, ost, l.lane_sw, it.mean != 0, f);
     __syncthreads();   // LDS is rewritten by the next tile
     bcur = bnext;
   }
@@ -976,7 +1032,7 @@ __device__ __forceinline__ int sw_count(bool flag, int lane_sw) {
 // in which a bag ends empty, or whose bag ends run past the G-bag window, takes a
 // slower path that reads each bag's end as it gets there (the whole wavefront takes
 // it if one of its SWs needs it).
-template <int G, bool F16>
+template <int G, bool F16, bool W>
 __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ indices,
                                             GMEM const int64_t* __restrict__ offsets, GMEM float* __restrict__ out,
                                             int E, int B, int64_t ostride, int lane_sw, FGather& f, RunQueue& q) {
@@ -998,6 +1054,8 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
   GMEM float* obb;   // bag b's output (this lane's part)
   int be, b;
   int64_t p, pend, win;
+  int64_t bstart;    // where bag b starts
+  bool mean;
   Acc<F16> acc;
   acc_zero(acc);
   auto open = [&]() {   // make cur (head h0) the current segment
@@ -1005,12 +1063,14 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     f.w = as_global(static_cast<const char*>(g.w));
     f.rows = static_cast<uint64_t>(g.rows);
     off = offsets + static_cast<int64_t>(g.table) * B;
+    mean = g.mean != 0;
     be = cur.be;
     b = cur.bs;
     obb = out + static_cast<int64_t>(g.table) * E + lane_sw * NA + static_cast<int64_t>(b) * ostride;
     p = h0.p;
     pend = h0.pend;
     win = h0.win;
+    bstart = p;
   };
   // The head of segment s2 is loaded with the next step's loads (h2_due), so that the
   // step's single wait covers it and the loop's entry never waits on a load (a wait
@@ -1030,8 +1090,10 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     has2 = has1 && q.next(s2);
     h2_due = has2;
   };
-  auto flush = [&]() {   // the bags left in the segment end here (the last one holds acc)
+  auto flush = [&]() {   // the bags left in the segment end at pend (the first one holds acc)
     for (; b < be; ++b, obb += ostride) {
+      if (mean) acc_mean(acc, pend - bstart);
+      bstart = pend;
       if (f.active) acc_store(obb, acc);
       acc_zero(acc);
     }
@@ -1044,8 +1106,8 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     if (!has1) return;
     advance();
   }
-  Ids<G> ids;
-  ids.load(indices, p, 1, pend, p, lane_sw);
+  Ids<G, W> ids;
+  ids.load(indices, p, 1, pend, p, lane_sw, f.wts);
   wait_all();
   while (true) {
     const int n = static_cast<int>(min64(kU, pend - p));
@@ -1059,6 +1121,8 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     const bool fast = !__any(__popc(fm) != sw_count<G>(here, lane_sw) || (here && lane_sw == G - 1));
     gchar* ra[kU];
     ids.resolve_addr(f, lane_sw, ra);
+    float wt[kU];
+    ids.weights(f, wt);
     uint4 raw[kU];
 #pragma unroll
     for (int u = 0; u < kU; ++u) raw[u] = ldg16(ra[u]);
@@ -1066,9 +1130,9 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     const bool seg_end = pn >= pend;
     // the next step's ids: more of this segment, or the start of the next one
     if (!seg_end)
-      ids.load(indices, pn, 1, pend, p, lane_sw);
+      ids.load(indices, pn, 1, pend, p, lane_sw, f.wts);
     else if (has1)
-      ids.load(indices, h1.p, 1, h1.pend, h1.p, lane_sw);
+      ids.load(indices, h1.p, 1, h1.pend, h1.p, lane_sw, f.wts);
     if (h2_due) {
       h2.issue(off_of(s2), s2, lane_sw);
       h2_due = false;
@@ -1083,11 +1147,13 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
 #pragma unroll
       for (int u = 0; u < kU; ++u) {   // lookups past the end read the zero row
         if ((fs >> u) & 1u) {
+          if (mean) acc_mean(acc, p + u - bstart);
+          bstart = p + u;
           acc_store(obb, acc);
           acc_zero(acc);
           obb += ostride;
         }
-        acc_add(acc, raw[u], f.one);
+        acc_add(acc, raw[u], wt[u]);
       }
       b += m;
     } else {
@@ -1096,13 +1162,15 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         while (u < n && e == p + u) {
+          if (mean) acc_mean(acc, e - bstart);
+          bstart = e;
           if (f.active) acc_store(obb, acc);
           acc_zero(acc);
           ++b;
           obb += ostride;
           e = off[min(b + 1, be)];
         }
-        acc_add(acc, raw[u], f.one);
+        acc_add(acc, raw[u], wt[u]);
       }
       win = off[min(b + 1 + lane_sw, be)];
       wait_all();
@@ -1121,7 +1189,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
         if (!has1) return;
       }
       if (reload) {
-        ids.load(indices, p, 1, pend, p, lane_sw);
+        ids.load(indices, p, 1, pend, p, lane_sw, f.wts);
         wait_all();
       }
     }
@@ -1160,19 +1228,30 @@ struct SingleHead {   // where each bag of a chunk starts and ends (slot j: bag 
   }
 };
 
-template <int G>
-struct SingleIds {
+template <int G, bool W>
+struct SingleIds {   // each bag's first id (and, with W, its weight)
   static constexpr int IPL = SingleHead<G>::IPL;
   int64_t raw[IPL];
-  __device__ __forceinline__ void load(GMEM const int64_t* __restrict__ indices, const SingleHead<G>& h) {
+  float wr[W ? IPL : 1];
+  __device__ __forceinline__ void load(GMEM const int64_t* __restrict__ indices, GMEM const float* __restrict__ wts,
+                                       const SingleHead<G>& h) {
 #pragma unroll
-    for (int j = 0; j < IPL; ++j) raw[j] = h.en[j] > h.st[j] ? indices[h.st[j]] : int64_t(0);
+    for (int j = 0; j < IPL; ++j) {
+      raw[j] = h.en[j] > h.st[j] ? indices[h.st[j]] : int64_t(0);
+      if constexpr (W) wr[j] = h.en[j] > h.st[j] ? wts[h.st[j]] : 0.0f;
+    }
   }
 };
 
-template <int G, bool F16>
-__device__ __forceinline__ void store_row(GMEM float* p, const uint4 r) {
-  if constexpr (F16) {
+// a bag of one lookup: its row (times its weight with W) is the bag's output
+template <int G, bool F16, bool W>
+__device__ __forceinline__ void store_row(GMEM float* p, const uint4 r, float wt) {
+  if constexpr (W) {
+    Acc<F16> a;
+    acc_zero(a);
+    acc_add(a, r, wt);
+    acc_store(p, a);
+  } else if constexpr (F16) {
     Acc<true> a;
     const uint32_t w[4] = {r.x, r.y, r.z, r.w};
 #pragma unroll
@@ -1186,7 +1265,7 @@ __device__ __forceinline__ void store_row(GMEM float* p, const uint4 r) {
   }
 }
 
-template <int G, bool F16>
+template <int G, bool F16, bool W>
 __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ indices,
                                             GMEM const int64_t* __restrict__ offsets, GMEM float* __restrict__ out,
                                             int E, int B, int64_t ostride, int lane_sw, FGather& f, RunQueue& q) {
@@ -1198,22 +1277,24 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
   SegRef cur, nxt, nn;
   if (!q.next(cur)) return;
   SingleHead<G> h0, h1, h2;
-  SingleIds<G> i0, i1;
+  SingleIds<G, W> i0, i1;
   h0.issue(off_of(cur), cur, lane_sw);
   bool has1 = q.next(nxt);
   if (has1) h1.issue(off_of(nxt), nxt, lane_sw);
   wait_all();
-  i0.load(indices, h0);
+  i0.load(indices, f.wts, h0);
   bool has2 = has1 && q.next(nn);
   if (has2) h2.issue(off_of(nn), nn, lane_sw);
-  if (has1) i1.load(indices, h1);
+  if (has1) i1.load(indices, f.wts, h1);
   while (true) {
     // ---- chunk cur: head h0 and ids i0 have landed (or are in flight)
     const LMEM GatherRun& g = q.r[cur.e];
     f.w = as_global(static_cast<const char*>(g.w));
     f.rows = static_cast<uint64_t>(g.rows);
     GMEM float* const ob = out + static_cast<int64_t>(g.table) * E + lane_sw * NA;
+    const bool mean = g.mean != 0;
     int64_t addr[IPL];
+    float wm[IPL];
     bool multi = false;
 #pragma unroll
     for (int j = 0; j < IPL; ++j) {
@@ -1221,6 +1302,7 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
       const bool ok = static_cast<uint64_t>(i0.raw[j]) < f.rows;
       if (has && !ok) f.bad();
       addr[j] = reinterpret_cast<int64_t>(has && ok ? f.w + i0.raw[j] * f.R : f.zero);
+      wm[j] = W && has && ok ? i0.wr[W ? j : 0] : 0.0f;
       multi = multi || h0.en[j] - h0.st[j] > 1;
     }
     uint4 raw[kU];
@@ -1229,11 +1311,14 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
       const int64_t a = G == 1 ? addr[u] : lane_i64_sw(addr[u / G], u % G, G);
       raw[u] = ldg16(reinterpret_cast<gchar*>(a) + f.lane_c);
     }
+    float wt[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) wt[u] = !W ? 0.0f : G == 1 ? wm[u] : __shfl(wm[u / G], u % G, G);
     wait_all();   // the one wait of the step
     const int nb = cur.be - cur.bs;
 #pragma unroll
     for (int u = 0; u < kU; ++u)
-      if (u < nb && f.active) store_row<G, F16>(ob + static_cast<int64_t>(cur.bs + u) * ostride, raw[u]);
+      if (u < nb && f.active) store_row<G, F16, W>(ob + static_cast<int64_t>(cur.bs + u) * ostride, raw[u], wt[u]);
     if (__ballot(multi) != 0) {   // bags of more than one lookup: sum them again in lookup order
 #pragma unroll 1
       for (int u = 0; u < kU; ++u) {
@@ -1246,8 +1331,10 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
             const int64_t x = indices[k];
             const bool ok = static_cast<uint64_t>(x) < f.rows;
             if (!ok && lane_sw == 0 && k > s0) f.bad();   // the first id was counted with the chunk
-            acc_add(acc, ldg16(ok ? f.w + x * f.R + f.lane_c : f.zero + f.lane_c), f.one);
+            const float wk = W ? (ok ? f.wts[k] : 0.0f) : f.one;
+            acc_add(acc, ldg16(ok ? f.w + x * f.R + f.lane_c : f.zero + f.lane_c), wk);
           }
+          if (mean) acc_mean(acc, e0 - s0);
           if (f.active) acc_store(ob + static_cast<int64_t>(cur.bs + u) * ostride, acc);
         }
       }
@@ -1261,7 +1348,7 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
     has1 = has2;
     has2 = has1 && q.next(nn);
     if (has2) h2.issue(off_of(nn), nn, lane_sw);
-    if (has1) i1.load(indices, h1);
+    if (has1) i1.load(indices, f.wts, h1);
   }
 }
 
@@ -1273,7 +1360,7 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
 // even when per-lookup cost differs between tables (cache-resident vs HBM-bound).  The
 // worker's runs are first copied into LDS (`lds`), so that finding a chunk's table and
 // bags costs no memory round trip.
-template <int G, bool F16>
+template <int G, bool F16, bool W>
 __device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, const Lane& l, int wg) {
   constexpr int NSW = kBlock / G;
   {   // the worker's slot: a header record, then its runs
@@ -1303,26 +1390,27 @@ __device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, co
       const LMEM GatherRun& g = runs[s.e];
       f.w = as_global(static_cast<const char*>(g.w));
       f.rows = static_cast<uint64_t>(g.rows);
-      walk_wave<G, F16>(idx, offsets + static_cast<int64_t>(g.table) * a.B, s.bs, s.be,
-                        out + static_cast<int64_t>(g.table) * a.E, ost, l.lane_sw, l.sw_w, f);
+      walk_wave<G, F16, W>(idx, offsets + static_cast<int64_t>(g.table) * a.B, s.bs, s.be,
+                           out + static_cast<int64_t>(g.table) * a.E, ost, l.lane_sw, l.sw_w, g.mean != 0, f);
     }
   }
   {  // single-lookup bags
     RunQueue q{runs, n_wave, n_wave + n_single, l.sw, NSW, single_chunks, a.B};
     FGather f;
     static_cast<RowBase&>(f) = rb0;
-    walk_single<G, F16>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
+    walk_single<G, F16, W>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
   }
   {  // SW mode
     RunQueue q{runs, n_wave + n_single, nr, l.sw, NSW, sw_chunks, a.B};
     FGather f;
     static_cast<RowBase&>(f) = rb0;
-    walk_stream<G, F16>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
+    walk_stream<G, F16, W>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
   }
 }
 
 // STAGED = false: the plan has gather slices only (no LDS, no staged-slice code).
-template <int G, bool F16, bool STAGED>
+// W: every lookup carries a weight (a.weights).
+template <int G, bool F16, bool STAGED, bool W>
 __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
   extern __shared__ __align__(16) char smem_raw[];
   __shared__ int s_last;
@@ -1346,11 +1434,11 @@ __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
       __syncthreads();   // the previous slice is done with LDS
       if (ti && l.tid == 0) ti[2 * i] = now_ticks();
       if (it.strat == 0)
-        lds_item<G, F16>(a, it, bs, be, smem, (LMEM int*)&s_last);
+        lds_item<G, F16, W>(a, it, bs, be, smem, (LMEM int*)&s_last);
       else if (it.strat == 1)
-        hot_item<G, F16>(a, it, bs, be, smem);
+        hot_item<G, F16, W>(a, it, bs, be, smem);
       else
-        dedup_item<G, F16>(a, it, bs, be, smem);
+        dedup_item<G, F16, W>(a, it, bs, be, smem);
       if (ti) {
         __syncthreads();
         if (l.tid == 0) ti[2 * i + 1] = now_ticks();
@@ -1359,7 +1447,7 @@ __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
   }
   if (tw && l.tid == 0) tw[1] = now_ticks();
   __syncthreads();   // staged slices are done with LDS
-  gather_phase<G, F16>(a, (lchar*)smem_raw, l, wg);
+  gather_phase<G, F16, W>(a, (lchar*)smem_raw, l, wg);
   if (tw && (l.tid & (kWave - 1)) == 0) tw[2 + l.wave] = now_ticks();
 }
 
@@ -1452,31 +1540,36 @@ __global__ void __launch_bounds__(256) fill_kernel(char* dst, int64_t row_begin,
 
 using KernelFn = void (*)(LookupArgs);
 
-template <bool F16, bool STAGED>
+template <bool F16, bool STAGED, bool W>
 KernelFn pick(int G) {
   switch (G) {
-    case 1: return &lookup_kernel<1, F16, STAGED>;
-    case 2: return &lookup_kernel<2, F16, STAGED>;
-    case 4: return &lookup_kernel<4, F16, STAGED>;
-    case 8: return &lookup_kernel<8, F16, STAGED>;
-    case 16: return &lookup_kernel<16, F16, STAGED>;
-    case 32: return &lookup_kernel<32, F16, STAGED>;
-    case 64: return &lookup_kernel<64, F16, STAGED>;
+    case 1: return &lookup_kernel<1, F16, STAGED, W>;
+    case 2: return &lookup_kernel<2, F16, STAGED, W>;
+    case 4: return &lookup_kernel<4, F16, STAGED, W>;
+    case 8: return &lookup_kernel<8, F16, STAGED, W>;
+    case 16: return &lookup_kernel<16, F16, STAGED, W>;
+    case 32: return &lookup_kernel<32, F16, STAGED, W>;
+    case 64: return &lookup_kernel<64, F16, STAGED, W>;
     default: return nullptr;
   }
 }
 
-KernelFn pick_any(int G, bool f16, bool staged) {
-  if (f16) return staged ? pick<true, true>(G) : pick<true, false>(G);
-  return staged ? pick<false, true>(G) : pick<false, false>(G);
+template <bool W>
+KernelFn pick_w(int G, bool f16, bool staged) {
+  if (f16) return staged ? pick<true, true, W>(G) : pick<true, false, W>(G);
+  return staged ? pick<false, true, W>(G) : pick<false, false, W>(G);
+}
+
+KernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
+  return weighted ? pick_w<true>(G, f16, staged) : pick_w<false>(G, f16, staged);
 }
 
 }  // namespace
 
 int prepare_lookup_kernels(int lds_bytes) {
   for (int G = 1; G <= 64; G <<= 1) {
-    for (int f = 0; f < 2; ++f) {
-      KernelFn k = pick_any(G, f != 0, true);
+    for (int f = 0; f < 4; ++f) {
+      KernelFn k = pick_any(G, (f & 1) != 0, true, (f & 2) != 0);
       if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                               lds_bytes) != hipSuccess)
         return 4;
@@ -1488,8 +1581,9 @@ int prepare_lookup_kernels(int lds_bytes) {
   return 0;
 }
 
-int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, int grid, int lds_bytes, void* stream) {
-  KernelFn k = pick_any(G, f16, staged);
+int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
+                  void* stream) {
+  KernelFn k = pick_any(G, f16, staged, weighted);
   if (!k) return 2;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kBlock), lds_bytes, static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? 0 : 4;
