@@ -76,8 +76,9 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(c: W.Config, batches, budget_s: float):
-    """The CPU oracle (plain NumPy, float64 accumulation) on a bounded sample of the workload."""
+def cpu_baseline(c: W.Config, batches, budget_s: float, pooling: str = "sum", psw=None):
+    """The CPU oracle (plain NumPy, float64 accumulation) on a bounded sample of the workload
+    (with the run's pooling and, for weighted runs, the same per-lookup weights)."""
     from oracle import pool as OP
     t0 = time.time()
     if c.cfg_id == 5:
@@ -95,22 +96,24 @@ def cpu_baseline(c: W.Config, batches, budget_s: float):
     for bt in batches:
         B = bt.B
         Bs = min(Bs, B)
-        parts, lens = [], []
+        parts, lens, wparts = [], [], []
         for t in keep:
             lo, hi = bt.offsets[t * B], bt.offsets[t * B + Bs]
             parts.append(bt.indices[lo:hi])
             lens.append(np.diff(bt.offsets[t * B: t * B + Bs + 1]))
+            if psw is not None:
+                wparts.append(psw[len(subs)][lo:hi])
         off = np.zeros(len(keep) * Bs + 1, np.int64)
         np.cumsum(np.concatenate(lens), out=off[1:])
-        subs.append((np.concatenate(parts), off))
+        subs.append((np.concatenate(parts), off, np.concatenate(wparts) if psw is not None else None))
     lat = []
     n_look = 0
     start = time.perf_counter()
     i = 0
     while True:
-        idx, off = subs[i % len(subs)]
+        idx, off, wk = subs[i % len(subs)]
         t1 = time.perf_counter()
-        OP.pool_reference(weights, idx, off, Bs)
+        OP.pool_reference(weights, idx, off, Bs, pooling=pooling, psw=wk)
         lat.append(time.perf_counter() - t1)
         n_look += int(off[-1])
         i += 1
@@ -169,6 +172,8 @@ def main():
     ap.add_argument("--no-copy", action="store_true")
     ap.add_argument("--lds-budget", type=int, default=0)
     ap.add_argument("--force", type=str, default="", help="force one strategy for all tables (lds|hot|dedup|gather)")
+    ap.add_argument("--pooling", choices=["sum", "mean"], default="sum", help="reduction of every table's bags")
+    ap.add_argument("--weighted", action="store_true", help="per-lookup weights (emb_lookup_weighted)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the lookup runs on a single MI355X "
@@ -199,12 +204,18 @@ def main():
         weights.append(w)
     d_idx = [torch.from_numpy(b.indices).cuda() for b in batches]
     d_off = [torch.from_numpy(b.offsets).cuda() for b in batches]
+    # weighted runs: seeded per-lookup weights, uniform in [0.5, 1.5)
+    psw = [np.random.default_rng(1000 + i).uniform(0.5, 1.5, size=b.indices.size).astype(np.float32)
+           for i, b in enumerate(batches)] if args.weighted else None
+    d_w = [torch.from_numpy(x).cuda() for x in psw] if psw is not None else None
     out = torch.empty((c.batch, c.T, c.E), dtype=torch.float32, device="cuda")
     opts = {}
     if args.lds_budget:
         opts["lds_budget"] = args.lds_budget
     if args.force:
         opts["force"] = [{"lds": 0, "hot": 1, "dedup": 2, "gather": 3}[args.force]] * c.T
+    if args.pooling != "sum":
+        opts["pooling"] = args.pooling
     tp = time.time()
     plan = embx.Plan(c.rows, c.E, c.dtype, stats, c.batch, **opts).bind(weights)
     plan_ms = (time.time() - tp) * 1e3
@@ -215,13 +226,14 @@ def main():
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
     ptrs = [(d_idx[i].data_ptr(), d_off[i].data_ptr()) for i in range(R)]
+    wptr = [d_w[i].data_ptr() if d_w is not None else 0 for i in range(R)]
     n_look = [b.n_lookups for b in batches]
     outp = out.data_ptr()
     B = c.batch
 
     for i in range(args.warmup):
         ip, op = ptrs[i % R]
-        plan.lookup_ptr(ip, op, B, outp, sp)
+        plan.lookup_ptr(ip, op, B, outp, sp, wptr[i % R])
     torch.cuda.synchronize()
     assert plan.check_errors() == 0
 
@@ -234,7 +246,7 @@ def main():
     for i in range(N):
         ip, op = ptrs[i % R]
         ev0[i].record(stream)
-        plan.lookup_ptr(ip, op, B, outp, sp)
+        plan.lookup_ptr(ip, op, B, outp, sp, wptr[i % R])
         ev1[i].record(stream)
     torch.cuda.synchronize()
     lat_ms = [ev0[i].elapsed_time(ev1[i]) for i in range(N)]
@@ -250,7 +262,7 @@ def main():
             flush.fill_(i & 0xFF)
             ip, op = ptrs[i % R]
             c0[i].record(stream)
-            plan.lookup_ptr(ip, op, B, outp, sp)
+            plan.lookup_ptr(ip, op, B, outp, sp, wptr[i % R])
             c1[i].record(stream)
         torch.cuda.synchronize()
         cl = [c0[i].elapsed_time(c1[i]) for i in range(args.cold_batches)]
@@ -268,7 +280,7 @@ def main():
     e_start.record(stream)
     for i in range(K):
         ip, op = ptrs[i % R]
-        plan.lookup_ptr(ip, op, B, outp, sp)
+        plan.lookup_ptr(ip, op, B, outp, sp, wptr[i % R])
     e_stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -277,19 +289,22 @@ def main():
     mean_ms = sum(lat_ms) / len(lat_ms)
 
     R_b = c.row_bytes
-    alg = [W.algorithmic_bytes(c, n_look[i % R])["total"] for i in range(K)]
+    # weighted runs also read 4 bytes of weight per lookup
+    alg = [W.algorithmic_bytes(c, n_look[i % R])["total"] + (4 * n_look[i % R] if args.weighted else 0)
+           for i in range(K)]
     alg_mean = sum(alg) / K
     useful_mean = sum(n_look[i % R] for i in range(K)) * R_b / K
     achieved = alg_mean / (launch_ms * 1e-3) / 1e9
     src_hash = kernel_source_hash()
     workload = f"workload{c.cfg_id}"
-    traffic = load_traffic(workload, src_hash)
+    variant = ("" if args.pooling == "sum" else f"-{args.pooling}") + ("-weighted" if args.weighted else "")
+    traffic = load_traffic(workload + variant, src_hash)
 
     copy_gbps = None if args.no_copy else copy_bandwidth_gbps()
     cpu = None
     if not args.no_cpu:
         log("timing the CPU oracle")
-        cpu = cpu_baseline(c, batches, args.cpu_seconds)
+        cpu = cpu_baseline(c, batches, args.cpu_seconds, args.pooling, psw)
 
     res = {
         "metric": METRIC,
@@ -304,9 +319,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{workload}: {c.name}", "tables": c.T, "E": c.E, "table_dtype": c.dtype,
+        "config": {"workload": f"{workload}{variant}: {c.name}", "tables": c.T, "E": c.E, "table_dtype": c.dtype,
                    "batch": c.batch, "lookups_per_batch": int(sum(n_look) / R), "resident_batches": R,
-                   "table_bytes": sum(c.rows) * R_b},
+                   "table_bytes": sum(c.rows) * R_b, "pooling": args.pooling, "weighted": bool(args.weighted)},
         "queries_per_s": B * K / wall,
         "p99_us": p99(lat_ms) * 1e3,
         "mean_us": mean_ms * 1e3,

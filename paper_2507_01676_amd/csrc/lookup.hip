@@ -369,20 +369,26 @@ struct Ids {
 
   // the weight of each of the kU lookups (the run-time 1 without weights)
   __device__ __forceinline__ void weights(const RowBase& f, float (&wt)[kU]) const {
-    if constexpr (!W) {
+    float mine[W ? IPL : 1];
+    own_weights(f, mine);
 #pragma unroll
-      for (int u = 0; u < kU; ++u) wt[u] = f.one;
-    } else {
-      float mine[IPL];
+    for (int u = 0; u < kU; ++u) wt[u] = weight_of(f, mine, u);
+  }
+  // the weights of this lane's own positions (0 past the end or for an invalid id) ...
+  __device__ __forceinline__ void own_weights(const RowBase& f, float (&mine)[W ? IPL : 1]) const {
+    if constexpr (W) {
 #pragma unroll
       for (int j = 0; j < IPL; ++j) {
         const bool in_range = (ok_bits >> j) & 1u;
         const bool ok = static_cast<uint64_t>(raw[j]) < f.rows;
         mine[j] = in_range && ok ? wr[j] : 0.0f;
       }
-#pragma unroll
-      for (int u = 0; u < kU; ++u) wt[u] = G == 1 ? mine[u] : __shfl(mine[u / G], u % G, G);
     }
+  }
+  // ... and position u's weight, shared within the SW when it is used
+  static __device__ __forceinline__ float weight_of(const RowBase& f, const float (&mine)[W ? IPL : 1], int u) {
+    if constexpr (!W) return f.one;
+    else return G == 1 ? mine[u] : __shfl(mine[u / G], u % G, G);
   }
 };
 
@@ -1121,8 +1127,8 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     const bool fast = !__any(__popc(fm) != sw_count<G>(here, lane_sw) || (here && lane_sw == G - 1));
     gchar* ra[kU];
     ids.resolve_addr(f, lane_sw, ra);
-    float wt[kU];
-    ids.weights(f, wt);
+    float wm[W ? Ids<G, W>::IPL : 1];
+    ids.own_weights(f, wm);
     uint4 raw[kU];
 #pragma unroll
     for (int u = 0; u < kU; ++u) raw[u] = ldg16(ra[u]);
@@ -1153,7 +1159,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
           acc_zero(acc);
           obb += ostride;
         }
-        acc_add(acc, raw[u], wt[u]);
+        acc_add(acc, raw[u], Ids<G, W>::weight_of(f, wm, u));
       }
       b += m;
     } else {
@@ -1170,7 +1176,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
           obb += ostride;
           e = off[min(b + 1, be)];
         }
-        acc_add(acc, raw[u], wt[u]);
+        acc_add(acc, raw[u], Ids<G, W>::weight_of(f, wm, u));
       }
       win = off[min(b + 1 + lane_sw, be)];
       wait_all();
