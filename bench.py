@@ -171,7 +171,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-copy", action="store_true")
     ap.add_argument("--lds-budget", type=int, default=0)
-    ap.add_argument("--force", type=str, default="", help="force one strategy for all tables (lds|hot|dedup|gather)")
+    ap.add_argument("--force", type=str, default="", help="force one strategy for all tables (lds|hot|dedup|gather|stream)")
     ap.add_argument("--pooling", choices=["sum", "mean"], default="sum", help="reduction of every table's bags")
     ap.add_argument("--weighted", action="store_true", help="per-lookup weights (emb_lookup_weighted)")
     args = ap.parse_args()
@@ -213,7 +213,7 @@ def main():
     if args.lds_budget:
         opts["lds_budget"] = args.lds_budget
     if args.force:
-        opts["force"] = [{"lds": 0, "hot": 1, "dedup": 2, "gather": 3}[args.force]] * c.T
+        opts["force"] = [{"lds": 0, "hot": 1, "dedup": 2, "gather": 3, "stream": 4}[args.force]] * c.T
     if args.pooling != "sum":
         opts["pooling"] = args.pooling
     tp = time.time()

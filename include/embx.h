@@ -60,13 +60,17 @@ typedef enum { EMB_POOL_SUM = 0, EMB_POOL_MEAN = 1 } emb_pooling_t;
  *             gather from HBM;
  *   DEDUP  -- each tile of indices is sorted, each distinct row fetched once into LDS, bags
  *             read their rows from there;
- *   GATHER -- one row per sub-wavefront straight from HBM with 16-byte loads (the GM flow). */
+ *   GATHER -- one row per sub-wavefront straight from HBM with 16-byte loads (the GM flow);
+ *   STREAM -- the whole table moves through LDS in chunks of floor(L / R) rows on one worker,
+ *             each chunk serving the slice's lookups that fall in it (the GM-UB flow);
+ *             partial sums are added onto the output in chunk order. */
 typedef enum {
   EMB_STRAT_AUTO = -1,
   EMB_STRAT_LDS = 0,
   EMB_STRAT_HOT = 1,
   EMB_STRAT_DEDUP = 2,
-  EMB_STRAT_GATHER = 3
+  EMB_STRAT_GATHER = 3,
+  EMB_STRAT_STREAM = 4
 } emb_strategy_t;
 
 /* Cost-model coefficients (Eq. (2) extended per strategy), picoseconds.  Layout of
@@ -76,6 +80,7 @@ typedef enum {
  *   chunk   = L0 + S*(rows*R) + I*lam + L1*lam/c
  *   hot     = H0 + S*(C*R) + lam*(P + h*L1 + (1-h)*G1)
  *   dedup   = D0 + D1*lam + G1*u*lam
+ *   stream  = L0 + S*(m*R) + I*lam*c + L1*lam   (c = ceil(m / floor(L / R)), m the table rows)
  * with lam the expected lookups of the slice, R the row bytes, c the chunk count,
  * C the hot rows staged, h the fraction of lookups they catch, u the unique fraction. */
 enum {
@@ -129,7 +134,7 @@ typedef struct {
   int32_t lds_budget_bytes;
   int64_t max_load_ps, sum_load_ps;
   int32_t lif_milli, r_symmetric;
-  int32_t n_strategy[4];    /* slices per strategy                             */
+  int32_t n_strategy[5];    /* slices per strategy (emb_strategy_t order)      */
 } emb_plan_info_t;
 
 /* Builds a plan for T tables of rows[t] x E elements of `dtype`, for batches of up to

@@ -18,11 +18,15 @@ pooling factor, B batch, K cores = GPU workers, L persistent-buffer size = LDS
 budget for rows):
 
   P1  strategy choice per table at split k: minimum cost among the feasible
-      strategies in the fixed order LDS, HOT, DEDUP, GATHER (ties -> earlier).
-      LDS is feasible iff m_t R <= L; HOT iff C_t >= 1 with C_t = min(hot rows
-      listed, floor(L / R), 2048) the hot rows staged, h_t the fraction of
-      lookups they catch (summed in list order); u_t = unique fraction (1 if
-      unknown).
+      strategies in the fixed order LDS, HOT, DEDUP, GATHER, STREAM (ties ->
+      earlier).  LDS is feasible iff m_t R <= L; HOT iff C_t >= 1 with C_t =
+      min(hot rows listed, floor(L / R), 2048) the hot rows staged, h_t the
+      fraction of lookups they catch (summed in list order); u_t = unique
+      fraction (1 if unknown).  STREAM (the GM-UB flow of Sec. II-B: the table
+      moves through the buffer in chunks, each chunk serving the lookups that
+      fall in it) takes c_t = ceil(m_t / floor(L / R)) chunks on one worker; it
+      is a candidate when forced, or when c_t <= 64 and its cost stays below the
+      cost cap (a larger one is left out, not an error).
   P2  (paper step 1) a table larger than L is split into the fewest chunks of
       at most floor(min(chunk_max, L) / R) rows, but only if its best unsplit
       cost exceeds the sum of the chunk costs (the speed-up exceeds the number
@@ -61,9 +65,9 @@ from dataclasses import dataclass, field
 from typing import List, Optional, Sequence, Tuple
 
 # strategies (same numbering as the C header)
-LDS, HOT, DEDUP, GATHER = 0, 1, 2, 3
+LDS, HOT, DEDUP, GATHER, STREAM = 0, 1, 2, 3, 4
 AUTO = -1
-STRAT_ORDER = (LDS, HOT, DEDUP, GATHER)
+STRAT_ORDER = (LDS, HOT, DEDUP, GATHER, STREAM)
 
 # beta layout (picoseconds; per item, per lookup, per staged byte)
 G0, G1, L0, L1, S, I, H0, P, D0, D1 = range(10)
@@ -72,6 +76,7 @@ NBETA = 10
 MAX_HOT = 4096          # hot rows a table's statistics may list
 MAX_HOT_SLOTS = 2048    # hot rows one HOT item stages at most
 MAX_CHUNKS = 65536
+STREAM_MAX_CHUNKS = 64  # STREAM is an automatic candidate up to this many chunks
 SYM_MAX_DEFAULT = 64    # GATHER tables split over all workers while the plan has at most this many
 
 
@@ -206,6 +211,13 @@ def cost_dedup(b, u, lam):
     return _fl(b[D0] + b[D1] * lam + (b[G1] * u) * lam), _fl(b[D0])
 
 
+def cost_stream(b, m, R, lam, c):
+    """The whole table through LDS in c chunks on one worker: each chunk scans the
+    slice's lookups (I), each lookup is read from LDS once (L1)."""
+    return (_fl(b[L0] + b[S] * float(m * R) + b[I] * lam * float(c) + b[L1] * lam),
+            _fl(b[L0] + b[S] * float(m * R)))
+
+
 class _Table:
     def __init__(self, t, m, st: Stat, R, L, B, force):
         self.t, self.m, self.R = t, m, R
@@ -219,9 +231,10 @@ class _Table:
         u = float(st.unique_frac)
         self.u = u if (u > 0.0 and u <= 1.0) else 1.0
         self.fits = m * R <= L
+        self.sc = (m + L // R - 1) // (L // R)   # STREAM chunks
         self.force = force
 
-    def allowed(self):
+    def allowed(self, b, k):
         out = []
         for s in STRAT_ORDER:
             if self.force != AUTO and s != self.force:
@@ -230,8 +243,17 @@ class _Table:
                 continue
             if s == HOT and self.C < 1:
                 continue
+            if s == STREAM and self.force == AUTO and not self.stream_ok(b, k):
+                continue
             out.append(s)
         return out
+
+    def stream_ok(self, b, k):
+        if self.sc > STREAM_MAX_CHUNKS:
+            return False
+        lam = self.Lam / float(k)
+        x = b[L0] + b[S] * float(self.m * self.R) + b[I] * lam * float(self.sc) + b[L1] * lam
+        return math.isfinite(x) and x < COST_CAP
 
     def cost(self, b, strat, k):
         lam = self.Lam / float(k)
@@ -241,12 +263,14 @@ class _Table:
             return cost_hot(b, self.C, self.R, self.h, lam)
         if strat == DEDUP:
             return cost_dedup(b, self.u, lam)
+        if strat == STREAM:
+            return cost_stream(b, self.m, self.R, lam, self.sc)
         return cost_gather(b, lam)
 
     def best(self, b, k):
         """(strategy, cost, fixed cost) -- P1, ties to the earlier strategy."""
         best = None
-        for s in self.allowed():
+        for s in self.allowed(b, k):
             c, f = self.cost(b, s, k)
             if best is None or c < best[1]:
                 best = (s, c, f)
@@ -301,7 +325,7 @@ def _validate(rows, E, dtype, stats, B, K, opts: Options):
     if len(beta) != NBETA or not all(math.isfinite(x) and x >= 0.0 for x in beta):
         raise PlanError("beta")
     force = list(opts.force) if opts.force is not None else [AUTO] * T
-    if len(force) != T or any(f not in (AUTO, LDS, HOT, DEDUP, GATHER) for f in force):
+    if len(force) != T or any(f not in (AUTO, LDS, HOT, DEDUP, GATHER, STREAM) for f in force):
         raise PlanError("force_strategy")
     return T, R, L, beta, force
 

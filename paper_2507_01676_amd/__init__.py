@@ -33,7 +33,7 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_OUT_OF_MEMORY, ERR_DEVICE, ERR_NO
     ERR_INDEX_OUT_OF_RANGE, ERR_BUFFER_TOO_SMALL = range(8)
 DTYPE_F32, DTYPE_F16 = 0, 1
 STRAT_AUTO, STRAT_LDS, STRAT_HOT, STRAT_DEDUP, STRAT_GATHER = -1, 0, 1, 2, 3
-STRATEGY_NAMES = {0: "LDS", 1: "HOT", 2: "DEDUP", 3: "GATHER"}
+STRATEGY_NAMES = {0: "LDS", 1: "HOT", 2: "DEDUP", 3: "GATHER", 4: "STREAM"}
 POOL_SUM, POOL_MEAN = 0, 1
 POOLING_CODES = {"sum": POOL_SUM, "mean": POOL_MEAN}
 BETA_COUNT = 10
@@ -71,7 +71,7 @@ class _Info(ctypes.Structure):
                 ("lds_bytes", ctypes.c_int32), ("num_items", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("lds_budget_bytes", ctypes.c_int32), ("max_load_ps", ctypes.c_int64),
                 ("sum_load_ps", ctypes.c_int64), ("lif_milli", ctypes.c_int32), ("r_symmetric", ctypes.c_int32),
-                ("n_strategy", ctypes.c_int32 * 4)]
+                ("n_strategy", ctypes.c_int32 * 5)]
 
 
 _vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
@@ -293,7 +293,7 @@ class Plan:
         i = _Info()
         _check(_lib.emb_plan_get_info(self._h, ctypes.byref(i)), "emb_plan_get_info")
         d = {k: getattr(i, k) for k, _ in _Info._fields_ if k != "n_strategy"}
-        d["n_strategy"] = {STRATEGY_NAMES[s]: i.n_strategy[s] for s in range(4)}
+        d["n_strategy"] = {STRATEGY_NAMES[s]: i.n_strategy[s] for s in range(5)}
         return d
 
     def hot_probe(self, table: int, idx, stream=None):

@@ -44,7 +44,7 @@ struct emb_plan {
   int32_t gr_slot = 1;                   // records per worker slot
   GatherRun* d_gr = nullptr;
   const char* d_zero_row = nullptr;      // R zero bytes
-  bool staged = false;                   // the plan has LDS / HOT / DEDUP slices
+  bool staged = false;                   // the plan has LDS / HOT / DEDUP / STREAM slices
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
   std::vector<int32_t> mean;             // per table: 1 = mean pooling
 };
@@ -289,7 +289,10 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     const double s_t = stats[x.t].mean_pooling;
     const int sw_per_wave = 64 / p->G;
     const int64_t bags_per_slice = static_cast<int64_t>(max_batch) / x.k;
-    d.mode = (x.strat != S_DEDUP && s_t >= 4.0 * sw_per_wave && bags_per_slice <= 16 * (kBlock / 64)) ? 1 : 0;
+    // (not for DEDUP, whose row source is addressed by tile position, nor STREAM, whose
+    // bags keep their sub-wavefront from chunk to chunk)
+    d.mode = (x.strat != S_DEDUP && x.strat != S_STREAM && s_t >= 4.0 * sw_per_wave &&
+              bags_per_slice <= 16 * (kBlock / 64)) ? 1 : 0;
     items.push_back(d);
     wg_ptr[x.wg + 1] += 1;
   }

@@ -181,6 +181,7 @@ struct Seg {
   GMEM float* ob;            // out + table * E (or a chunk's partial-sum slab)
   int bs, be;
   bool mean;                 // average each bag (never for a chunk's partial sums)
+  bool add;                  // add each bag's sum to what the output already holds
 };
 
 struct RowBase {
@@ -436,7 +437,7 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
     f.bind(cur);
     GMEM const int64_t* const off = cur.off;
     const int be = cur.be;
-    const bool mean = cur.mean;
+    const bool mean = cur.mean, add = cur.add;
     wait_all();
     const int64_t pend = cs.pend;
     int64_t p = cs.p;
@@ -478,6 +479,7 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
       for (int u = 0; u < kU; ++u) {
         if (u < n) {
           while (u == rel) {
+            if (add && f.active) acc_add_f32(acc, ob + static_cast<int64_t>(b) * ostride);
             if (mean) acc_mean(acc, bag_end - bstart);
             bstart = bag_end;
             if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
@@ -501,6 +503,7 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
       p = pn;
     }
     for (; b < be; ++b) {   // the bags left end at pend (the first one holds acc)
+      if (add && f.active) acc_add_f32(acc, ob + static_cast<int64_t>(b) * ostride);
       if (mean) acc_mean(acc, pend - bstart);
       bstart = pend;
       if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
@@ -518,7 +521,7 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
 template <int G, bool F16, bool W, class F>
 __device__ __forceinline__ void walk(GMEM const int64_t* __restrict__ indices, GMEM const int64_t* __restrict__ off,
                                      int bs, int be, GMEM float* __restrict__ obase, int64_t ostride, int lane_sw,
-                                     bool mean, F& f) {
+                                     bool mean, F& f, bool add = false) {
   if (bs >= be) return;
   OneSeg src;
   src.s.w = f.w;
@@ -528,6 +531,7 @@ __device__ __forceinline__ void walk(GMEM const int64_t* __restrict__ indices, G
   src.s.bs = bs;
   src.s.be = be;
   src.s.mean = mean;
+  src.s.add = add;
   src.done = false;
   walk_seq<G, F16, W>(indices, ostride, lane_sw, f, src);
 }
@@ -871,6 +875,37 @@ __device__ __attribute__((noinline)) void lds_item(const LookupArgs& a, const De
     __threadfence();
     combine_chunks<G, F16>(a, it, tb, bs, be, l);
     if (l.tid == 0) atomicExch(as_global(a.counters) + it.counter, 0);
+  }
+}
+
+// STREAM slice: the whole table passes through LDS in chunks of floor(L / R) rows.  For
+// every chunk each SW walks its own bags (the same bags every time) and adds the rows
+// that fall in the chunk; the first chunk stores the partial sums, later chunks add
+// onto them, so a bag's sum is built in chunk order by one SW and needs no combine.
+template <int G, bool F16, bool W>
+__device__ __attribute__((noinline)) void stream_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                                      lchar* smem) {
+  const Lane l = lane_of<G>(a.R);
+  const DevTable tb = a.tables[it.table];
+  const int64_t crow = a.lds_rows / a.R;
+  GMEM const int64_t* idx = as_global(a.indices);
+  GMEM const int64_t* off = as_global(a.offsets) + static_cast<int64_t>(it.table) * a.B;
+  GMEM float* const ob = as_global(a.out) + static_cast<int64_t>(it.table) * a.E;
+  const int64_t ost = static_cast<int64_t>(a.T) * a.E;
+  int lo, hi;
+  split_bags(bs, be, l.sw, kBlock / G, &lo, &hi);
+  FLds f;
+  static_cast<RowBase&>(f) = row_base(a, tb, l);
+  f.lds = smem;
+  for (int64_t r0 = 0; r0 < tb.rows; r0 += crow) {
+    const int64_t r1 = r0 + crow < tb.rows ? r0 + crow : tb.rows;
+    if (r0 > 0) __syncthreads();   // every SW is done with the previous chunk
+    stage_linear(smem, as_global(static_cast<const char*>(tb.w)) + r0 * a.R, (r1 - r0) * a.R, l.tid);
+    __syncthreads();
+    f.r0 = static_cast<int32_t>(r0);
+    f.r1 = static_cast<int32_t>(r1);
+    f.count = r0 == 0;   // each invalid id is counted once
+    walk<G, F16, W>(idx, off, lo, hi, ob, ost, l.lane_sw, it.mean != 0 && r1 == tb.rows, f, r0 > 0);
   }
 }
 
@@ -1443,8 +1478,10 @@ __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
         lds_item<G, F16, W>(a, it, bs, be, smem, (LMEM int*)&s_last);
       else if (it.strat == 1)
         hot_item<G, F16, W>(a, it, bs, be, smem);
-      else
+      else if (it.strat == 2)
         dedup_item<G, F16, W>(a, it, bs, be, smem);
+      else
+        stream_item<G, F16, W>(a, it, bs, be, smem);
       if (ti) {
         __syncthreads();
         if (l.tid == 0) ti[2 * i + 1] = now_ticks();

@@ -1,7 +1,7 @@
 // Planner: cost model (Eq. (2) extended to the four GPU data flows) and the
 // greedy asymmetric mapping of Sec. III-B.  Steps:
-//   P1 per-table strategy at split k: cheapest feasible of LDS, HOT, DEDUP, GATHER
-//      (that order breaks ties);
+//   P1 per-table strategy at split k: cheapest feasible of LDS, HOT, DEDUP, GATHER,
+//      STREAM (that order breaks ties);
 //   P2 (Sec. III-B step 1) a table larger than the LDS budget L is cut into the fewest
 //      row chunks of at most floor(min(chunk_max, L) / R) rows if its best unsplit cost
 //      exceeds the sum of the chunk costs;
@@ -68,6 +68,13 @@ CF cost_hot(const std::array<double, B_COUNT>& b, int64_t C, int64_t R, double h
 CF cost_dedup(const std::array<double, B_COUNT>& b, double u, double lam) {
   return {fl(b[B_D0] + b[B_D1] * lam + (b[B_G1] * u) * lam), fl(b[B_D0])};
 }
+// STREAM: the whole table passes through LDS in c chunks on one worker; every chunk
+// scans the slice's lookups and each lookup is read from LDS in the chunk holding it
+CF cost_stream(const std::array<double, B_COUNT>& b, int64_t m, int64_t R, double lam, int64_t c) {
+  const double bytes = static_cast<double>(m * R);
+  return {fl(b[B_L0] + b[B_S] * bytes + b[B_I] * lam * static_cast<double>(c) + b[B_L1] * lam),
+          fl(b[B_L0] + b[B_S] * bytes)};
+}
 
 struct Tab {
   int32_t t;
@@ -75,6 +82,7 @@ struct Tab {
   double s, Lam, h, u;
   int32_t C;
   bool fits;
+  int64_t sc;            // STREAM chunks: ceil(m / floor(L / R))
   int32_t force;
 };
 
@@ -108,16 +116,28 @@ struct Planner {
       case S_LDS: return cost_lds(b, tb.m, R, lam);
       case S_HOT: return cost_hot(b, tb.C, R, tb.h, lam);
       case S_DEDUP: return cost_dedup(b, tb.u, lam);
+      case S_STREAM: return cost_stream(b, tb.m, R, lam, tb.sc);
       default: return cost_gather(b, lam);
     }
   }
 
+  // STREAM as an automatic candidate: a table of at most kStreamMaxChunks chunks whose
+  // cost stays within the cap (a larger one is left out rather than failing the plan)
+  bool stream_ok(const Tab& tb, int32_t k) const {
+    if (tb.sc > kStreamMaxChunks) return false;
+    const double lam = tb.Lam / static_cast<double>(k);
+    const double x = b[B_L0] + b[B_S] * static_cast<double>(tb.m * R) + b[B_I] * lam * static_cast<double>(tb.sc) +
+                     b[B_L1] * lam;
+    return std::isfinite(x) && x < kCostCap;
+  }
+
   Best best(const Tab& tb, int32_t k) const {
     Best out{-1, 0, 0};
-    for (int32_t s = S_LDS; s <= S_GATHER; ++s) {
+    for (int32_t s = S_LDS; s <= S_STREAM; ++s) {
       if (tb.force != S_AUTO && s != tb.force) continue;
       if (s == S_LDS && !tb.fits) continue;
       if (s == S_HOT && tb.C < 1) continue;
+      if (s == S_STREAM && tb.force == S_AUTO && !stream_ok(tb, k)) continue;
       CF c = cost_of(tb, s, k);
       if (out.strat < 0 || c.cost < out.cost) out = {s, c.cost, c.fixed};
     }
@@ -266,7 +286,7 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     if (!std::isfinite(x) || x < 0.0) return fail(1, "beta");   // negative times would pile slices on one worker
   if (!in.force.empty() && static_cast<int32_t>(in.force.size()) != T) return fail(1, "force_strategy");
   for (int32_t f : in.force)
-    if (f < S_AUTO || f > S_GATHER) return fail(1, "force_strategy");
+    if (f < S_AUTO || f > S_STREAM) return fail(1, "force_strategy");
   const int64_t cm = in.chunk_max > 0 ? in.chunk_max : P.L;
   const int64_t crow = std::min(cm, P.L) / P.R;
   if (crow < 1) return fail(1, "chunk_max_bytes below one row");
@@ -287,6 +307,7 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     tb.h = h;
     tb.u = (ti.unique_frac > 0.0 && ti.unique_frac <= 1.0) ? ti.unique_frac : 1.0;
     tb.fits = tb.m * P.R <= P.L;
+    tb.sc = (tb.m + P.L / P.R - 1) / (P.L / P.R);
     tb.force = in.force.empty() ? S_AUTO : in.force[t];
     if (tb.force == S_HOT && tb.C < 1) return fail(1, "HOT forced on a table without hot rows");
     P.tabs.push_back(tb);

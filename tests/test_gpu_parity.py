@@ -11,7 +11,7 @@ from gpu_helpers import TOL, check_full, host_tables, log, plan_for, to_device, 
 
 pytestmark = pytest.mark.gpu
 
-STRATS = {"auto": -1, "lds": 0, "hot": 1, "dedup": 2, "gather": 3}
+STRATS = {"auto": -1, "lds": 0, "hot": 1, "dedup": 2, "gather": 3, "stream": 4}
 MIXED_ROWS = [1, 7, 300, 512, 513, 2000, 50000, 300000]
 
 

@@ -340,3 +340,62 @@ def test_many_gather_tables_are_placed_whole_not_split_over_all_workers():
     p3 = OPL.plan_reference(rows[:10], 64, "f32", stats[:10], 512, 64,
                             OPL.Options(beta=b, sym_max=-1, lif_milli=10 ** 9))
     assert all(s.k < 64 for s in p3.slices)
+
+
+
+# ---- STREAM (the GM-UB flow: the table through LDS in chunks on one worker)
+
+@pytest.mark.parametrize("m,R,lam", [(10000, 256, 5000.0), (3000, 512, 12.5), (70001, 128, 1e5)])
+def test_stream_cost_is_the_chunk_costs_without_their_extra_item_costs(m, R, lam):
+    """One worker scanning c chunks costs what c chunk items cost together, less the
+    (c - 1) per-item costs the single item does not pay (up to 1 ps of flooring per term)."""
+    b = OPL.default_beta(R)
+    L = 131072
+    crow = L // R
+    c = (m + crow - 1) // crow
+    chunks = sum(OPL.cost_chunk(b, ((i + 1) * m) // c - (i * m) // c, R, lam, c)[0] for i in range(c))
+    stream, fixed = OPL.cost_stream(b, m, R, lam, c)
+    assert abs(stream - (chunks - (c - 1) * b[OPL.L0])) <= c + 1
+    assert fixed == math.floor(b[OPL.L0] + b[OPL.S] * float(m * R))
+
+
+def _stream_beta():
+    beta = list(OPL.default_beta(256))
+    beta[OPL.S], beta[OPL.I], beta[OPL.L0] = 0.01, 1.0, 1000.0
+    beta[OPL.G1] = beta[OPL.D1] = beta[OPL.P] = 1e6
+    return beta
+
+
+def test_stream_is_chosen_when_it_is_cheapest_and_never_past_64_chunks():
+    R = 256
+    crow = 131072 // R
+    rows = [3 * crow, 64 * crow, 64 * crow + 1, 100]
+    stats = [OPL.Stat(20.0)] * 4
+    p = OPL.plan_reference(rows, 64, "f32", stats, 512, 64, OPL.Options(beta=_stream_beta()))
+    strat = {}
+    for ln in p.text().splitlines():
+        if ln.startswith("item "):
+            f = ln.split()
+            strat.setdefault(int(f[2]), set()).add(int(f[3]))
+    assert strat[0] == {OPL.STREAM} and strat[1] == {OPL.STREAM}
+    assert OPL.STREAM not in strat[2]          # 65 chunks: not an automatic candidate
+    assert strat[3] == {OPL.LDS}               # fits LDS: staging once beats scanning
+    # forcing STREAM is allowed at any size; the plan then has no row chunks
+    q = OPL.plan_reference(rows, 64, "f32", stats, 512, 64,
+                           OPL.Options(beta=_stream_beta(), force=[OPL.STREAM] * 4))
+    for ln in q.text().splitlines():
+        if ln.startswith("item "):
+            f = ln.split()
+            assert int(f[3]) == OPL.STREAM and int(f[5]) == 1
+
+
+def test_stream_cost_overflow_leaves_stream_out_instead_of_failing():
+    # 6.5e6 lookups on a 60-chunk table: scanning them 60 times passes the cost cap while
+    # gathering them does not; the plan still builds, without STREAM
+    R = 256
+    crow = 131072 // R
+    b = OPL.default_beta(R)
+    lam = 65536 * 100.0
+    assert b[OPL.I] * lam * 60 > OPL.COST_CAP > b[OPL.G1] * lam
+    p = OPL.plan_reference([60 * crow], 64, "f32", [OPL.Stat(100.0)], 65536, 256)
+    assert all(int(ln.split()[3]) != OPL.STREAM for ln in p.text().splitlines() if ln.startswith("item "))

@@ -35,16 +35,19 @@ def test_library_exports_every_declared_symbol():
     assert embx.status_string(embx.ERR_NOT_BOUND) == "weights not bound"
 
 
-def _both(rows, E, dtype, stats, B, K, opts: OPL.Options):
+def _cpp(rows, E, dtype, stats, B, K, opts: OPL.Options):
     embx = _lib()
-    want = OPL.plan_reference(rows, E, dtype, stats, B, K, opts).text()
     cst = [dict(mean_pooling=s.mean_pooling, max_pooling=s.max_pooling,
                 hot_rows=list(range(len(s.hot_freq))), hot_freq=list(s.hot_freq), unique_frac=s.unique_frac)
            for s in stats]
-    got = embx.plan_text(rows, E, dtype, cst, B, K, lds_budget=opts.lds_budget, lif_milli=opts.lif_milli,
-                         chunk_max_bytes=opts.chunk_max_bytes, order_mode=opts.order_mode, beta=opts.beta,
-                         force=opts.force, sym_max=opts.sym_max)
-    return got, want
+    return embx.plan_text(rows, E, dtype, cst, B, K, lds_budget=opts.lds_budget, lif_milli=opts.lif_milli,
+                          chunk_max_bytes=opts.chunk_max_bytes, order_mode=opts.order_mode, beta=opts.beta,
+                          force=opts.force, sym_max=opts.sym_max)
+
+
+def _both(rows, E, dtype, stats, B, K, opts: OPL.Options):
+    want = OPL.plan_reference(rows, E, dtype, stats, B, K, opts).text()
+    return _cpp(rows, E, dtype, stats, B, K, opts), want
 
 
 @pytest.mark.parametrize("seed", range(60))
@@ -65,7 +68,7 @@ def test_cpp_planner_equals_oracle_hypothesis(seed, variant):
     elif variant == "force":
         f = []
         for s in stats:
-            choices = [OPL.AUTO, OPL.LDS, OPL.DEDUP, OPL.GATHER] + ([OPL.HOT] if len(s.hot_freq) else [])
+            choices = [OPL.AUTO, OPL.LDS, OPL.DEDUP, OPL.GATHER, OPL.STREAM] + ([OPL.HOT] if len(s.hot_freq) else [])
             f.append(int(g.choice(choices)))
         opts.force = f
     try:
@@ -73,7 +76,7 @@ def test_cpp_planner_equals_oracle_hypothesis(seed, variant):
     except OPL.PlanError:
         embx = _lib()
         with pytest.raises(embx.EmbxError):
-            _both(rows, E, dtype, stats, B, K, opts)
+            _cpp(rows, E, dtype, stats, B, K, opts)
         return
     got, _ = _both(rows, E, dtype, stats, B, K, opts)
     assert got == want
@@ -121,3 +124,20 @@ def test_cpp_planner_equals_oracle_with_many_tables(T, sym_max):
     got, want = _both(rows, 64, "f32", stats, 1024, 128, opts)
     assert got == want
     assert f"symmax {sym_max if sym_max else OPL.SYM_MAX_DEFAULT}" in want
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_cpp_planner_equals_oracle_when_stream_is_cheapest(seed):
+    """Coefficients that make the table scan win for mid-size tables: both planners
+    choose STREAM for them and emit the same plan."""
+    rows, E, dtype, stats, B, K, opts = _random_instance(1000 + seed)
+    beta = list(OPL.default_beta(256))
+    beta[OPL.S] = 0.01
+    beta[OPL.I] = 1.0
+    beta[OPL.L0] = 1000.0
+    beta[OPL.G1] = 1e6
+    beta[OPL.D1] = 1e6
+    beta[OPL.P] = 1e6
+    opts.beta = beta
+    got, want = _both(rows, E, dtype, stats, B, K, opts)
+    assert got == want
