@@ -174,6 +174,8 @@ def main():
     ap.add_argument("--force", type=str, default="", help="force one strategy for all tables (lds|hot|dedup|gather|stream)")
     ap.add_argument("--pooling", choices=["sum", "mean"], default="sum", help="reduction of every table's bags")
     ap.add_argument("--weighted", action="store_true", help="per-lookup weights (emb_lookup_weighted)")
+    ap.add_argument("--sym-max", type=int, default=0,
+                    help="gather tables split over all workers while at most this many (0: the library default)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the lookup runs on a single MI355X "
@@ -216,6 +218,8 @@ def main():
         opts["force"] = [{"lds": 0, "hot": 1, "dedup": 2, "gather": 3, "stream": 4}[args.force]] * c.T
     if args.pooling != "sum":
         opts["pooling"] = args.pooling
+    if args.sym_max:
+        opts["sym_max"] = args.sym_max
     tp = time.time()
     plan = embx.Plan(c.rows, c.E, c.dtype, stats, c.batch, **opts).bind(weights)
     plan_ms = (time.time() - tp) * 1e3

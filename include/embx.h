@@ -115,9 +115,10 @@ typedef struct {
                                NULL -> built-in MI355X fit; a negative one is an invalid argument  */
   const int32_t* force_strategy; /* host, T entries of emb_strategy_t, or NULL (all AUTO)        */
   int32_t num_workers;      /* > 0 overrides K (must not exceed 65535)                          */
-  int32_t sym_max_gather;   /* GATHER tables are split over all workers (symmetric partitioning,
-                               Sec. III-A) while the plan has at most this many of them, else
-                               placed by cost like the rest (Sec. III-B); 0 -> 64, < 0 -> never */
+  int32_t sym_max_gather;   /* 0: a GATHER table is split over all workers (symmetric partitioning,
+                               Sec. III-A) when each slice would hold >= 64 expected lookups, else
+                               placed by cost like the rest (Sec. III-B); > 0: also every GATHER
+                               table while the plan has at most this many; < 0: never            */
   const int32_t* pooling;   /* host, T entries of emb_pooling_t, or NULL (all SUM); does not change
                                the placement, only each bag's final scaling                       */
 } emb_plan_options_t;

@@ -32,13 +32,15 @@ budget for rows):
       cost exceeds the sum of the chunk costs (the speed-up exceeds the number
       of chunks); chunks use the LDS strategy.
   P3  tau = ceil(sum of item costs / K), the ideal per-worker load.
-  P4  while the plan has at most sym_max unchunked GATHER items (default 64),
-      each is split k = min(K, B) ways (symmetric partitioning, Sec. III-A: a
-      gather slice stages nothing, so every worker takes 1/k of every such
-      table and the mix of cache-resident and HBM-bound tables is the same on
-      every worker); with more of them, T x K slices would swamp the launch, and
-      they are split like the others, which leaves small tables whole and
-      places them asymmetrically (Sec. III-B).  Any other item
+  P4  an unchunked GATHER item whose k = min(K, B) slices would each hold at
+      least 64 expected lookups (Lam_t / k >= 64) is split k ways (symmetric
+      partitioning, Sec. III-A: a gather slice stages nothing, so every worker
+      takes 1/k of every such table and the mix of cache-resident and
+      HBM-bound tables is the same on every worker); smaller ones are split
+      like the others (T x K tiny slices would swamp the launch), which leaves
+      small tables whole and places them asymmetrically (Sec. III-B).  With
+      sym_max > 0 every GATHER item is split k ways while the plan has at most
+      sym_max of them; sym_max < 0 turns symmetric splitting off.  Any other item
       costing more than tau is batch-split k ways (the paper's optional
       replication): the smallest k in [2, min(K, B)] whose best cost is at most
       max(tau, 2 x its fixed cost); all chunks of one table share one k.  A
@@ -77,7 +79,7 @@ MAX_HOT = 4096          # hot rows a table's statistics may list
 MAX_HOT_SLOTS = 2048    # hot rows one HOT item stages at most
 MAX_CHUNKS = 65536
 STREAM_MAX_CHUNKS = 64  # STREAM is an automatic candidate up to this many chunks
-SYM_MAX_DEFAULT = 64    # GATHER tables split over all workers while the plan has at most this many
+SYM_SHARE_MIN = 64.0    # GATHER tables split over all workers when each slice would hold this many lookups
 
 
 class PlanError(ValueError):
@@ -128,7 +130,7 @@ class Options:
     order_mode: int = 0
     beta: Optional[Sequence[float]] = None
     force: Optional[Sequence[int]] = None
-    sym_max: int = 0                  # 0 -> SYM_MAX_DEFAULT; < 0: GATHER items never split symmetrically
+    sym_max: int = 0                  # > 0: GATHER items split symmetrically while at most this many; < 0: never
 
 
 @dataclass
@@ -163,7 +165,7 @@ class Plan:
     sum_ps: int = 0
     lif_milli: int = 0
     r_sym: int = 0
-    sym_max: int = SYM_MAX_DEFAULT
+    sym_max: int = 0
 
     def text(self) -> str:
         lines = ["embx-plan v1",
@@ -395,11 +397,13 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
             return LDS, c, f
         return tb.best(b, k)
 
-    sym_max = opts.sym_max if opts.sym_max != 0 else SYM_MAX_DEFAULT
+    sym_max = opts.sym_max
     n_gather = sum(1 for g in groups if g[0].nchunks == 1 and g[0].strat == GATHER)
-    sym_gather = sym_max > 0 and n_gather <= sym_max
+    few_gather = sym_max > 0 and n_gather <= sym_max
     for g in groups:
-        if sym_gather and g[0].nchunks == 1 and g[0].strat == GATHER:
+        sym = (sym_max >= 0 and g[0].nchunks == 1 and g[0].strat == GATHER and
+               (few_gather or tabs[g[0].t].Lam / float(kmax) >= SYM_SHARE_MIN))
+        if sym:
             ks = [kmax]
         else:
             ks = [1 if it.cost <= tau else split_k(it) for it in g]

@@ -7,7 +7,10 @@
 //      exceeds the sum of the chunk costs;
 //   P3 tau = ceil(total cost / K);
 //   P4 a GATHER item is split k = min(K, B) ways (symmetric partitioning, Sec. III-A:
-//      a gather slice stages nothing, so every worker takes 1/k of every such table);
+//      a gather slice stages nothing, so every worker takes 1/k of every such table)
+//      when its slices would hold at least kSymShareMin expected lookups each, or
+//      (sym_max > 0) while the plan has at most sym_max of them; sym_max < 0: never;
+//      others are split like the rest;
 //      any other item above tau is batch-split k ways: the smallest k in [2, min(K, B)]
 //      whose best cost is at most max(tau, 2 x fixed cost); the chunks of a table share
 //      one k;
@@ -354,14 +357,16 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     P.tau = static_cast<int64_t>((total1 + P.K - 1) / P.K);
 
     // P4
-    const int32_t sym_max = in.sym_max != 0 ? in.sym_max : kSymMaxDefault;
+    const int32_t sym_max = in.sym_max;
     int32_t n_gather = 0;
     for (const auto& g : P.groups) n_gather += (g[0].nchunks == 1 && g[0].strat == S_GATHER) ? 1 : 0;
-    const bool sym_gather = sym_max > 0 && n_gather <= sym_max;
+    const bool few_gather = sym_max > 0 && n_gather <= sym_max;
     out->sym_max = sym_max;
     for (auto& g : P.groups) {
       int32_t k = 1;
-      if (sym_gather && g[0].nchunks == 1 && g[0].strat == S_GATHER)
+      const bool sym = sym_max >= 0 && g[0].nchunks == 1 && g[0].strat == S_GATHER &&
+                       (few_gather || P.tabs[g[0].t].Lam / static_cast<double>(P.kmax) >= kSymShareMin);
+      if (sym)
         k = P.kmax;
       else
         for (const Item& it : g) k = std::max(k, it.cost <= P.tau ? 1 : P.split_k(it));

@@ -40,9 +40,10 @@ struct PlanIn {
   std::array<double, B_COUNT> beta{};
   bool has_beta = false;
   std::vector<int32_t> force;   // empty = all AUTO
-  int32_t sym_max = 0;          // 0 -> kSymMaxDefault; < 0: GATHER items never split symmetrically
+  int32_t sym_max = 0;          // > 0: GATHER items split symmetrically while at most this many; < 0: never
 };
-constexpr int32_t kSymMaxDefault = 64;   // GATHER tables split over all workers while at most this many
+constexpr double kSymShareMin = 64.0;   // GATHER tables split over all workers when each slice would hold
+                                        // at least this many expected lookups
 
 struct PSlice {
   int32_t wg, t, strat, chunk, nchunks;
@@ -53,7 +54,7 @@ struct PSlice {
 };
 
 struct PlanOut {
-  int32_t T = 0, E = 0, R = 0, K = 0, B = 0, theta = 0, order_mode = 0, sym_max = kSymMaxDefault;
+  int32_t T = 0, E = 0, R = 0, K = 0, B = 0, theta = 0, order_mode = 0, sym_max = 0;
   int64_t L = 0;
   bool f16 = false;
   std::vector<PSlice> slices;   // sorted by (wg, seq)

@@ -182,9 +182,12 @@ def test_gather_tables_are_partitioned_symmetrically():
         assert sorted(s.wg for s in p.slices if s.t == t) == list(range(K))
         assert all(s.k == K for s in p.slices if s.t == t)
     assert p.lif_milli == 1000
-    # fewer samples than workers: k = B
-    p = OPL.plan_reference(rows, 64, "f32", stats, 5, K, OPL.Options(force=[OPL.GATHER] * 3))
+    # fewer samples than workers: k = B (with sym_max > 0 every gather table is split)
+    p = OPL.plan_reference(rows, 64, "f32", stats, 5, K, OPL.Options(force=[OPL.GATHER] * 3, sym_max=10))
     assert all(s.k == 5 for s in p.slices)
+    # by default slices of 1..8 lookups are too small to split a table into
+    p = OPL.plan_reference(rows, 64, "f32", stats, 5, K, OPL.Options(force=[OPL.GATHER] * 3))
+    assert not any(s.k == 5 for s in p.slices if s.t == 0)
 
 
 def test_one_huge_table_is_split_over_all_workers():
@@ -312,9 +315,9 @@ def test_lpt_bound_is_tight_on_the_classic_instance():
 
 
 def test_many_gather_tables_are_placed_whole_not_split_over_all_workers():
-    # 200 small gather tables on 64 workers: T x K slices would swamp a launch, so past
-    # sym_max tables they are priced and split like any item; small ones stay whole and
-    # are spread over the workers by least-loaded placement (the asymmetric mapping)
+    # 200 small gather tables on 64 workers (8 lookups per worker share): T x K tiny slices
+    # would swamp a launch, so they are priced and split like any item; small ones stay
+    # whole and are spread over the workers by least-loaded placement (the asymmetric mapping)
     g = np.random.default_rng(11)
     rows = [int(x) for x in g.integers(1000, 100000, size=200)]
     stats = [OPL.Stat(1.0) for _ in rows]
@@ -322,7 +325,7 @@ def test_many_gather_tables_are_placed_whole_not_split_over_all_workers():
     b[OPL.L0] = b[OPL.H0] = b[OPL.D0] = 1e12      # only GATHER is affordable
     p = OPL.plan_reference(rows, 64, "f32", stats, 512, 64, OPL.Options(beta=b))
     assert all(s.strat == OPL.GATHER for s in p.slices)
-    assert p.sym_max == OPL.SYM_MAX_DEFAULT
+    assert p.sym_max == 0
     assert len(p.slices) < 200 * 64 // 4
     whole = [s for s in p.slices if s.k == 1]
     assert len(whole) >= 150
@@ -399,3 +402,33 @@ def test_stream_cost_overflow_leaves_stream_out_instead_of_failing():
     assert b[OPL.I] * lam * 60 > OPL.COST_CAP > b[OPL.G1] * lam
     p = OPL.plan_reference([60 * crow], 64, "f32", [OPL.Stat(100.0)], 65536, 256)
     assert all(int(ln.split()[3]) != OPL.STREAM for ln in p.text().splitlines() if ln.startswith("item "))
+
+
+def test_many_gather_tables_split_over_all_workers_only_when_their_slices_are_large():
+    """Past sym_max gather tables, a table is split over all workers only if each slice
+    would hold at least 64 expected lookups; the small ones are placed by cost."""
+    g = np.random.default_rng(4)
+    T, B, K = 100, 4096, 256
+    rows = [int(x) for x in np.exp(g.uniform(np.log(1e3), np.log(1e6), size=T))]
+    pools = [8.0 if t % 2 == 0 else 1.0 for t in range(T)]   # shares 128 and 16 lookups
+    stats = [OPL.Stat(s) for s in pools]
+    p = OPL.plan_reference(rows, 64, "f32", stats, B, K)
+    ks = {}
+    for ln in p.text().splitlines():
+        if ln.startswith("item "):
+            f = ln.split()
+            ks.setdefault(int(f[2]), set()).add(int(f[8]))
+    for t in range(T):
+        if t % 2 == 0:
+            assert ks[t] == {K}, (t, ks[t])
+        else:
+            assert max(ks[t]) < K, (t, ks[t])
+    # sym_max < 0 turns both rules off (a table may still reach K slices by its cost or
+    # the LIF fallback, but fewer do); a large sym_max splits every table
+    def n_full(plan):
+        return len({int(ln.split()[2]) for ln in plan.text().splitlines()
+                    if ln.startswith("item ") and int(ln.split()[8]) == K})
+    q = OPL.plan_reference(rows, 64, "f32", stats, B, K, OPL.Options(sym_max=-1))
+    assert n_full(q) < n_full(p) == T // 2
+    r = OPL.plan_reference(rows, 64, "f32", stats, B, K, OPL.Options(sym_max=1000))
+    assert all(int(ln.split()[8]) == K for ln in r.text().splitlines() if ln.startswith("item "))

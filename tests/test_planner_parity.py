@@ -123,7 +123,7 @@ def test_cpp_planner_equals_oracle_with_many_tables(T, sym_max):
     opts = OPL.Options(sym_max=sym_max)
     got, want = _both(rows, 64, "f32", stats, 1024, 128, opts)
     assert got == want
-    assert f"symmax {sym_max if sym_max else OPL.SYM_MAX_DEFAULT}" in want
+    assert f"symmax {sym_max}" in want
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -141,3 +141,15 @@ def test_cpp_planner_equals_oracle_when_stream_is_cheapest(seed):
     opts.beta = beta
     got, want = _both(rows, E, dtype, stats, B, K, opts)
     assert got == want
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_cpp_planner_equals_oracle_with_many_tables_of_mixed_shares(seed):
+    g = np.random.default_rng(50 + seed)
+    T = int(g.integers(65, 160))
+    rows = [int(x) for x in np.exp(g.uniform(np.log(100), np.log(2e6), size=T))]
+    stats = [OPL.Stat(float(g.choice([0.0, 1.0, 4.0, 20.0]))) for _ in range(T)]
+    B = int(g.choice([1024, 4096, 16384]))
+    for sym_max in (0, -1, 80):
+        got, want = _both(rows, 64, "f32", stats, B, 256, OPL.Options(sym_max=sym_max))
+        assert got == want
