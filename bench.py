@@ -45,7 +45,11 @@ import workloads as W  # noqa: E402
 HBM_PEAK_GBPS = 8000.0
 METRIC = "embedding lookups/s + queries/s, P99 batch latency, % HBM peak (1 MI355X)"
 DEFAULT_CONFIG = 2
-KERNEL_SOURCES = ["paper_2507_01676_amd/csrc/lookup.hip", "paper_2507_01676_amd/csrc/device_types.hpp"]
+# what decides a launch's memory traffic: the kernels and the plan (planner + metadata);
+# a stored traffic measurement is used only while their hash is unchanged
+KERNEL_SOURCES = ["paper_2507_01676_amd/csrc/lookup.hip", "paper_2507_01676_amd/csrc/device_types.hpp",
+                  "paper_2507_01676_amd/csrc/planner.cpp", "paper_2507_01676_amd/csrc/planner.hpp",
+                  "paper_2507_01676_amd/csrc/api.cpp"]
 
 
 def log(msg):
