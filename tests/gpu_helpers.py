@@ -71,8 +71,9 @@ def check_full(got: np.ndarray, weights_host, batch: W.Batch, dtype: str, exact:
 
 
 def check_sampled(c: W.Config, got: np.ndarray, batch: W.Batch, n_bags: int, seed: int,
-                  mode=W.VAL_UNIFORM, exact: bool = False):
-    """Oracle on n_bags random (table, sample) bags; table rows regenerated on the host."""
+                  mode=W.VAL_UNIFORM, exact: bool = False, pooling=None, psw=None):
+    """Oracle on n_bags random (table, sample) bags; table rows regenerated on the host.
+    pooling: None / "sum" / "mean" or one per table; psw: per-lookup weights (all lookups)."""
     g = np.random.default_rng(seed)
     B, T = batch.B, c.T
     tsel = g.integers(0, T, size=n_bags)
@@ -84,11 +85,14 @@ def check_sampled(c: W.Config, got: np.ndarray, batch: W.Batch, n_bags: int, see
         hi = batch.offsets[t * B + bs + 1]
         parts = [batch.indices[a:b] for a, b in zip(lo, hi)]
         idx = np.concatenate(parts) if parts else np.zeros(0, np.int64)
+        wk = None if psw is None else np.concatenate([psw[a:b] for a, b in zip(lo, hi)])
+        mode_t = pooling if (pooling is None or isinstance(pooling, str)) else pooling[int(t)]
         uniq, inv = np.unique(idx, return_inverse=True)
         vals = W.table_rows_at(int(t), uniq, c.E, c.dtype, seed=c.value_seeds[t], lo=c.lo, hi=c.hi, mode=mode)
         off = np.zeros(bs.size + 1, np.int64)
         np.cumsum(hi - lo, out=off[1:])
-        ref, mag, _ = OP.pool_reference([vals], inv.reshape(-1).astype(np.int64), off, bs.size)
+        ref, mag, _ = OP.pool_reference([vals], inv.reshape(-1).astype(np.int64), off, bs.size,
+                                        pooling=mode_t, psw=wk)
         mine = got[bs, t, :][:, None, :]
         if exact:
             assert np.array_equal(mine, ref), f"table {t}: sampled bags differ"

@@ -70,6 +70,32 @@ def test_workload_full_size_sampled(cfg):
     _free()
 
 
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_workload_full_size_sampled_weighted_and_mean(cfg):
+    """Weighted lookups with mean and sum tables alternating, at full size, with the
+    plan and launch bench.py uses for --weighted --pooling."""
+    import torch
+    log(f"workload {cfg}: full size, weighted, mean/sum tables, sampled bags")
+    c = W.make_config(cfg)
+    batch = W.gen_batch(c, 0)
+    stats = W.history_stats(c)
+    wd = filled_tables(c)
+    pooling = ["mean" if t % 2 == 0 else "sum" for t in range(c.T)]
+    psw = np.random.default_rng(1000).uniform(0.5, 1.5, size=batch.indices.size).astype(np.float32)
+    p = plan_for(c, c.batch, stats=stats, pooling=pooling)
+    p.bind(wd)
+    idx, off = to_device(batch)
+    out = p.lookup(idx, off, batch.B, weights=torch.from_numpy(psw).cuda())
+    torch.cuda.synchronize()
+    assert p.check_errors() == 0
+    got = out.cpu().numpy()
+    del out, idx, off
+    err = check_sampled(c, got, batch, 4000, seed=200 + cfg, pooling=pooling, psw=psw)
+    log(f"  worst pooled error on 4000 bags {err:.2e}")
+    del wd
+    _free()
+
+
 def test_workload5_full_size_sampled():
     import torch
     log("workload 5 (100 tables <= 150 GB, E128 fp32, B65536): full size, sampled bags")
