@@ -999,19 +999,49 @@ struct SegRef {
   int e, bs, be;
 };
 
-// Chunks c = first, first + step, ... of one worker's gather queue held in LDS (runs
-// [e, e_end); chunk c of run x is bags [bs + (c - chunk_base) cb, + cb) of its slice,
-// clipped to the slice at the runtime batch).  Only LDS is read.
+// The chunks of one worker's gather queue held in LDS (runs [e, e_end); chunk c of run
+// x is bags [bs + (c - chunk_base) cb, + cb) of its slice, clipped to the slice at the
+// runtime batch).  A group (a SW, or a wavefront in wave mode) first takes the chunk
+// numbered like itself.  With a counter (dynamic), it then claims further chunks in
+// order from that counter in LDS, shared by the worker and starting after the first
+// round, so groups that run fast take more chunks and the worker's groups finish
+// together; without one, group g takes chunks g, g + groups, ...  (Claiming even the
+// first chunk from the counter would let the walkers' look-ahead -- they open up to
+// three chunks at once -- give all of a short queue to the first few groups.)  Only
+// LDS is read.
 struct RunQueue {
   const LMEM GatherRun* r;
-  int e, e_end, c, step, nchunks, B;
+  int e, e_end, nchunks, B;
+  bool dynamic;         // further chunks from the counter (else every groups-th chunk)
+  LMEM int* ctr;        // the queue's next unclaimed chunk after the first round (LDS
+                        // offsets start at 0, so this may be a null-valued pointer)
+  int lane_g, width;    // this lane's index in its group, the group's lanes
+  int c;                // the group's next chunk (static), or its first-round chunk, -1 once taken
+  int groups;           // groups sharing the queue
+  __device__ __forceinline__ int claim() {
+    if (!dynamic) {
+      const int v = c;
+      c += groups;
+      return v;
+    }
+    if (c >= 0) {
+      const int v = c;
+      c = -1;
+      return v;
+    }
+    if (nchunks <= groups) return nchunks;   // the first round took every chunk
+    int v = 0;
+    if (lane_g == 0) v = atomicAdd(ctr, 1);
+    return width == 1 ? v : __shfl(v, 0, width);
+  }
   __device__ __forceinline__ bool next(SegRef& s) {
-    while (c < nchunks) {
+    while (true) {
+      const int c = claim();
+      if (c >= nchunks) return false;
       while (e + 1 < e_end && r[e + 1].chunk_base <= c) ++e;
       const int bs = slice_lo(r[e].j, r[e].k, B), be = slice_lo(r[e].j + 1, r[e].k, B);
       const int c0 = bs + (c - r[e].chunk_base) * r[e].cb;
       const int c1 = min(be, c0 + r[e].cb);
-      c += step;
       if (c0 < c1) {
         s.e = e;
         s.bs = c0;
@@ -1019,7 +1049,6 @@ struct RunQueue {
         return true;
       }
     }
-    return false;
   }
 };
 
@@ -1395,19 +1424,22 @@ __device__ __forceinline__ void walk_single(GMEM const int64_t* __restrict__ ind
 
 // Gather slices.  A worker's gather slices are cut into three queues of chunks (runs
 // of bags of one slice): long-bag slices (wave mode), single-lookup-bag slices, and
-// the rest (SW mode).  Wavefront v
-// takes wave-mode chunks v, v + 16, ...; SW s takes SW-mode chunks s, s + NSW, ...  The
-// chunks are small, so every SW samples every slice of the worker: the split stays
-// even when per-lookup cost differs between tables (cache-resident vs HBM-bound).  The
-// worker's runs are first copied into LDS (`lds`), so that finding a chunk's table and
-// bags costs no memory round trip.
+// the rest (SW mode).  Wavefront v takes wave-mode chunks v, v + 16, ... and SW s
+// single-lookup chunks s, s + NSW, ... (about one each: wave chunks are sized so);
+// SW-mode chunks are many per SW, and after the first round they are claimed one at
+// a time from a counter, so the split stays even when per-lookup cost differs between
+// tables (cache-resident vs HBM-bound) or from step to step.  The worker's runs are
+// first copied into LDS (`lds`), so that finding a chunk's table and bags costs no
+// memory round trip.
 template <int G, bool F16, bool W>
-__device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, const Lane& l, int wg) {
-  constexpr int NSW = kBlock / G;
+__device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, const Lane& l, int wg,
+                                             LMEM int* qctr) {
   {   // the worker's slot: a header record, then its runs
     gchar* src = reinterpret_cast<gchar*>(as_global(a.gr) + static_cast<int64_t>(wg) * a.gr_slot);
     for (int q = l.tid; q < 3 * a.gr_slot; q += kBlock) sts16(lds + 16 * q, ldg16(src + 16 * q));
   }
+  constexpr int NSW = kBlock / G;
+  if (l.tid == 0) *qctr = NSW;   // the SW-mode queue's counter, after its first round
   __syncthreads();
   const LMEM GatherSlotHeader* hd = reinterpret_cast<const LMEM GatherSlotHeader*>(lds);
   const int n_wave = hd->n_wave, wave_chunks = hd->wave_chunks, n_single = hd->n_single,
@@ -1423,7 +1455,7 @@ __device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, co
   tb0.rows = 0;
   const RowBase rb0 = row_base(a, tb0, l);
   {  // wave mode
-    RunQueue q{runs, 0, n_wave, l.wave, kNumWaves, wave_chunks, a.B};
+    RunQueue q{runs, 0, n_wave, wave_chunks, a.B, false, qctr, 0, kWave, l.wave, kNumWaves};
     SegRef s;
     while (q.next(s)) {
       FGather f;
@@ -1436,13 +1468,13 @@ __device__ __forceinline__ void gather_phase(const LookupArgs& a, lchar* lds, co
     }
   }
   {  // single-lookup bags
-    RunQueue q{runs, n_wave, n_wave + n_single, l.sw, NSW, single_chunks, a.B};
+    RunQueue q{runs, n_wave, n_wave + n_single, single_chunks, a.B, false, qctr, l.lane_sw, G, l.sw, NSW};
     FGather f;
     static_cast<RowBase&>(f) = rb0;
     walk_single<G, F16, W>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
   }
   {  // SW mode
-    RunQueue q{runs, n_wave + n_single, nr, l.sw, NSW, sw_chunks, a.B};
+    RunQueue q{runs, n_wave + n_single, nr, sw_chunks, a.B, true, qctr, l.lane_sw, G, l.sw, NSW};
     FGather f;
     static_cast<RowBase&>(f) = rb0;
     walk_stream<G, F16, W>(idx, offsets, out, a.E, a.B, ost, l.lane_sw, f, q);
@@ -1455,6 +1487,7 @@ template <int G, bool F16, bool STAGED, bool W>
 __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
   extern __shared__ __align__(16) char smem_raw[];
   __shared__ int s_last;
+  __shared__ int s_queue;
   const Lane l = lane_of<G>(a.R);
   const int wg = blockIdx.x;
   GMEM const int32_t* wg_ptr = as_global(a.wg_ptr);
@@ -1490,7 +1523,7 @@ __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
   }
   if (tw && l.tid == 0) tw[1] = now_ticks();
   __syncthreads();   // staged slices are done with LDS
-  gather_phase<G, F16, W>(a, (lchar*)smem_raw, l, wg);
+  gather_phase<G, F16, W>(a, (lchar*)smem_raw, l, wg, (LMEM int*)&s_queue);
   if (tw && (l.tid & (kWave - 1)) == 0) tw[2 + l.wave] = now_ticks();
 }
 
