@@ -317,10 +317,10 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
 
   // gather run queues per worker, slices in plan order: wave-mode runs, then runs of
   // tables whose bags hold at most one lookup (kChunkSingle bags per chunk: one step
-  // of a SW), then SW-mode runs.  SW-mode chunks carry about W / (4 NSW) expected lookups (W: the worker's
-  // SW-mode lookups at the max batch), at least one full step (8) and at most 32, so
-  // that each SW gets several chunks; wave-mode chunks carry about four wavefront
-  // steps of lookups, fewer when that leaves some of the 16 wavefronts without one.
+  // of a SW), then SW-mode runs.  SW-mode chunks carry about sqrt(5 W / NSW) expected
+  // lookups (W: the worker's SW-mode lookups at the max batch), at least one full step
+  // (8) and at most 128; wave-mode chunks carry about four wavefront steps of lookups,
+  // fewer when that leaves some of the 16 wavefronts without one.
   std::vector<GatherRun> gr;                       // runs, worker-major
   std::vector<int32_t> gr_ptr(K + 1, 0);
   std::vector<GatherSlotHeader> gr_head(K);
@@ -342,7 +342,11 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
         else if (stats[items[i].table].max_pooling > 1)
           Ws += lk;
       }
-      const double target = std::min(32.0, std::max(8.0, std::floor(Ws / (4.0 * nsw))));
+      // SW-mode chunks are claimed dynamically: a chunk boundary costs about five lookups
+      // of a SW's time and the worker's tail is up to one chunk, so ~sqrt(5 W / NSW)
+      // lookups per chunk balances the two; measured, chunks past ~128 lookups lose again
+      // (the SWs then work on fewer tables at a time), hence the cap
+      const double target = std::min(128.0, std::max(8.0, std::floor(std::sqrt(5.0 * Ws / nsw))));
       const double wtarget = std::min(wave_chunk, std::max(1.0, std::floor(Ww / nwaves)));
       gr_ptr[w] = static_cast<int32_t>(gr.size());
       // classes, in queue order: 0 wave mode, 1 single-lookup bags, 2 SW mode
