@@ -178,6 +178,9 @@ def main():
     ap.add_argument("--force", type=str, default="", help="force one strategy for all tables (lds|hot|dedup|gather|stream)")
     ap.add_argument("--pooling", choices=["sum", "mean"], default="sum", help="reduction of every table's bags")
     ap.add_argument("--weighted", action="store_true", help="per-lookup weights (emb_lookup_weighted)")
+    ap.add_argument("--dist", choices=list(W.DISTRIBUTIONS), default="config",
+                    help="query distribution of every table: the workload's own, uniform, or fixed "
+                         "(every lookup of a table on one row)")
     ap.add_argument("--sym-max", type=int, default=0,
                     help="gather tables split over all workers while at most this many (0: the library default)")
     args = ap.parse_args()
@@ -192,7 +195,7 @@ def main():
     assert torch.cuda.is_available(), "no GPU"
     torch.cuda.set_device(0)
 
-    c = W.make_config(args.config)
+    c = W.with_distribution(W.make_config(args.config), args.dist)
     R = args.batches or (4 if args.config == 5 else 8)
     t0 = time.time()
     log(f"workload {c.cfg_id}: {c.name}; generating {R} batches + statistics")
@@ -305,7 +308,8 @@ def main():
     achieved = alg_mean / (launch_ms * 1e-3) / 1e9
     src_hash = kernel_source_hash()
     workload = f"workload{c.cfg_id}"
-    variant = ("" if args.pooling == "sum" else f"-{args.pooling}") + ("-weighted" if args.weighted else "")
+    variant = (("" if args.dist == "config" else f"-{args.dist}") + ("" if args.pooling == "sum" else f"-{args.pooling}")
+               + ("-weighted" if args.weighted else ""))
     traffic = load_traffic(workload + variant, src_hash)
 
     copy_gbps = None if args.no_copy else copy_bandwidth_gbps()
@@ -329,7 +333,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{workload}{variant}: {c.name}", "tables": c.T, "E": c.E, "table_dtype": c.dtype,
                    "batch": c.batch, "lookups_per_batch": int(sum(n_look) / R), "resident_batches": R,
-                   "table_bytes": sum(c.rows) * R_b, "pooling": args.pooling, "weighted": bool(args.weighted)},
+                   "table_bytes": sum(c.rows) * R_b, "pooling": args.pooling, "weighted": bool(args.weighted),
+                   "queries": args.dist},
         "queries_per_s": B * K / wall,
         "p99_us": p99(lat_ms) * 1e3,
         "mean_us": mean_ms * 1e3,

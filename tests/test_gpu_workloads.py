@@ -70,6 +70,36 @@ def test_workload_full_size_sampled(cfg):
     _free()
 
 
+@pytest.mark.parametrize("cfg,dist", [(1, "fixed"), (2, "fixed"), (2, "uniform"), (4, "fixed")])
+def test_workload_query_distributions(cfg, dist):
+    """The workloads under the paper's other query distributions (Sec. IV-A): uniform,
+    and fixed (every lookup of a table on one row, the paper's stress test for
+    same-line conflicts), planned from statistics of that distribution, at full size."""
+    log(f"workload {cfg}, {dist} queries: full size")
+    c = W.with_distribution(W.make_config(cfg), dist)
+    batch = W.gen_batch(c, 0)
+    stats = W.history_stats(c)
+    if cfg == 1:
+        hw = host_tables(c)
+        got = _lookup(c, batch, upload_tables(hw), stats)
+        check_full(got, hw, batch, c.dtype)
+        hi = host_tables(c, W.VAL_INTEGER)
+        got = _lookup(c, batch, upload_tables(hi), stats)
+        check_full(got, hi, batch, c.dtype, exact=True)
+        return
+    wd = filled_tables(c)
+    got = _lookup(c, batch, wd, stats)
+    err = check_sampled(c, got, batch, 4000, seed=200 + cfg)
+    log(f"  worst pooled error on 4000 bags {err:.2e}")
+    wi = filled_tables(c, W.VAL_INTEGER)
+    del wd
+    _free()
+    got = _lookup(c, batch, wi, stats)
+    check_sampled(c, got, batch, 4000, seed=300 + cfg, mode=W.VAL_INTEGER, exact=True)
+    del wi
+    _free()
+
+
 @pytest.mark.parametrize("cfg", [3, 4])
 def test_workload_full_size_sampled_weighted_and_mean(cfg):
     """Weighted lookups with mean and sum tables alternating, at full size, with the

@@ -115,3 +115,31 @@ def test_cfg4_skew_matches_zipf_1_5():
     _, cnt = np.unique(idx, return_counts=True)
     top = cnt.max() / idx.size
     assert abs(top - 1.0 / 2.612375348685488) < 0.02
+
+
+def test_query_distributions():
+    """The three query distributions of the paper's experiments (Sec. IV-A): the
+    workload's own, uniform, and fixed (every lookup of a table on one row)."""
+    c = W.make_config(2)
+    assert W.with_distribution(c, "config") is c
+    with pytest.raises(ValueError):
+        W.with_distribution(c, "zipf")
+    f = W.with_distribution(c, "fixed")
+    assert f.rows == c.rows and f.E == c.E and f.value_seeds == c.value_seeds and f.batch == c.batch
+    b0, b1, b = W.gen_batch(f, 0), W.gen_batch(f, 1), W.gen_batch(c, 0)
+    assert np.array_equal(b0.offsets, b.offsets)                # pooling factors unchanged
+    for t in range(f.T):
+        ids = b0.indices[b0.offsets[t * f.batch]:b0.offsets[(t + 1) * f.batch]]
+        assert ids.size > 0 and np.all(ids == ids[0]) and 0 <= ids[0] < f.rows[t]
+        assert ids[0] == W.fixed_row(2, t, f.rows[t])
+    assert np.array_equal(b0.indices, b1.indices)               # the same row in every batch
+    st = W.history_stats(f)
+    for t in range(f.T):                                        # statistics see the one row
+        assert st[t].hot_freq[0] == 1.0 and st[t].hot_rows[0] == W.fixed_row(2, t, f.rows[t])
+        assert st[t].unique_frac == 1.0 / W.make_config(2).batch
+    u = W.with_distribution(c, "uniform")
+    bu = W.gen_batch(u, 0)
+    t = c.T - 1                                                 # 4M rows: a uniform draw spreads out
+    ids = bu.indices[bu.offsets[t * c.batch]:bu.offsets[(t + 1) * c.batch]]
+    assert np.unique(ids).size > 0.99 * ids.size
+    assert abs(ids.mean() / c.rows[t] - 0.5) < 0.05

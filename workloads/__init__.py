@@ -36,7 +36,7 @@ import numpy as np
 MASTER = 250701676
 
 # purposes of the seeded streams
-P_SIZES, P_ALPHA, P_PERM, P_PF, P_INDICES, P_VALUE = 0, 1, 2, 3, 4, 5
+P_SIZES, P_ALPHA, P_PERM, P_PF, P_INDICES, P_VALUE, P_FIXED = 0, 1, 2, 3, 4, 5, 6
 
 GOLDEN = 0x9E3779B97F4A7C15
 MIX1 = 0xBF58476D1CE4E5B9
@@ -168,7 +168,7 @@ class TableSpec:
     pf_value: float         # fixed PF, or Poisson mean
     pf_lo: int              # clip bounds (poisson) / both = value (fixed)
     pf_hi: int
-    dist: str               # 'uniform' or 'zipf'
+    dist: str               # 'uniform', 'zipf', or 'fixed' (every lookup on one row)
     alpha: float = 0.0
 
 
@@ -199,6 +199,24 @@ class Config:
 
     def max_pooling(self, t: int) -> int:
         return self.tables[t].pf_hi
+
+
+DISTRIBUTIONS = ("config", "uniform", "fixed")
+
+
+def with_distribution(c: Config, dist: str) -> Config:
+    """``c`` with every table's query distribution replaced: 'uniform' (ids uniform over
+    the table's rows) or 'fixed' (every lookup of a table on one row), the
+    distributions besides the skewed one that the paper runs its workloads under
+    (Sec. IV-A).  Shapes, pooling factors and values are unchanged; 'config' returns
+    ``c`` itself."""
+    if dist == "config":
+        return c
+    if dist not in DISTRIBUTIONS:
+        raise ValueError(f"unknown query distribution {dist!r}")
+    tabs = [TableSpec(tb.rows, tb.pf_kind, tb.pf_value, tb.pf_lo, tb.pf_hi, dist, tb.alpha) for tb in c.tables]
+    return Config(c.cfg_id, f"{c.name}; {dist} queries", c.E, c.dtype, c.lo, c.hi, c.batch, tabs, c.note,
+                  list(c.value_seeds))
 
 
 def cfg2_sizes() -> List[int]:
@@ -286,9 +304,17 @@ def pooling_factors(c: Config, t: int, batch_id: int, B: Optional[int] = None) -
     return np.clip(g.poisson(tb.pf_value, size=B), tb.pf_lo, tb.pf_hi).astype(np.int64)
 
 
+def fixed_row(cfg: int, t: int, m: int) -> int:
+    """The one row every lookup of table t reads under the 'fixed' distribution: a
+    seeded row, the same in every batch (history batch included)."""
+    return int(rng(cfg, P_FIXED, t).integers(0, m))
+
+
 def table_indices(c: Config, t: int, n: int, batch_id: int, perm: Optional[np.ndarray] = None) -> np.ndarray:
     """n row ids of table t for batch ``batch_id``."""
     tb = c.tables[t]
+    if tb.dist == "fixed":
+        return np.full(n, fixed_row(c.cfg_id, t, tb.rows), dtype=np.int64)
     g = rng(c.cfg_id, P_INDICES, t, batch_id)
     if tb.dist == "uniform":
         return g.integers(0, tb.rows, size=n, dtype=np.int64)
