@@ -39,20 +39,44 @@ def _run(cmd, verbose):
     return r
 
 
+# lookup.hip is compiled in parts (EMBX_PART): one per (row type, weighted) kernel
+# family, plus the probes, filler and launch code
+LOOKUP_PARTS = 5
+
+
+def _run_all(cmds, verbose):
+    """Runs the compile commands in parallel; raises on the first failure."""
+    procs = []
+    for cmd in cmds:
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
+    failed = None
+    for cmd, p in procs:
+        out, _ = p.communicate()
+        if p.returncode != 0 and failed is None:
+            failed = (cmd, out)
+    if failed is not None:
+        sys.stderr.write(failed[1])
+        raise RuntimeError(f"build step failed: {' '.join(failed[0][:3])} ...")
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     hipcc = _hipcc()
-    objs = []
-    o = os.path.join(BUILD, "lookup.o")
-    _run([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, "lookup.hip"), "-o", o], verbose)
-    objs.append(o)
+    cmds, objs = [], []
+    for part in range(LOOKUP_PARTS):
+        o = os.path.join(BUILD, f"lookup_{part}.o")
+        cmds.append([hipcc, *HIP_FLAGS, f"-DEMBX_PART={part}", "-c", os.path.join(CSRC, "lookup.hip"), "-o", o])
+        objs.append(o)
     o = os.path.join(BUILD, "api.o")
-    _run([hipcc, *HIP_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, "api.cpp"), "-o", o], verbose)
+    cmds.append([hipcc, *HIP_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, "api.cpp"), "-o", o])
     objs.append(o)
     # the planner is plain host C++: every binary64 operation rounds as written
     o = os.path.join(BUILD, "planner.o")
-    _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, "planner.cpp"), "-o", o], verbose)
+    cmds.append(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, "planner.cpp"), "-o", o])
     objs.append(o)
+    _run_all(cmds, verbose)
     tmp = LIB + ".tmp"
     _run([hipcc, "-shared", f"--offload-arch={ARCH}", "-o", tmp, *objs], verbose)
     os.replace(tmp, LIB)

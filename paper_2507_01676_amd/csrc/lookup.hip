@@ -38,6 +38,15 @@
 
 #include "device_types.hpp"
 
+// The lookup kernels are compiled in parts so that a build can run the parts in
+// parallel: EMBX_PART 0..3 holds the kernels of one (row type, weighted) pair, part 4
+// the probes, the table filler and the launch code.  Without EMBX_PART one compile
+// holds everything.
+#ifndef EMBX_PART
+#define EMBX_PART -1
+#endif
+#define EMBX_HAS_PART(p) (EMBX_PART < 0 || EMBX_PART == (p))
+
 // address spaces exist in the device pass only; the host pass sees plain pointers
 #if defined(__HIP_DEVICE_COMPILE__)
 #define GMEM __attribute__((address_space(1)))
@@ -846,8 +855,8 @@ __device__ __forceinline__ void combine_chunks(const LookupArgs& a, const DevIte
 // LDS slice: the table (or row chunk [r0, r1)) staged into LDS.  A chunk writes
 // partial sums; the last chunk worker of the batch slice sums them in chunk order.
 template <int G, bool F16, bool W>
-__device__ __attribute__((noinline)) void lds_item(const LookupArgs& a, const DevItem& it, int bs, int be,
-                                                   lchar* smem, LMEM int* s_last) {
+__device__ __forceinline__ void lds_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                         lchar* smem, LMEM int* s_last) {
   const Lane l = lane_of<G>(a.R);
   const DevTable tb = a.tables[it.table];
   stage_linear(smem, as_global(static_cast<const char*>(tb.w)) + it.r0 * a.R, (it.r1 - it.r0) * a.R, l.tid);
@@ -883,8 +892,8 @@ __device__ __attribute__((noinline)) void lds_item(const LookupArgs& a, const De
 // that fall in the chunk; the first chunk stores the partial sums, later chunks add
 // onto them, so a bag's sum is built in chunk order by one SW and needs no combine.
 template <int G, bool F16, bool W>
-__device__ __attribute__((noinline)) void stream_item(const LookupArgs& a, const DevItem& it, int bs, int be,
-                                                      lchar* smem) {
+__device__ __forceinline__ void stream_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                            lchar* smem) {
   const Lane l = lane_of<G>(a.R);
   const DevTable tb = a.tables[it.table];
   const int64_t crow = a.lds_rows / a.R;
@@ -911,8 +920,8 @@ __device__ __attribute__((noinline)) void stream_item(const LookupArgs& a, const
 
 // HOT slice: the C hottest rows and their id hash staged into LDS
 template <int G, bool F16, bool W>
-__device__ __attribute__((noinline)) void hot_item(const LookupArgs& a, const DevItem& it, int bs, int be,
-                                                   lchar* smem) {
+__device__ __forceinline__ void hot_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                         lchar* smem) {
   const Lane l = lane_of<G>(a.R);
   const DevTable tb = a.tables[it.table];
   lchar* meta = smem + a.lds_rows;
@@ -939,9 +948,9 @@ __device__ __attribute__((noinline)) void hot_item(const LookupArgs& a, const De
 
 // one bag gathered straight from HBM by one SW
 template <int G, bool F16, bool W>
-__device__ __attribute__((noinline)) void gather_one_bag(const LookupArgs& a, const RowBase& rb,
-                                                         GMEM const int64_t* off, int b, GMEM float* ob, int64_t ost,
-                                                         int lane_sw, bool mean) {
+__device__ __forceinline__ void gather_one_bag(const LookupArgs& a, const RowBase& rb,
+                                               GMEM const int64_t* off, int b, GMEM float* ob, int64_t ost,
+                                               int lane_sw, bool mean) {
   FGather fg;
   static_cast<RowBase&>(fg) = rb;
   walk<G, F16, W>(as_global(a.indices), off, b, b + 1, ob, ost, lane_sw, mean, fg);
@@ -949,8 +958,8 @@ __device__ __attribute__((noinline)) void gather_one_bag(const LookupArgs& a, co
 
 // DEDUP slice: tiles of whole bags holding at most kTile lookups
 template <int G, bool F16, bool W>
-__device__ __attribute__((noinline)) void dedup_item(const LookupArgs& a, const DevItem& it, int bs, int be,
-                                                     lchar* smem) {
+__device__ __forceinline__ void dedup_item(const LookupArgs& a, const DevItem& it, int bs, int be,
+                                           lchar* smem) {
   const Lane l = lane_of<G>(a.R);
   const DevTable tb = a.tables[it.table];
   GMEM const int64_t* idx = as_global(a.indices);
@@ -1527,6 +1536,7 @@ __global__ void __launch_bounds__(kBlock) lookup_kernel(LookupArgs a) {
   if (tw && (l.tid & (kWave - 1)) == 0) tw[2 + l.wave] = now_ticks();
 }
 
+#if EMBX_HAS_PART(4)
 // ---------------------------------------------------------------- index-handling probes
 
 __global__ void __launch_bounds__(kBlock) dedup_probe_kernel(const int64_t* idx, int n, int32_t* uniq,
@@ -1614,6 +1624,8 @@ __global__ void __launch_bounds__(256) fill_kernel(char* dst, int64_t row_begin,
   }
 }
 
+#endif  // EMBX_HAS_PART(4)
+
 using KernelFn = void (*)(LookupArgs);
 
 template <bool F16, bool STAGED, bool W>
@@ -1630,14 +1642,43 @@ KernelFn pick(int G) {
   }
 }
 
-template <bool W>
-KernelFn pick_w(int G, bool f16, bool staged) {
-  if (f16) return staged ? pick<true, true, W>(G) : pick<true, false, W>(G);
-  return staged ? pick<false, true, W>(G) : pick<false, false, W>(G);
-}
+}  // namespace
 
-KernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
-  return weighted ? pick_w<true>(G, f16, staged) : pick_w<false>(G, f16, staged);
+// The kernel for rows of G lanes, one per (row type, weighted) pair, each defined in
+// its own part.
+using LookupKernelFn = void (*)(LookupArgs);
+LookupKernelFn lookup_kernel_f32(int G, bool staged);
+LookupKernelFn lookup_kernel_f32_weighted(int G, bool staged);
+LookupKernelFn lookup_kernel_f16(int G, bool staged);
+LookupKernelFn lookup_kernel_f16_weighted(int G, bool staged);
+
+#if EMBX_HAS_PART(0)
+LookupKernelFn lookup_kernel_f32(int G, bool staged) {
+  return staged ? pick<false, true, false>(G) : pick<false, false, false>(G);
+}
+#endif
+#if EMBX_HAS_PART(1)
+LookupKernelFn lookup_kernel_f32_weighted(int G, bool staged) {
+  return staged ? pick<false, true, true>(G) : pick<false, false, true>(G);
+}
+#endif
+#if EMBX_HAS_PART(2)
+LookupKernelFn lookup_kernel_f16(int G, bool staged) {
+  return staged ? pick<true, true, false>(G) : pick<true, false, false>(G);
+}
+#endif
+#if EMBX_HAS_PART(3)
+LookupKernelFn lookup_kernel_f16_weighted(int G, bool staged) {
+  return staged ? pick<true, true, true>(G) : pick<true, false, true>(G);
+}
+#endif
+
+#if EMBX_HAS_PART(4)
+namespace {
+
+LookupKernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
+  if (f16) return weighted ? lookup_kernel_f16_weighted(G, staged) : lookup_kernel_f16(G, staged);
+  return weighted ? lookup_kernel_f32_weighted(G, staged) : lookup_kernel_f32(G, staged);
 }
 
 }  // namespace
@@ -1645,7 +1686,7 @@ KernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
 int prepare_lookup_kernels(int lds_bytes) {
   for (int G = 1; G <= 64; G <<= 1) {
     for (int f = 0; f < 4; ++f) {
-      KernelFn k = pick_any(G, (f & 1) != 0, true, (f & 2) != 0);
+      LookupKernelFn k = pick_any(G, (f & 1) != 0, true, (f & 2) != 0);
       if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                               lds_bytes) != hipSuccess)
         return 4;
@@ -1659,7 +1700,7 @@ int prepare_lookup_kernels(int lds_bytes) {
 
 int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
                   void* stream) {
-  KernelFn k = pick_any(G, f16, staged, weighted);
+  LookupKernelFn k = pick_any(G, f16, staged, weighted);
   if (!k) return 2;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kBlock), lds_bytes, static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? 0 : 4;
@@ -1692,5 +1733,7 @@ int launch_fill(void* dst, int64_t row_begin, int64_t n_rows, int E, bool f16, i
                      lo, hi, mode);
   return hipGetLastError() == hipSuccess ? 0 : 4;
 }
+
+#endif  // EMBX_HAS_PART(4)
 
 }  // namespace embx
