@@ -74,18 +74,19 @@ typedef enum {
 } emb_strategy_t;
 
 /* Cost-model coefficients (Eq. (2) extended per strategy), picoseconds.  Layout of
- * emb_plan_options_t.beta: per-item (*0), per-lookup (*1, P, I), per staged byte (S).
+ * emb_plan_options_t.beta: per-item (*0), per-lookup (*1, P, I), per staged byte (S; SH for
+ * the hot rows, which are fetched by id rather than copied as a block).
  *   gather  = G0 + G1*lam
  *   lds     = L0 + S*(rows*R) + L1*lam
  *   chunk   = L0 + S*(rows*R) + I*lam + L1*lam/c
- *   hot     = H0 + S*(C*R) + lam*(P + h*L1 + (1-h)*G1)
+ *   hot     = H0 + SH*(C*R) + lam*(P + h*L1 + (1-h)*G1)
  *   dedup   = D0 + D1*lam + G1*u*lam
  *   stream  = L0 + S*(m*R) + I*lam*c + L1*lam   (c = ceil(m / floor(L / R)), m the table rows)
  * with lam the expected lookups of the slice, R the row bytes, c the chunk count,
  * C the hot rows staged, h the fraction of lookups they catch, u the unique fraction. */
 enum {
   EMB_BETA_G0 = 0, EMB_BETA_G1, EMB_BETA_L0, EMB_BETA_L1, EMB_BETA_S, EMB_BETA_I,
-  EMB_BETA_H0, EMB_BETA_P, EMB_BETA_D0, EMB_BETA_D1, EMB_BETA_COUNT
+  EMB_BETA_H0, EMB_BETA_P, EMB_BETA_D0, EMB_BETA_D1, EMB_BETA_SH, EMB_BETA_COUNT
 };
 
 #define EMB_MAX_HOT_STATS 4096   /* hot rows a table's statistics may list     */

@@ -72,8 +72,8 @@ AUTO = -1
 STRAT_ORDER = (LDS, HOT, DEDUP, GATHER, STREAM)
 
 # beta layout (picoseconds; per item, per lookup, per staged byte)
-G0, G1, L0, L1, S, I, H0, P, D0, D1 = range(10)
-NBETA = 10
+G0, G1, L0, L1, S, I, H0, P, D0, D1, SH = range(11)
+NBETA = 11
 
 MAX_HOT = 4096          # hot rows a table's statistics may list
 MAX_HOT_SLOTS = 2048    # hot rows one HOT item stages at most
@@ -92,8 +92,9 @@ def default_beta(R: int) -> List[float]:
     Measured with every strategy forced in turn on the synthetic workloads with
     R = 256 B rows (uniform, Zipf and single-hot-table mixes); the per-lookup
     terms are latency-bound there and serve unchanged for other row sizes.
-    H0's fit came out negative (it is collinear with S C R, since the staged
-    hot rows C sit at L / R for nearly every sample) and is clipped to 0.
+    HOT (H0, SH, P) and DEDUP (D0, D1) were fitted again, with the other
+    coefficients held, on workloads 1-4 under their own and under fixed queries,
+    which vary the staged hot rows C from 1 to 512.
     """
     del R
     b = [0.0] * NBETA
@@ -103,10 +104,11 @@ def default_beta(R: int) -> List[float]:
     b[L1] = 10950.0
     b[S] = 477.0
     b[I] = 8280.0
-    b[H0] = 0.0
-    b[P] = 2340.0
-    b[D0] = 21600000.0
-    b[D1] = 29400.0
+    b[H0] = 1020000.0
+    b[P] = 2720.0
+    b[D0] = 7260000.0
+    b[D1] = 24080.0
+    b[SH] = 77.0
     return b
 
 
@@ -205,8 +207,8 @@ def cost_chunk(b, mu, R, lam, c):
 
 
 def cost_hot(b, C, R, h, lam):
-    return (_fl(b[H0] + b[S] * float(C * R) + lam * (b[P] + h * b[L1] + (1.0 - h) * b[G1])),
-            _fl(b[H0] + b[S] * float(C * R)))
+    return (_fl(b[H0] + b[SH] * float(C * R) + lam * (b[P] + h * b[L1] + (1.0 - h) * b[G1])),
+            _fl(b[H0] + b[SH] * float(C * R)))
 
 
 def cost_dedup(b, u, lam):

@@ -36,7 +36,7 @@ STRAT_AUTO, STRAT_LDS, STRAT_HOT, STRAT_DEDUP, STRAT_GATHER = -1, 0, 1, 2, 3
 STRATEGY_NAMES = {0: "LDS", 1: "HOT", 2: "DEDUP", 3: "GATHER", 4: "STREAM"}
 POOL_SUM, POOL_MEAN = 0, 1
 POOLING_CODES = {"sum": POOL_SUM, "mean": POOL_MEAN}
-BETA_COUNT = 10
+BETA_COUNT = 11
 MAX_HOT_STATS = 4096
 
 EXPORTED = ["emb_plan_create", "emb_plan_bind_weights", "emb_lookup", "emb_lookup_weighted", "emb_plan_check_errors",
@@ -160,7 +160,8 @@ class _Marshal:
         beta = opts.get("beta")
         if beta is not None:
             b = np.ascontiguousarray(np.asarray(beta, dtype=np.float64))
-            assert b.size == BETA_COUNT
+            if b.size != BETA_COUNT:
+                raise ValueError(f"beta needs {BETA_COUNT} coefficients, got {b.size}")
             self.keep.append(b)
             o.beta = b.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
         force = opts.get("force")

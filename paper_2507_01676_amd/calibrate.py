@@ -7,22 +7,24 @@ workloads with every table forced to one strategy and the per-slice timers of
 ``emb_plan_set_trace`` switched on; the coefficients are the planner's beta
 vector (picoseconds), in the layout of ``include/embx.h``:
 
-    G0 G1 L0 L1 S I H0 P D0 D1
+    G0 G1 L0 L1 S I H0 P D0 D1 SH
 
 and each strategy's cost of one slice with lambda lookups is
 
     GATHER   G0 + G1 lambda
     LDS      L0 + S mu R + L1 lambda                 (mu rows staged)
     chunk    L0 + S mu R + I lambda + L1 lambda / c  (one of c row chunks)
-    HOT      H0 + S C R + lambda (P + h L1 + (1 - h) G1)
+    HOT      H0 + SH C R + lambda (P + h L1 + (1 - h) G1)   (C hot rows staged)
     DEDUP    D0 + D1 lambda + G1 u lambda
 
 Shared coefficients are fitted once and then held fixed: GATHER first (G0,
 G1 from each worker's gather-phase time against its gather slices and
 lookups), LDS next (L0, S, L1 from whole-table slices, then I from what they
 leave of the row-chunk slices' times, so that I also carries the chunk
-combine), then HOT (H0, P) and DEDUP (D0, D1) on what their costs leave after
-the shared terms.
+combine), then HOT (H0, SH, P) and DEDUP (D0, D1) on what their costs leave
+after the shared terms.  HOT has its own per-byte staging term: its rows are
+fetched by id, one row per sub-wavefront, where an LDS slice copies a block, and
+the paper's coefficients differ per strategy in the same way (Sec. III-A).
 Every fit is ``numpy.linalg.lstsq``, constrained to non-negative coefficients
 (an active-set NNLS) when the unconstrained solution has a negative one: the
 coefficients are times, and the planner refuses negative ones.
@@ -42,8 +44,9 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-G0, G1, L0, L1, S, I, H0, P, D0, D1 = range(10)
-NBETA = 10
+G0, G1, L0, L1, S, I, H0, P, D0, D1, SH = range(11)
+NBETA = 11
+BETA_NAMES = ["G0", "G1", "L0", "L1", "S", "I", "H0", "P", "D0", "D1", "SH"]
 LDS, HOT, DEDUP, GATHER = 0, 1, 2, 3
 TICK_PS = 10_000.0          # the kernel timers count a 100 MHz clock
 
@@ -109,9 +112,9 @@ def fit_beta(s: Samples, base: Optional[Sequence[float]] = None) -> List[float]:
         b[I] = float(_lstsq(A, y)[0])
     hot = [x for x in s.slices if x.strat == HOT]
     if hot:
-        A = np.array([[1.0, x.lam] for x in hot])
-        y = np.array([x.ps - b[S] * x.mu * x.R - x.lam * (x.h * b[L1] + (1.0 - x.h) * b[G1]) for x in hot])
-        b[H0], b[P] = (float(v) for v in _lstsq(A, y))
+        A = np.array([[1.0, x.mu * x.R, x.lam] for x in hot])
+        y = np.array([x.ps - x.lam * (x.h * b[L1] + (1.0 - x.h) * b[G1]) for x in hot])
+        b[H0], b[SH], b[P] = (float(v) for v in _lstsq(A, y))
     dd = [x for x in s.slices if x.strat == DEDUP]
     if dd:
         A = np.array([[1.0, x.lam] for x in dd])
@@ -128,7 +131,7 @@ def predict(b: Sequence[float], x) -> float:
         extra = b[I] * x.lam if x.c > 1 else 0.0
         return b[L0] + b[S] * x.mu * x.R + extra + b[L1] * x.lam / x.c
     if x.strat == HOT:
-        return b[H0] + b[S] * x.mu * x.R + x.lam * (b[P] + x.h * b[L1] + (1.0 - x.h) * b[G1])
+        return b[H0] + b[SH] * x.mu * x.R + x.lam * (b[P] + x.h * b[L1] + (1.0 - x.h) * b[G1])
     if x.strat == DEDUP:
         return b[D0] + b[D1] * x.lam + b[G1] * x.u * x.lam
     raise ValueError(x.strat)
@@ -198,15 +201,16 @@ def measure(plan, indices, offsets, batch: int, out, host_offsets: np.ndarray, s
 
 
 def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("gather", "lds", "hot", "dedup"),
-            lds_max_bytes: int = 32 << 20, log=print) -> Samples:
-    """Measures the synthetic workloads with each strategy forced on every table."""
+            lds_max_bytes: int = 32 << 20, log=print, dists: Sequence[str] = ("config",)) -> Samples:
+    """Measures the synthetic workloads with each strategy forced on every table, under
+    each query distribution of ``dists`` (the workload's own, 'uniform', 'fixed')."""
     import torch
     import workloads as W
     from . import Plan, fill_table
     code = {"lds": LDS, "hot": HOT, "dedup": DEDUP, "gather": GATHER}
     allS = Samples()
-    for cfg in configs:
-        c = W.make_config(cfg)
+    for cfg, dist in [(cfg, d) for cfg in configs for d in dists]:
+        c = W.with_distribution(W.make_config(cfg), dist)
         bt = W.gen_batch(c, 0)
         stats = W.history_stats(c)
         dt = torch.float16 if c.dtype == "f16" else torch.float32
@@ -230,7 +234,7 @@ def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("ga
             plan.close()
             if name == "lds":
                 s.workers = []
-            log(f"workload {cfg} {name}: {len(s.slices)} slices, {len(s.workers)} gather workers")
+            log(f"workload {cfg} ({dist} queries) {name}: {len(s.slices)} slices, {len(s.workers)} gather workers")
             allS.slices += s.slices
             allS.workers += s.workers
         del ws
@@ -298,13 +302,22 @@ def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--configs", type=int, nargs="+", default=[2, 3, 4])
     ap.add_argument("--strategies", nargs="+", default=["gather", "lds", "hot", "dedup"])
+    ap.add_argument("--dists", nargs="+", default=["config"],
+                    help="query distributions to measure under (config, uniform, fixed)")
+    ap.add_argument("--base", default=None,
+                    help="JSON object of coefficients (by name) kept where no sample fits them")
     ap.add_argument("--out", default=None, help="write the samples and the fit as JSON")
     ap.add_argument("--report", type=int, nargs="*", default=None,
                     help="re-plan these workloads with the fitted beta and compare predicted and measured makespans")
     a = ap.parse_args(argv)
-    s = collect(a.configs, a.strategies, log=lambda m: print(m, file=sys.stderr, flush=True))
-    b = fit_beta(s)
-    names = ["G0", "G1", "L0", "L1", "S", "I", "H0", "P", "D0", "D1"]
+    s = collect(a.configs, a.strategies, log=lambda m: print(m, file=sys.stderr, flush=True), dists=a.dists)
+    base = None
+    if a.base:
+        with open(a.base) as f:
+            given = json.load(f)
+        base = [float(given.get(n, 0.0)) for n in BETA_NAMES]
+    b = fit_beta(s, base)
+    names = BETA_NAMES
     for st, nm in ((LDS, "LDS"), (HOT, "HOT"), (DEDUP, "DEDUP")):
         xs = [x for x in s.slices if x.strat == st]
         if xs:

@@ -65,8 +65,8 @@ CF cost_chunk(const std::array<double, B_COUNT>& b, int64_t mu, int64_t R, doubl
 }
 CF cost_hot(const std::array<double, B_COUNT>& b, int64_t C, int64_t R, double h, double lam) {
   const double bytes = static_cast<double>(C * R);
-  return {fl(b[B_H0] + b[B_S] * bytes + lam * (b[B_P] + h * b[B_L1] + (1.0 - h) * b[B_G1])),
-          fl(b[B_H0] + b[B_S] * bytes)};
+  return {fl(b[B_H0] + b[B_SH] * bytes + lam * (b[B_P] + h * b[B_L1] + (1.0 - h) * b[B_G1])),
+          fl(b[B_H0] + b[B_SH] * bytes)};
 }
 CF cost_dedup(const std::array<double, B_COUNT>& b, double u, double lam) {
   return {fl(b[B_D0] + b[B_D1] * lam + (b[B_G1] * u) * lam), fl(b[B_D0])};
@@ -252,10 +252,11 @@ std::array<double, B_COUNT> default_beta(int32_t) {
   b[B_L1] = 10950.0;
   b[B_S] = 477.0;
   b[B_I] = 8280.0;
-  b[B_H0] = 0.0;
-  b[B_P] = 2340.0;
-  b[B_D0] = 21600000.0;
-  b[B_D1] = 29400.0;
+  b[B_H0] = 1020000.0;
+  b[B_P] = 2720.0;
+  b[B_D0] = 7260000.0;
+  b[B_D1] = 24080.0;
+  b[B_SH] = 77.0;
   return b;
 }
 

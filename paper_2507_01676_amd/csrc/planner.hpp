@@ -12,7 +12,7 @@
 namespace embx {
 
 enum Strat : int32_t { S_LDS = 0, S_HOT = 1, S_DEDUP = 2, S_GATHER = 3, S_STREAM = 4, S_AUTO = -1 };
-enum BetaIdx { B_G0 = 0, B_G1, B_L0, B_L1, B_S, B_I, B_H0, B_P, B_D0, B_D1, B_COUNT };
+enum BetaIdx { B_G0 = 0, B_G1, B_L0, B_L1, B_S, B_I, B_H0, B_P, B_D0, B_D1, B_SH, B_COUNT };
 
 constexpr int32_t kMaxHotStats = 4096;
 constexpr int32_t kMaxHotSlots = 2048;

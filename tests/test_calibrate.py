@@ -7,7 +7,7 @@ import pytest
 from oracle import plan as OPL
 from paper_2507_01676_amd import calibrate as CAL
 
-BETA_TRUE = [350_000.0, 9_000.0, 2_500_000.0, 900.0, 45.0, 300.0, 8_000_000.0, 1_200.0, 17_000_000.0, 28_000.0]
+BETA_TRUE = [350_000.0, 9_000.0, 2_500_000.0, 900.0, 45.0, 300.0, 8_000_000.0, 1_200.0, 17_000_000.0, 28_000.0, 11.0]
 
 
 def _samples(g, noise=0.0, n=400):
@@ -71,7 +71,7 @@ def test_unsampled_strategies_keep_the_base_value():
     g = np.random.default_rng(3)
     s = _samples(g)
     s.slices = [x for x in s.slices if x.strat != CAL.DEDUP]
-    base = [float(i) for i in range(10)]
+    base = [float(i) for i in range(CAL.NBETA)]
     b = CAL.fit_beta(s, base)
     assert b[CAL.D0] == 8.0 and b[CAL.D1] == 9.0
     assert b[CAL.G1] == pytest.approx(BETA_TRUE[CAL.G1], rel=1e-5)

@@ -31,6 +31,7 @@ def _roofline_beta(R=256):
     b[OPL.G0], b[OPL.G1] = 200000.0, R * 32.0 / 0.7
     b[OPL.L0], b[OPL.L1], b[OPL.S], b[OPL.I] = 200000.0, R / 0.3072, 32.0, 256.0
     b[OPL.H0], b[OPL.P], b[OPL.D0], b[OPL.D1] = 200000.0, 100.0, 200000.0, 4000.0
+    b[OPL.SH] = 32.0
     return b
 
 
@@ -48,10 +49,12 @@ def test_cost_formulas_coincide_where_strategies_do():
     bz[OPL.P] = 0.0
     bz[OPL.H0] = bz[OPL.G0]
     hot0, fx = OPL.cost_hot(bz, 100, R, 0.0, lam)
-    assert abs(hot0 - (g1 + b[OPL.S] * 100 * R)) <= 1 and fx == math.floor(bz[OPL.G0] + b[OPL.S] * 100 * R)
-    # a hot set that catches everything with a free probe is an LDS table of C rows
+    assert abs(hot0 - (g1 + b[OPL.SH] * 100 * R)) <= 1 and fx == math.floor(bz[OPL.G0] + b[OPL.SH] * 100 * R)
+    # a hot set that catches everything with a free probe, staged at the LDS byte
+    # cost, is an LDS table of C rows
     bl = list(bz)
     bl[OPL.H0] = bl[OPL.L0]
+    bl[OPL.SH] = bl[OPL.S]
     hot1, _ = OPL.cost_hot(bl, 100, R, 1.0, lam)
     lds, _ = OPL.cost_lds(bl, 100, R, lam)
     assert abs(hot1 - lds) <= 1
