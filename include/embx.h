@@ -205,6 +205,12 @@ emb_status_t emb_plan_text(int32_t num_tables, const int64_t* rows, int32_t embe
                            int32_t num_workers, const emb_plan_options_t* opts, char* buf,
                            size_t cap, size_t* len_out);
 
+/* The built-in cost coefficients (the MI355X fit of Eq. (2), Sec. III-A) used when
+ * emb_plan_options_t.beta is NULL, for rows of row_bytes bytes: writes EMB_BETA_COUNT
+ * picosecond values to out (host, n >= EMB_BETA_COUNT entries).  Host only.
+ * EMB_ERR_INVALID_ARGUMENT if out is NULL, n is too small or row_bytes < 1. */
+emb_status_t emb_default_beta(int32_t row_bytes, double* out, int32_t n);
+
 const char* emb_status_string(emb_status_t s);
 
 /* ---- index-handling probes (tests of the exact integer work) ---------------------------

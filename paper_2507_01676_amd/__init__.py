@@ -42,7 +42,7 @@ MAX_HOT_STATS = 4096
 EXPORTED = ["emb_plan_create", "emb_plan_bind_weights", "emb_lookup", "emb_lookup_weighted", "emb_plan_check_errors",
             "emb_plan_serialize", "emb_plan_get_info", "emb_plan_destroy", "emb_plan_text",
             "emb_status_string", "emb_debug_dedup_tile", "emb_debug_hot_probe", "embx_fill_table",
-            "emb_plan_set_trace"]
+            "emb_plan_set_trace", "emb_default_beta"]
 
 
 class EmbxError(RuntimeError):
@@ -89,6 +89,7 @@ _lib.emb_plan_destroy.argtypes = [_vp]
 _lib.emb_plan_text.argtypes = [_i32, ctypes.POINTER(_i64), _i32, _i32, ctypes.POINTER(_Stats), _i32, _i32,
                                ctypes.POINTER(_Opts), ctypes.c_char_p, _sz, ctypes.POINTER(_sz)]
 _lib.emb_plan_set_trace.argtypes = [_vp, _vp, _sz, ctypes.POINTER(_sz)]
+_lib.emb_default_beta.argtypes = [_i32, ctypes.POINTER(ctypes.c_double), _i32]
 _lib.emb_debug_dedup_tile.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
 _lib.emb_debug_hot_probe.argtypes = [_vp, _i32, _vp, _i32, _vp, _vp]
 _lib.embx_fill_table.argtypes = [_vp, _i64, _i64, _i32, _i32, _i32, ctypes.c_uint64, ctypes.c_double,
@@ -188,6 +189,14 @@ def _stream_ptr(stream) -> Optional[int]:
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
+
+
+def default_beta(row_bytes: int) -> List[float]:
+    """The built-in cost coefficients (picoseconds, layout of ``include/embx.h``) the
+    planner uses for rows of ``row_bytes`` bytes when no beta is given."""
+    out = (ctypes.c_double * BETA_COUNT)()
+    _check(_lib.emb_default_beta(int(row_bytes), out, BETA_COUNT), "emb_default_beta")
+    return [float(x) for x in out]
 
 
 def plan_text(rows: Sequence[int], E: int, dtype, stats, max_batch: int, num_workers: int, **opts) -> str:

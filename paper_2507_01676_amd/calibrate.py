@@ -305,14 +305,18 @@ def main(argv=None) -> int:
     ap.add_argument("--dists", nargs="+", default=["config"],
                     help="query distributions to measure under (config, uniform, fixed)")
     ap.add_argument("--base", default=None,
-                    help="JSON object of coefficients (by name) kept where no sample fits them")
+                    help="coefficients kept where no sample fits them: 'builtin' (the library's own), "
+                         "or a JSON file of {name: value}")
     ap.add_argument("--out", default=None, help="write the samples and the fit as JSON")
     ap.add_argument("--report", type=int, nargs="*", default=None,
                     help="re-plan these workloads with the fitted beta and compare predicted and measured makespans")
     a = ap.parse_args(argv)
     s = collect(a.configs, a.strategies, log=lambda m: print(m, file=sys.stderr, flush=True), dists=a.dists)
     base = None
-    if a.base:
+    if a.base == "builtin":
+        from . import default_beta
+        base = default_beta(256)
+    elif a.base:
         with open(a.base) as f:
             given = json.load(f)
         base = [float(given.get(n, 0.0)) for n in BETA_NAMES]

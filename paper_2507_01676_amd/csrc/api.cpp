@@ -145,6 +145,16 @@ emb_status_t emb_plan_text(int32_t num_tables, const int64_t* rows, int32_t embe
   return write_text(plan_text(out), buf, cap, len_out);
 }
 
+static_assert(static_cast<int>(B_COUNT) == static_cast<int>(EMB_BETA_COUNT),
+              "the planner's coefficient layout is the one include/embx.h publishes");
+
+emb_status_t emb_default_beta(int32_t row_bytes, double* out, int32_t n) {
+  if (!out || n < B_COUNT || row_bytes < 1) return EMB_ERR_INVALID_ARGUMENT;
+  const std::array<double, B_COUNT> b = default_beta(row_bytes);
+  for (int i = 0; i < B_COUNT; ++i) out[i] = b[i];
+  return EMB_OK;
+}
+
 emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows, int32_t embedding_dim,
                              emb_dtype_t dtype, const emb_table_stats_t* stats, int32_t max_batch,
                              const emb_plan_options_t* opts) {

@@ -35,6 +35,19 @@ def test_library_exports_every_declared_symbol():
     assert embx.status_string(embx.ERR_NOT_BOUND) == "weights not bound"
 
 
+def test_builtin_coefficients_equal_the_oracles():
+    """The library's built-in beta (emb_default_beta) is the oracle's, entry by entry,
+    and the binding rejects a beta of the wrong length."""
+    embx = _lib()
+    for R in (16, 128, 256, 512, 1024):
+        assert embx.default_beta(R) == OPL.default_beta(R)
+    with pytest.raises(embx.EmbxError):
+        embx.default_beta(0)
+    with pytest.raises(ValueError):
+        embx.plan_text([10], 4, "f32", [dict(mean_pooling=1.0, max_pooling=1, hot_rows=[], hot_freq=[],
+                                              unique_frac=1.0)], 8, 2, beta=[1.0] * (embx.BETA_COUNT - 1))
+
+
 def _cpp(rows, E, dtype, stats, B, K, opts: OPL.Options):
     embx = _lib()
     cst = [dict(mean_pooling=s.mean_pooling, max_pooling=s.max_pooling,
