@@ -181,6 +181,8 @@ def main():
     ap.add_argument("--dist", choices=list(W.DISTRIBUTIONS), default="config",
                     help="query distribution of every table: the workload's own, uniform, or fixed "
                          "(every lookup of a table on one row)")
+    ap.add_argument("--lif-milli", type=int, default=0,
+                    help="load-imbalance threshold x 1000 of the symmetric fallback (0: the library default)")
     ap.add_argument("--sym-max", type=int, default=0,
                     help="gather tables split over all workers while at most this many (0: the library default)")
     args = ap.parse_args()
@@ -227,6 +229,8 @@ def main():
         opts["pooling"] = args.pooling
     if args.sym_max:
         opts["sym_max"] = args.sym_max
+    if args.lif_milli:
+        opts["lif_milli"] = args.lif_milli
     tp = time.time()
     plan = embx.Plan(c.rows, c.E, c.dtype, stats, c.batch, **opts).bind(weights)
     plan_ms = (time.time() - tp) * 1e3

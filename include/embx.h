@@ -108,7 +108,7 @@ typedef struct {
   int32_t wg_per_cu;        /* workers per CU; 0 -> 1.  K = CUs * wg_per_cu unless num_workers   */
   int32_t lds_budget_bytes; /* L, LDS bytes for staged rows per worker; 0 -> 131072 (capped by
                                the device's LDS per workgroup minus a 28 KiB metadata reserve)   */
-  int32_t lif_milli;        /* LIF threshold x 1000 (Sec. III-B step 4); 0 -> 1250               */
+  int32_t lif_milli;        /* LIF threshold x 1000 (Sec. III-B step 4); 0 -> 1500               */
   int32_t order_mode;       /* 0 = longest first with the paper's keys as tie-breaks;
                                1 = the paper's order (s desc, m asc)                             */
   int64_t chunk_max_bytes;  /* max row-chunk bytes (Sec. III-B); <= 0 -> lds_budget_bytes      */

@@ -127,7 +127,7 @@ class Stat:
 @dataclass
 class Options:
     lds_budget: int = 131072
-    lif_milli: int = 1250
+    lif_milli: int = 1500
     chunk_max_bytes: int = 0          # <= 0 -> lds_budget
     order_mode: int = 0
     beta: Optional[Sequence[float]] = None

@@ -34,7 +34,7 @@ struct PlanIn {
   int32_t B = 0;            // max batch
   int32_t K = 0;            // workers
   int64_t L = 131072;       // LDS budget for rows
-  int32_t lif_milli = 1250;
+  int32_t lif_milli = 1500;
   int64_t chunk_max = 0;    // <= 0 -> L
   int32_t order_mode = 0;
   std::array<double, B_COUNT> beta{};
