@@ -168,7 +168,8 @@ class _Marshal:
         force = opts.get("force")
         if force is not None:
             f = np.ascontiguousarray(np.asarray(force, dtype=np.int32))
-            assert f.size == T
+            if f.size != T:
+                raise ValueError(f"force needs one strategy per table ({T}), got {f.size}")
             self.keep.append(f)
             o.force_strategy = f.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
         pooling = opts.get("pooling")
@@ -176,7 +177,8 @@ class _Marshal:
             if isinstance(pooling, (str, int)):
                 pooling = [pooling] * T
             pc = np.ascontiguousarray(np.asarray([POOLING_CODES.get(x, x) for x in pooling], dtype=np.int32))
-            assert pc.size == T
+            if pc.size != T:
+                raise ValueError(f"pooling needs one reduction per table ({T}), got {pc.size}")
             self.keep.append(pc)
             o.pooling = pc.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
         self.opts = o
@@ -231,7 +233,8 @@ class Plan:
 
     def bind(self, weights: List) -> "Plan":
         import torch
-        assert len(weights) == self.T
+        if len(weights) != self.T:
+            raise ValueError(f"bind needs one table per plan table ({self.T}), got {len(weights)}")
         want = torch.float16 if self.dtype == DTYPE_F16 else torch.float32
         for w in weights:
             if not (w.is_cuda and w.dtype == want and w.dim() == 2 and w.shape[1] == self.E and w.is_contiguous()):
@@ -247,14 +250,21 @@ class Plan:
         import torch
         if out is None:
             out = torch.empty((batch, self.T, self.E), dtype=torch.float32, device=indices.device)
-        assert indices.dtype == torch.int64 and offsets.dtype == torch.int64 and out.dtype == torch.float32
-        assert out.is_contiguous() and out.numel() >= batch * self.T * self.E
-        assert offsets.numel() >= self.T * batch + 1
+        for name, x, dt in (("indices", indices, torch.int64), ("offsets", offsets, torch.int64),
+                            ("out", out, torch.float32)):
+            if not (x.is_cuda and x.dtype == dt and x.is_contiguous()):
+                raise ValueError(f"{name} must be a contiguous {dt} device tensor")
+        if out.numel() < batch * self.T * self.E:
+            raise ValueError(f"out holds {out.numel()} elements, the batch needs {batch * self.T * self.E}")
+        if offsets.numel() < self.T * batch + 1:
+            raise ValueError(f"offsets holds {offsets.numel()} entries, the batch needs {self.T * batch + 1}")
         if weights is None:
             _check(_lib.emb_lookup(self._h, indices.data_ptr(), offsets.data_ptr(), int(batch), out.data_ptr(),
                                    _stream_ptr(stream)), "emb_lookup")
         else:
-            assert weights.dtype == torch.float32 and weights.is_contiguous() and weights.numel() >= indices.numel()
+            if not (weights.is_cuda and weights.dtype == torch.float32 and weights.is_contiguous()
+                    and weights.numel() >= indices.numel()):
+                raise ValueError("weights must be a contiguous fp32 device tensor with one weight per index")
             _check(_lib.emb_lookup_weighted(self._h, indices.data_ptr(), offsets.data_ptr(), weights.data_ptr(),
                                             int(batch), out.data_ptr(), _stream_ptr(stream)), "emb_lookup_weighted")
         return out
@@ -329,7 +339,8 @@ def fill_table(w, table_id: int, seed: int, lo: float = -0.05, hi: float = 0.05,
                row_begin: int = 0, stream=None):
     """Fills device tensor ``w`` [n, E] with rows [row_begin, row_begin+n) of the synthetic table."""
     import torch
-    assert w.is_cuda and w.is_contiguous() and w.dim() == 2
+    if not (w.is_cuda and w.is_contiguous() and w.dim() == 2 and w.dtype in (torch.float16, torch.float32)):
+        raise ValueError("fill_table needs a contiguous 2-D fp16 or fp32 device tensor")
     dt = DTYPE_F16 if w.dtype == torch.float16 else DTYPE_F32
     _check(_lib.embx_fill_table(w.data_ptr(), int(row_begin), int(w.shape[0]), int(w.shape[1]), dt, int(table_id),
                                 int(seed) & ((1 << 64) - 1), float(lo), float(hi), int(mode), _stream_ptr(stream)),

@@ -263,3 +263,35 @@ def test_many_tables_placed_whole(gpu):
     assert nbad == 0
     ks = [int(ln.split()[8]) for ln in p.serialize().splitlines() if ln.startswith("item ")]
     assert ks.count(1) > 100 and max(ks) <= p.info()["num_workers"]
+
+
+def test_binding_rejects_bad_tensors_before_launch(gpu):
+    """Undersized, mistyped, non-contiguous or host tensors are refused on the host (no
+    launch): the kernel trusts the sizes it is given."""
+    import torch
+    c = mixed_config(108, 64, "f32", rows=[100, 200], B=16)
+    batch = W.gen_batch(c, 0)
+    p = plan_for(c, 16).bind(upload_tables(host_tables(c)))
+    idx, off = to_device(batch)
+    B = batch.B
+    good = torch.empty((B, c.T, c.E), device="cuda")
+    bad = [
+        dict(out=torch.empty((B - 1, c.T, c.E), device="cuda")),                     # too small
+        dict(out=torch.empty((B, c.T, c.E), device="cuda", dtype=torch.float16)),    # wrong dtype
+        dict(out=torch.empty((c.E, c.T, B), device="cuda").permute(2, 1, 0)),         # not contiguous
+        dict(idx=idx.to(torch.int32)),
+        dict(idx=idx.cpu()),
+        dict(off=off[:-1]),
+        dict(weights=torch.ones(idx.numel() - 1, device="cuda")),
+        dict(weights=torch.ones(idx.numel(), device="cuda", dtype=torch.float64)),
+    ]
+    for case in bad:
+        with pytest.raises(ValueError):
+            p.lookup(case.get("idx", idx), case.get("off", off), B, case.get("out", good), weights=case.get("weights"))
+    with pytest.raises(ValueError):
+        p.bind(upload_tables(host_tables(c))[:1])
+    torch.cuda.synchronize()
+    assert p.check_errors() == 0
+    got = p.lookup(idx, off, B, good)                                               # still usable
+    torch.cuda.synchronize()
+    check_full(got.cpu().numpy(), host_tables(c), batch, "f32")
