@@ -20,7 +20,9 @@ R distinct batches are cycled.  Prints ONE JSON line:
                    launch (profiles/traffic_<workload>.json: FETCH_SIZE and WRITE_SIZE, each
                    scaled by its reading for a 1 GiB device copy) when the committed counters
                    were taken on this kernel source, else null
-  cpu_baseline     the CPU oracle timed on a bounded sample of the same workload
+  cpu_baseline     the CPU oracle timed on a bounded sample of the same workload; beside it
+                   (torch_embedding_bag) torch's CPU embedding_bag on the same sample, with
+                   the threads it used, for unweighted runs
 
   python bench.py [--config 2] [--steps 200] [--warmup 20]
 """
@@ -126,9 +128,42 @@ def cpu_baseline(c: W.Config, batches, budget_s: float, pooling: str = "sum", ps
     tot = sum(lat)
     sample = (f"{'all' if len(keep) == c.T else len(keep)} of {c.T} tables, {Bs}-query batches, "
               f"{i} batches cycled over {len(subs)} distinct")
-    return {"value": n_look / tot, "unit": "lookups/s", "cores": 1, "kind": "oracle", "sample": sample,
-            "queries_per_s": Bs * i / tot, "p99_us": p99(lat) * 1e6, "cpu_model": cpu_model(),
-            "cpu_count": os.cpu_count()}
+    res = {"value": n_look / tot, "unit": "lookups/s", "cores": 1, "kind": "oracle", "sample": sample,
+           "queries_per_s": Bs * i / tot, "p99_us": p99(lat) * 1e6, "cpu_model": cpu_model(),
+           "cpu_count": os.cpu_count()}
+    if psw is None:
+        res["torch_embedding_bag"] = torch_cpu_reference(weights, subs, Bs, budget_s / 2, pooling)
+    return res
+
+
+def torch_cpu_reference(weights, subs, Bs: int, budget_s: float, pooling: str):
+    """A second CPU reference on the same sample: torch.nn.functional.embedding_bag per
+    table (fp32, torch's own thread pool), timed like the oracle."""
+    import torch
+    import torch.nn.functional as F
+    tw = [torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)) for w in weights]
+    T = len(tw)
+    prepared = []
+    for idx, off, _ in subs:
+        ti = torch.from_numpy(idx)
+        starts = [torch.from_numpy(off[t * Bs:(t + 1) * Bs] - off[t * Bs]) for t in range(T)]
+        prepared.append((ti, [(int(off[t * Bs]), int(off[(t + 1) * Bs])) for t in range(T)], starts, int(off[-1])))
+    lat, n_look, i = [], 0, 0
+    start = time.perf_counter()
+    while True:
+        ti, spans, starts, n = prepared[i % len(prepared)]
+        t1 = time.perf_counter()
+        out = torch.stack([F.embedding_bag(ti[a:b], tw[t], starts[t], mode=pooling)
+                           for t, (a, b) in enumerate(spans)], dim=1)
+        lat.append(time.perf_counter() - t1)
+        del out
+        n_look += n
+        i += 1
+        if (time.perf_counter() - start >= budget_s and i >= 3) or i >= 1000:
+            break
+    tot = sum(lat)
+    return {"value": n_look / tot, "unit": "lookups/s", "threads": torch.get_num_threads(),
+            "queries_per_s": Bs * i / tot, "p99_us": p99(lat) * 1e6, "batches": i}
 
 
 def copy_bandwidth_gbps() -> float:
