@@ -20,6 +20,8 @@ R distinct batches are cycled.  Prints ONE JSON line:
                    launch (profiles/traffic_<workload>.json: FETCH_SIZE and WRITE_SIZE, each
                    scaled by its reading for a 1 GiB device copy) when the committed counters
                    were taken on this kernel source, else null
+  launch_floor_us  back-to-back interval of a one-workgroup kernel launched through the same
+                   ctypes path and stream (the floor of launch_us)
   cpu_baseline     the CPU oracle timed on a bounded sample of the same workload; beside it
                    (torch_embedding_bag) torch's CPU embedding_bag on the same sample, with
                    the threads it used, for unweighted runs
@@ -183,6 +185,31 @@ def copy_bandwidth_gbps() -> float:
     ms = e0.elapsed_time(e1) / 10
     del a, b
     return 2 * n / (ms * 1e-3) / 1e9
+
+
+def launch_floor_us(stream) -> float:
+    """Back-to-back interval of a near-empty kernel (the library's table filler on one
+    row of 4 floats: one workgroup) launched through the same ctypes path and stream as
+    the timed lookups: the per-launch cost that no launch of this loop goes below."""
+    import torch
+    import paper_2507_01676_amd as embx
+    x = torch.empty((1, 4), device="cuda")
+    ptr, sp = x.data_ptr(), stream.cuda_stream
+    fill = embx._lib.embx_fill_table
+
+    def launch():
+        if fill(ptr, 0, 1, 4, embx.DTYPE_F32, 0, 1, 0.0, 1.0, 0, sp) != 0:
+            raise RuntimeError("embx_fill_table failed")
+    for _ in range(20):
+        launch()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(500):
+        launch()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / 500
 
 
 def load_traffic(workload: str, src_hash: str):
@@ -352,6 +379,7 @@ def main():
     traffic = load_traffic(workload + variant, src_hash)
 
     copy_gbps = None if args.no_copy else copy_bandwidth_gbps()
+    floor_us = launch_floor_us(stream)
     cpu = None
     if not args.no_cpu:
         log("timing the CPU oracle")
@@ -388,6 +416,7 @@ def main():
         "p99_batches": len(lat_ms),
         "cold_cache": cold,
         "copy_gbps": copy_gbps,
+        "launch_floor_us": floor_us,
         "plan": {"strategies": info["n_strategy"], "items": info["num_items"], "lif_milli": info["lif_milli"],
                  "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms},
         "kernel_source_hash": src_hash,
