@@ -113,7 +113,7 @@ typedef struct {
                                1 = the paper's order (s desc, m asc)                             */
   int64_t chunk_max_bytes;  /* max row-chunk bytes (Sec. III-B); <= 0 -> lds_budget_bytes      */
   const double* beta;       /* host, EMB_BETA_COUNT finite non-negative coefficients (picoseconds);
-                               NULL -> built-in MI355X fit; a negative one is an invalid argument  */
+                               NULL -> built-in MI355X fit (emb_default_beta); negative: invalid */
   const int32_t* force_strategy; /* host, T entries of emb_strategy_t, or NULL (all AUTO)        */
   int32_t num_workers;      /* > 0 overrides K (must not exceed 65535)                          */
   int32_t sym_max_gather;   /* 0: a GATHER table is split over all workers (symmetric partitioning,
