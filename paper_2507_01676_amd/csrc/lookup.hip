@@ -139,11 +139,24 @@ __device__ __forceinline__ void acc_add_f32(Acc<F16>& a, GMEM const float* p) {
   }
 }
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// Pooled outputs are written once and not read again by the launch: they are stored
+// with the non-temporal hint (nt), so that they neither displace table rows in L2 nor
+// leave dirty lines for the write-back at the end of the kernel.  Partial sums that are
+// read back (row-chunk slabs, STREAM's running sums) are stored normally (nt = false).
 template <bool F16>
-__device__ __forceinline__ void acc_store(GMEM float* p, const Acc<F16>& a) {
+__device__ __forceinline__ void acc_store(GMEM float* p, const Acc<F16>& a, bool nt = true) {
 #pragma unroll
-  for (int h = 0; h < (F16 ? 2 : 1); ++h)
-    *reinterpret_cast<GMEM float4*>(p + 4 * h) = make_float4(a.v[4 * h], a.v[4 * h + 1], a.v[4 * h + 2], a.v[4 * h + 3]);
+  for (int h = 0; h < (F16 ? 2 : 1); ++h) {
+    const f32x4 v = {a.v[4 * h], a.v[4 * h + 1], a.v[4 * h + 2], a.v[4 * h + 3]};
+    GMEM f32x4* q = reinterpret_cast<GMEM f32x4*>(p + 4 * h);
+    if (nt)
+      __builtin_nontemporal_store(v, q);
+    else
+      *q = v;
+  }
 }
 
 // sum of the S = 64/G sub-wavefront partials of a wavefront (xor butterflies)
@@ -204,6 +217,7 @@ struct RowBase {
   gchar* zero;            // R zero bytes (+ lane_c): what an invalid id (or a position past the end) reads
   float one;              // 1.0f from the launch arguments (see acc_add)
   GMEM const float* wts;  // per-lookup weights (weighted launches)
+  bool nt;                // outputs are final: store them non-temporally (see acc_store)
   __device__ __forceinline__ void bad() const {
     if (count) atomicAdd(err, 1ull);
   }
@@ -491,7 +505,7 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
             if (add && f.active) acc_add_f32(acc, ob + static_cast<int64_t>(b) * ostride);
             if (mean) acc_mean(acc, bag_end - bstart);
             bstart = bag_end;
-            if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+            if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc, f.nt);
             acc_zero(acc);
             ++b;
             bag_end = end_of(b);
@@ -515,7 +529,7 @@ __device__ __forceinline__ void walk_seq(GMEM const int64_t* __restrict__ indice
       if (add && f.active) acc_add_f32(acc, ob + static_cast<int64_t>(b) * ostride);
       if (mean) acc_mean(acc, pend - bstart);
       bstart = pend;
-      if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+      if (f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc, f.nt);
       acc_zero(acc);
     }
     if (!has_nxt) break;
@@ -581,7 +595,7 @@ __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indic
     Acc<F16> z;
     acc_zero(z);
     for (int b = bs; b < be; ++b)
-      if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, z);
+      if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, z, f.nt);
     return;
   }
   auto off_of = [&](int bb) -> int64_t {   // bb - wb in [0, 128)
@@ -626,7 +640,7 @@ __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indic
     if (lastq) {
       acc_wave_reduce<G>(acc);
       if (mean) acc_mean(acc, p1 - bstart);
-      if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc);
+      if (sw_w == 0 && f.active) acc_store(ob + static_cast<int64_t>(b) * ostride, acc, f.nt);
       acc_zero(acc);
       bstart = qbn;
     }
@@ -803,6 +817,7 @@ __device__ __forceinline__ RowBase row_base(const LookupArgs& a, const DevTable&
   rb.zero = as_global(static_cast<const char*>(a.zero_row));
   rb.one = a.one;
   rb.wts = as_global(a.weights);
+  rb.nt = true;
   return rb;
 }
 
@@ -872,7 +887,9 @@ __device__ __forceinline__ void lds_item(const LookupArgs& a, const DevItem& it,
                          static_cast<int64_t>(a.T) * a.E, it.mean != 0, f);
     return;
   }
-  // a chunk's partial sums are never averaged: the combine divides the total
+  // a chunk's partial sums are never averaged: the combine divides the total; the
+  // last chunk worker reads them back, so they stay cached
+  f.nt = false;
   run_slice<G, F16, W>(a, it, l, bs, be,
                        as_global(a.partials) + tb.part_base + static_cast<int64_t>(it.chunk) * a.Bmax * a.E, a.E,
                        false, f);
@@ -913,7 +930,8 @@ __device__ __forceinline__ void stream_item(const LookupArgs& a, const DevItem& 
     __syncthreads();
     f.r0 = static_cast<int32_t>(r0);
     f.r1 = static_cast<int32_t>(r1);
-    f.count = r0 == 0;   // each invalid id is counted once
+    f.count = r0 == 0;     // each invalid id is counted once
+    f.nt = r1 == tb.rows;  // the sums before the last chunk are read back by the next
     walk<G, F16, W>(idx, off, lo, hi, ob, ost, l.lane_sw, it.mean != 0 && r1 == tb.rows, f, r0 > 0);
   }
 }
@@ -1173,7 +1191,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
     for (; b < be; ++b, obb += ostride) {
       if (mean) acc_mean(acc, pend - bstart);
       bstart = pend;
-      if (f.active) acc_store(obb, acc);
+      if (f.active) acc_store(obb, acc, f.nt);
       acc_zero(acc);
     }
   };
@@ -1228,7 +1246,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
         if ((fs >> u) & 1u) {
           if (mean) acc_mean(acc, p + u - bstart);
           bstart = p + u;
-          acc_store(obb, acc);
+          acc_store(obb, acc, f.nt);
           acc_zero(acc);
           obb += ostride;
         }
@@ -1243,7 +1261,7 @@ __device__ __forceinline__ void walk_stream(GMEM const int64_t* __restrict__ ind
         while (u < n && e == p + u) {
           if (mean) acc_mean(acc, e - bstart);
           bstart = e;
-          if (f.active) acc_store(obb, acc);
+          if (f.active) acc_store(obb, acc, f.nt);
           acc_zero(acc);
           ++b;
           obb += ostride;
@@ -1340,7 +1358,8 @@ __device__ __forceinline__ void store_row(GMEM float* p, const uint4 r, float wt
     }
     acc_store(p, a);
   } else {
-    *reinterpret_cast<GMEM uint4*>(p) = r;   // fp32 rows are their own output (bit for bit)
+    const u32x4 v = {r.x, r.y, r.z, r.w};   // fp32 rows are their own output (bit for bit)
+    __builtin_nontemporal_store(v, reinterpret_cast<GMEM u32x4*>(p));
   }
 }
 
