@@ -295,3 +295,17 @@ def test_binding_rejects_bad_tensors_before_launch(gpu):
     got = p.lookup(idx, off, B, good)                                               # still usable
     torch.cuda.synchronize()
     check_full(got.cpu().numpy(), host_tables(c), batch, "f32")
+
+
+def test_more_gather_slices_per_worker_than_lds_holds_is_refused(gpu):
+    """A worker's gather run queue lives in LDS (at most 1024 runs): 1,100 tables that are
+    each split over all workers are refused with EMB_ERR_UNSUPPORTED at plan creation,
+    and placing them whole (sym_max < 0) plans them."""
+    T = 1100
+    stats = [dict(mean_pooling=20.0, max_pooling=40, hot_rows=[], hot_freq=[], unique_frac=1.0)] * T
+    with pytest.raises(gpu.EmbxError) as e:
+        gpu.Plan([100000] * T, 64, "f32", stats, 4096)
+    assert e.value.code == gpu.ERR_UNSUPPORTED
+    p = gpu.Plan([100000] * T, 64, "f32", stats, 4096, sym_max=-1)
+    assert p.info()["num_items"] >= T
+    p.close()
