@@ -144,9 +144,9 @@ typedef struct {
  * K, I, L).  Host-side work plus one upload of the plan's metadata; allocates the device
  * workspace for row-chunk partial sums.  rows[t] in [1, 2^31); E a multiple of 4 (fp32) or
  * 8 (fp16), E <= 256; opts may be NULL.  On success *plan_out owns everything it allocated.
- * EMB_ERR_UNSUPPORTED when a worker would hold more than 1024 gather slices (its run queue
- * lives in LDS): with every table split over all workers that is T > 1024 tables; such
- * plans need sym_max_gather < 0 (tables placed whole) or fewer workers per table. */
+ * EMB_ERR_UNSUPPORTED when a worker would hold more gather slices than its run queue in
+ * LDS takes (48 B each, about 3,400 in 160 KiB): with every table split over all workers,
+ * more than ~3,400 tables; such plans need sym_max_gather < 0 (tables placed whole). */
 emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows,
                              int32_t embedding_dim, emb_dtype_t dtype,
                              const emb_table_stats_t* stats, int32_t max_batch,

@@ -389,8 +389,11 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
           nrun[cls] += 1;
         }
       }
+      // the worker's header and runs are copied into LDS (all of a workgroup's LDS but
+      // the kernel's own static variables)
+      const int64_t run_cap = (smem - kStaticLdsReserve) / static_cast<int64_t>(sizeof(GatherRun)) - 1;
       if (base[0] > INT32_MAX || base[1] > INT32_MAX || base[2] > INT32_MAX ||
-          nrun[0] + nrun[1] + nrun[2] > kMaxRunsPerWorker) {
+          nrun[0] + nrun[1] + nrun[2] > run_cap) {
         delete p;
         return EMB_ERR_UNSUPPORTED;
       }

@@ -58,7 +58,7 @@ struct GatherSlotHeader {
   int32_t pad[6];
 };
 static_assert(sizeof(GatherSlotHeader) == sizeof(GatherRun), "a slot header takes one run record");
-constexpr int kMaxRunsPerWorker = 1024;   // a worker's gather runs held in LDS at once
+constexpr int kStaticLdsReserve = 1024;   // LDS kept for the kernel's static variables
 constexpr int kChunkSingle = 8;           // bags per chunk of a single-lookup-bag run (one SW step)
 
 struct LookupArgs {

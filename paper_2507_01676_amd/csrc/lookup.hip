@@ -1703,9 +1703,11 @@ LookupKernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
 }  // namespace
 
 int prepare_lookup_kernels(int lds_bytes) {
+  // staged kernels hold rows and metadata; gather-only ones the worker's run queue,
+  // which may also pass the default 64 KiB
   for (int G = 1; G <= 64; G <<= 1) {
-    for (int f = 0; f < 4; ++f) {
-      LookupKernelFn k = pick_any(G, (f & 1) != 0, true, (f & 2) != 0);
+    for (int f = 0; f < 8; ++f) {
+      LookupKernelFn k = pick_any(G, (f & 1) != 0, (f & 4) == 0, (f & 2) != 0);
       if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
                               lds_bytes) != hipSuccess)
         return 4;

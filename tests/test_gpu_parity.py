@@ -298,10 +298,10 @@ def test_binding_rejects_bad_tensors_before_launch(gpu):
 
 
 def test_more_gather_slices_per_worker_than_lds_holds_is_refused(gpu):
-    """A worker's gather run queue lives in LDS (at most 1024 runs): 1,100 tables that are
-    each split over all workers are refused with EMB_ERR_UNSUPPORTED at plan creation,
-    and placing them whole (sym_max < 0) plans them."""
-    T = 1100
+    """A worker's gather run queue lives in LDS (about 3,400 runs of 48 B in 160 KiB):
+    3,500 tables that are each split over all workers are refused with
+    EMB_ERR_UNSUPPORTED at plan creation, and placing them whole (sym_max < 0) plans them."""
+    T = 3500
     stats = [dict(mean_pooling=20.0, max_pooling=40, hot_rows=[], hot_freq=[], unique_frac=1.0)] * T
     with pytest.raises(gpu.EmbxError) as e:
         gpu.Plan([100000] * T, 64, "f32", stats, 4096)
@@ -309,3 +309,28 @@ def test_more_gather_slices_per_worker_than_lds_holds_is_refused(gpu):
     p = gpu.Plan([100000] * T, 64, "f32", stats, 4096, sym_max=-1)
     assert p.info()["num_items"] >= T
     p.close()
+
+
+def test_run_queue_beyond_64k_of_lds(gpu):
+    """1,500 tables split over all workers: each worker's run queue (1,501 records of 48 B,
+    72 KB) needs more than the default 64 KiB of dynamic LDS; the lookup matches the
+    oracle on sampled bags, bit-exact on integer tables."""
+    from gpu_helpers import check_sampled, filled_tables
+    T = 1500
+    tabs = [W.TableSpec(1000 + 7 * t, "fixed", 16, 16, 16, "uniform") for t in range(T)]
+    c = W.Config(110, "1100 tables", 64, "f32", -0.05, 0.05, 1024, tabs)
+    c.value_seeds = [W.value_seed(c.cfg_id, t) for t in range(c.T)]
+    batch = W.gen_batch(c, 0)
+    stats = W.history_stats(c)
+    idx, off = to_device(batch)
+    for mode, exact in ((W.VAL_UNIFORM, False), (W.VAL_INTEGER, True)):
+        ws = filled_tables(c, mode)
+        p = plan_for(c, c.batch, stats=stats).bind(ws)
+        info = p.info()
+        log(f"  {T} tables: {info['num_items']} slices, LDS {info['lds_bytes']} B")
+        assert info["num_items"] == T * 256 and info["lds_bytes"] > 65536
+        got = p.lookup(idx, off, batch.B).cpu().numpy()
+        assert p.check_errors() == 0
+        check_sampled(c, got, batch, 2000, seed=11, mode=mode, exact=exact)
+        p.close()
+        del ws
