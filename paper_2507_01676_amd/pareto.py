@@ -36,11 +36,14 @@ def pareto_front(points: List[Dict]) -> List[Dict]:
 
 
 def sweep(cfg: int, fractions: Sequence[float] = (1 / 16, 1 / 8, 1 / 4, 1 / 2, 1.0), steps: int = 100,
-          warmup: int = 10, n_p99: int = 500, n_batches: int = 4, log=print) -> List[Dict]:
+          warmup: int = 10, n_p99: int = 500, n_batches: int = 0, log=print) -> List[Dict]:
     import torch
     import workloads as W
     from . import Plan, fill_table
     c = W.make_config(cfg)
+    # distinct resident batches cycled, as bench.py does (fewer let a workload's rows stay
+    # in the MALL from one batch to the next)
+    n_batches = n_batches or (4 if cfg == 5 else 8)
     stats = W.history_stats(c)
     dt = torch.float16 if c.dtype == "f16" else torch.float32
     weights = []
@@ -121,10 +124,12 @@ def main(argv=None) -> int:
     ap.add_argument("--p99", type=int, default=500)
     ap.add_argument("--out", default=None, help="markdown summary")
     ap.add_argument("--json", default=None)
+    ap.add_argument("--batches", type=int, default=0, help="distinct resident batches (default 8, 4 for workload 5)")
     a = ap.parse_args(argv)
     pts = []
     for cfg in a.configs:
-        pts += sweep(cfg, a.fractions, a.steps, n_p99=a.p99, log=lambda m: print(m, file=sys.stderr, flush=True))
+        pts += sweep(cfg, a.fractions, a.steps, n_p99=a.p99, n_batches=a.batches,
+                     log=lambda m: print(m, file=sys.stderr, flush=True))
     cmd = "python -m paper_2507_01676_amd.pareto " + " ".join(argv if argv is not None else sys.argv[1:])
     md = to_markdown(pts, cmd)
     print(md)
