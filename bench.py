@@ -195,11 +195,9 @@ def launch_floor_us(stream) -> float:
     import paper_2507_01676_amd as embx
     x = torch.empty((1, 4), device="cuda")
     ptr, sp = x.data_ptr(), stream.cuda_stream
-    fill = embx._lib.embx_fill_table
 
     def launch():
-        if fill(ptr, 0, 1, 4, embx.DTYPE_F32, 0, 1, 0.0, 1.0, 0, sp) != 0:
-            raise RuntimeError("embx_fill_table failed")
+        embx.fill_table_ptr(ptr, 0, 1, 4, embx.DTYPE_F32, 0, 1, 0.0, 1.0, 0, sp)
     for _ in range(20):
         launch()
     torch.cuda.synchronize()

@@ -348,6 +348,15 @@ def fill_table(w, table_id: int, seed: int, lo: float = -0.05, hi: float = 0.05,
     return w
 
 
+def fill_table_ptr(ptr: int, row_begin: int, n_rows: int, E: int, dtype_code: int, table_id: int, seed: int,
+                   lo: float, hi: float, mode: int, stream_ptr) -> None:
+    """Raw-pointer form of fill_table for timing loops (as thin as Plan.lookup_ptr: ctypes
+    converts the arguments): rows [row_begin, row_begin + n_rows) of the synthetic table
+    into device memory at ptr; dtype_code DTYPE_F32 or DTYPE_F16, seed < 2**64."""
+    _check(_lib.embx_fill_table(ptr, row_begin, n_rows, E, dtype_code, table_id, seed, lo, hi, mode, stream_ptr),
+           "embx_fill_table")
+
+
 def dedup_tile(idx, stream=None):
     """Device tile sort/dedup of up to 2048 row ids: (sorted distinct ids, slot of each input)."""
     import torch
