@@ -94,7 +94,8 @@ def default_beta(R: int) -> List[float]:
     terms are latency-bound there and serve unchanged for other row sizes.
     HOT (H0, SH, P) and DEDUP (D0, D1) were fitted again, with the other
     coefficients held, on workloads 1-4 under their own and under fixed queries,
-    which vary the staged hot rows C from 1 to 512.
+    which vary the staged hot rows C from 1 to 512, with residuals relative to each
+    slice's predicted time (so that short slices set the fixed costs).
     """
     del R
     b = [0.0] * NBETA
@@ -104,11 +105,11 @@ def default_beta(R: int) -> List[float]:
     b[L1] = 10950.0
     b[S] = 477.0
     b[I] = 8280.0
-    b[H0] = 1020000.0
-    b[P] = 2720.0
-    b[D0] = 7260000.0
-    b[D1] = 24080.0
-    b[SH] = 77.0
+    b[H0] = 3990000.0
+    b[P] = 1180.0
+    b[D0] = 6690000.0
+    b[D1] = 26720.0
+    b[SH] = 45.0
     return b
 
 

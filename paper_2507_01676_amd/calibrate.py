@@ -25,7 +25,8 @@ combine), then HOT (H0, SH, P) and DEDUP (D0, D1) on what their costs leave
 after the shared terms.  HOT has its own per-byte staging term: its rows are
 fetched by id, one row per sub-wavefront, where an LDS slice copies a block, and
 the paper's coefficients differ per strategy in the same way (Sec. III-A).
-Every fit is ``numpy.linalg.lstsq``, constrained to non-negative coefficients
+Every fit is ``numpy.linalg.lstsq``, reweighted once so that residuals count
+relative to each sample's predicted time, and constrained to non-negative coefficients
 (an active-set NNLS) when the unconstrained solution has a negative one: the
 coefficients are times, and the planner refuses negative ones.
 
@@ -78,10 +79,23 @@ class Samples:
     workers: List[WorkerSample] = field(default_factory=list)
 
 
-def _lstsq(A: np.ndarray, y: np.ndarray) -> np.ndarray:
+def _lstsq(A: np.ndarray, y: np.ndarray, offset: Optional[np.ndarray] = None) -> np.ndarray:
     """Least squares with non-negative coefficients (the planner refuses negative ones):
-    the unconstrained OLS solution when it is non-negative, else the best fit over the
-    columns that stay free (scipy's active-set NNLS), columns scaled to unit norm."""
+    the unconstrained solution when it is non-negative, else the best fit over the
+    columns that stay free (scipy's active-set NNLS), columns scaled to unit norm.
+
+    With ``offset`` (the part of each sample's time already accounted for, so that the
+    sample's time is A x + offset) the fit is reweighted once: residuals are divided by
+    each sample's time as predicted by a first plain fit (at least 1 us).  Timing noise
+    grows with the time (contention), so unweighted, the long slices' scatter sets the
+    intercept -- it then came out negative for strategies whose short slices are
+    nearly all fixed cost.  The predicted rather than the measured time keeps the
+    weights free of the noise they correct for."""
+    if offset is not None:
+        x0, *_ = np.linalg.lstsq(A, y, rcond=None)
+        w = 1.0 / np.maximum(A @ x0 + np.asarray(offset, dtype=np.float64), 1e6)
+        A = A * w[:, None]
+        y = y * w
     x, *_ = np.linalg.lstsq(A, y, rcond=None)
     if np.all(x >= 0.0):
         return x
@@ -93,33 +107,37 @@ def _lstsq(A: np.ndarray, y: np.ndarray) -> np.ndarray:
 
 
 def fit_beta(s: Samples, base: Optional[Sequence[float]] = None) -> List[float]:
-    """OLS fit of the beta vector; coefficients with no samples keep ``base``'s value."""
+    """Least-squares fit of the beta vector, residuals relative to each sample's predicted
+    time (one reweighting step); coefficients with no samples keep ``base``'s value."""
     b = list(base) if base is not None else [0.0] * NBETA
     if s.workers:
         A = np.array([[w.n_slices, w.lam] for w in s.workers], dtype=np.float64)
         y = np.array([w.ps for w in s.workers], dtype=np.float64)
-        b[G0], b[G1] = (float(v) for v in _lstsq(A, y))
+        b[G0], b[G1] = (float(v) for v in _lstsq(A, y, np.zeros(len(y))))
     whole = [x for x in s.slices if x.strat == LDS and x.c == 1]
     if whole:
         A = np.array([[1.0, x.mu * x.R, x.lam] for x in whole])
         y = np.array([x.ps for x in whole])
-        b[L0], b[S], b[L1] = (float(v) for v in _lstsq(A, y))
+        b[L0], b[S], b[L1] = (float(v) for v in _lstsq(A, y, np.zeros(len(y))))
     chunks = [x for x in s.slices if x.strat == LDS and x.c > 1]
     if chunks:
         # I on what the whole-table terms leave; it absorbs the chunk combine as well
         A = np.array([[x.lam] for x in chunks])
-        y = np.array([x.ps - b[L0] - b[S] * x.mu * x.R - b[L1] * x.lam / x.c for x in chunks])
-        b[I] = float(_lstsq(A, y)[0])
+        off = np.array([b[L0] + b[S] * x.mu * x.R + b[L1] * x.lam / x.c for x in chunks])
+        y = np.array([x.ps for x in chunks]) - off
+        b[I] = float(_lstsq(A, y, off)[0])
     hot = [x for x in s.slices if x.strat == HOT]
     if hot:
         A = np.array([[1.0, x.mu * x.R, x.lam] for x in hot])
-        y = np.array([x.ps - x.lam * (x.h * b[L1] + (1.0 - x.h) * b[G1]) for x in hot])
-        b[H0], b[SH], b[P] = (float(v) for v in _lstsq(A, y))
+        off = np.array([x.lam * (x.h * b[L1] + (1.0 - x.h) * b[G1]) for x in hot])
+        y = np.array([x.ps for x in hot]) - off
+        b[H0], b[SH], b[P] = (float(v) for v in _lstsq(A, y, off))
     dd = [x for x in s.slices if x.strat == DEDUP]
     if dd:
         A = np.array([[1.0, x.lam] for x in dd])
-        y = np.array([x.ps - b[G1] * x.u * x.lam for x in dd])
-        b[D0], b[D1] = (float(v) for v in _lstsq(A, y))
+        off = np.array([b[G1] * x.u * x.lam for x in dd])
+        y = np.array([x.ps for x in dd]) - off
+        b[D0], b[D1] = (float(v) for v in _lstsq(A, y, off))
     return b
 
 

@@ -252,11 +252,11 @@ std::array<double, B_COUNT> default_beta(int32_t) {
   b[B_L1] = 10950.0;
   b[B_S] = 477.0;
   b[B_I] = 8280.0;
-  b[B_H0] = 1020000.0;
-  b[B_P] = 2720.0;
-  b[B_D0] = 7260000.0;
-  b[B_D1] = 24080.0;
-  b[B_SH] = 77.0;
+  b[B_H0] = 3990000.0;
+  b[B_P] = 1180.0;
+  b[B_D0] = 6690000.0;
+  b[B_D1] = 26720.0;
+  b[B_SH] = 45.0;
   return b;
 }
 

@@ -87,3 +87,49 @@ def test_a_dropped_term_is_caught():
     v, *_ = np.linalg.lstsq(A, y, rcond=None)
     resid = np.abs(A @ v - y).max()
     assert resid > 1e5
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_relative_residuals_keep_the_fixed_cost_of_short_slices(seed):
+    """Mostly long HOT slices whose times scatter by 30% (contention) and a few short ones
+    (5%) that are nearly all fixed cost: with residuals relative to each slice's predicted
+    time the fit recovers H0, what a short slice costs; unweighted, the long slices'
+    scatter sets the intercept (off by more than the weighted fit in most seeds)."""
+    g = np.random.default_rng(seed)
+    b = list(BETA_TRUE)
+    b[CAL.H0] = 2e6
+    s = CAL.Samples()
+    for i in range(600):
+        short = i % 10 == 0
+        lam = float(g.integers(1, 8)) if short else float(g.integers(2000, 20000))
+        C = int(g.integers(1, 4)) if short else int(g.integers(256, 512))
+        h = float(g.random())
+        y, _ = OPL.cost_hot(b, C, 256, h, lam)
+        noise = 0.05 if short else 0.3
+        s.slices.append(CAL.SliceSample(CAL.HOT, lam, float(C), 256, 1, h=h, ps=float(y) * (1.0 + noise * g.standard_normal())))
+    got = CAL.fit_beta(s, b)
+    assert got[CAL.H0] == pytest.approx(b[CAL.H0], rel=0.05)
+
+
+def test_unweighted_fit_misses_the_fixed_cost():
+    """Planted mistake: the same samples fitted without the reweighting miss H0 by more
+    than 25% in at least half of the seeds above."""
+    misses = 0
+    for seed in range(6):
+        g = np.random.default_rng(seed)
+        b = list(BETA_TRUE)
+        b[CAL.H0] = 2e6
+        rows, ys = [], []
+        for i in range(600):
+            short = i % 10 == 0
+            lam = float(g.integers(1, 8)) if short else float(g.integers(2000, 20000))
+            C = int(g.integers(1, 4)) if short else int(g.integers(256, 512))
+            h = float(g.random())
+            y, _ = OPL.cost_hot(b, C, 256, h, lam)
+            noise = 0.05 if short else 0.3
+            ps = float(y) * (1.0 + noise * g.standard_normal())
+            rows.append([1.0, C * 256.0, lam])
+            ys.append(ps - lam * (h * b[CAL.L1] + (1.0 - h) * b[CAL.G1]))
+        x = CAL._lstsq(np.array(rows), np.array(ys))
+        misses += abs(x[0] - b[CAL.H0]) > 0.25 * b[CAL.H0]
+    assert misses >= 3
