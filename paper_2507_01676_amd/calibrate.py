@@ -287,9 +287,11 @@ def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=pri
             plan.lookup(idx, off, c.batch, out)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
+        # raw-pointer launches, as bench.py times them (no per-call argument checks)
+        ip, op, rp, sp = idx.data_ptr(), off.data_ptr(), out.data_ptr(), torch.cuda.current_stream().cuda_stream
         a.record()
         for _ in range(50):
-            plan.lookup(idx, off, c.batch, out)
+            plan.lookup_ptr(ip, op, c.batch, rp, sp)
         b.record()
         torch.cuda.synchronize()
         launch_us = a.elapsed_time(b) * 1e3 / 50

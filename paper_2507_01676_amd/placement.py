@@ -50,9 +50,11 @@ def study(tables: Sequence[int] = (26, 100, 1000), batch: int = 1024, E: int = 6
                 plan.lookup(idx, off, c.batch, res)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             torch.cuda.synchronize()
+            # raw-pointer launches, as bench.py times them (no per-call argument checks)
+            ip, op, rp, sp = idx.data_ptr(), off.data_ptr(), res.data_ptr(), torch.cuda.current_stream().cuda_stream
             a.record()
             for _ in range(launches):
-                plan.lookup(idx, off, c.batch, res)
+                plan.lookup_ptr(ip, op, c.batch, rp, sp)
             b.record()
             torch.cuda.synchronize()
             info = plan.info()

@@ -53,9 +53,11 @@ def study(rows: Sequence[int], pooling: Sequence[int], T: int = 8, batch: int = 
                     plan.lookup(idx, off, batch, res)
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 torch.cuda.synchronize()
+                # raw-pointer launches, as bench.py times them (no per-call argument checks)
+                ip, op, rp, sp = idx.data_ptr(), off.data_ptr(), res.data_ptr(), torch.cuda.current_stream().cuda_stream
                 a.record()
                 for _ in range(launches):
-                    plan.lookup(idx, off, batch, res)
+                    plan.lookup_ptr(ip, op, batch, rp, sp)
                 b.record()
                 torch.cuda.synchronize()
                 us = a.elapsed_time(b) * 1e3 / launches
