@@ -97,7 +97,10 @@ enum {
  * distribution), Sec. III-A.  Measured on a representative batch. */
 typedef struct {
   double mean_pooling;      /* s_t >= 0: mean lookups per bag                                   */
-  int32_t max_pooling;      /* upper bound on lookups per bag, 0 = unknown (informational)      */
+  int32_t max_pooling;      /* upper bound on lookups per bag; 0 = unknown.  Exactly 1 lets the
+                               gather path store each bag's single row as its output (a bag that
+                               holds more at run time is still summed, on a slower path); any
+                               other value, 0 included, walks bags as sums                        */
   int32_t n_hot;            /* entries in hot_rows / hot_freq, 0..EMB_MAX_HOT_STATS             */
   const int64_t* hot_rows;  /* host, hottest first, distinct, each in [0, rows)                 */
   const double* hot_freq;   /* host, fraction of the table's lookups that hit each hot row       */
@@ -137,12 +140,18 @@ typedef struct {
   int64_t max_load_ps, sum_load_ps;
   int32_t lif_milli, r_symmetric;
   int32_t n_strategy[5];    /* slices per strategy (emb_strategy_t order)      */
+  int32_t gather_runs[3];   /* gather slices over all workers' queues: a wavefront per bag
+                               (long bags), single-lookup bags (max_pooling == 1), SW sums */
 } emb_plan_info_t;
 
 /* Builds a plan for T tables of rows[t] x E elements of `dtype`, for batches of up to
  * max_batch samples, on the current HIP device (Sec. III-A problem statement: N, M, S, B,
- * K, I, L).  Host-side work plus one upload of the plan's metadata; allocates the device
- * workspace for row-chunk partial sums.  rows[t] in [1, 2^31); E a multiple of 4 (fp32) or
+ * K, I, L; the policy of Eq. (1) chosen with the cost model of Eq. (2) and mapped onto the
+ * workers by Sec. III-B steps 1-4).  Host-side work plus one upload of the plan's metadata;
+ * allocates the device workspace for row-chunk partial sums ([chunks, max_batch, E] fp32 per
+ * row-chunked table).  No workspace grows with the number of indices: the kernels read
+ * indices and offsets in place, and a DEDUP tile is sorted in LDS, so the plan needs no
+ * index count.  rows[t] in [1, 2^31); E a multiple of 4 (fp32) or
  * 8 (fp16), E <= 256; opts may be NULL.  On success *plan_out owns everything it allocated.
  * EMB_ERR_UNSUPPORTED when a worker would hold more gather slices than its run queue in
  * LDS takes (48 B each, about 3,400 in 160 KiB): with every table split over all workers,
@@ -152,11 +161,14 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
                              const emb_table_stats_t* stats, int32_t max_batch,
                              const emb_plan_options_t* opts);
 
-/* Records the T device pointers of the tables (weights[t] -> rows[t] x E contiguous,
- * row-major, 16-byte aligned).  The caller keeps ownership and keeps them alive. */
+/* Records the T device pointers of the tables: the paper's lookup tables of m_i rows of E
+ * elements (Sec. II-B), weights[t] -> rows[t] x E contiguous, row-major, 16-byte aligned.
+ * The caller keeps ownership and keeps them alive.  Copies the pointers into the plan's
+ * device metadata (synchronous). */
 emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights);
 
-/* One batch.  indices: device int64 [offsets[T*batch]], table-local row ids;
+/* One batch of the embedding-bag lookup of Sec. II-B (each sample's bag of rows per table,
+ * reduced per Sec. IV-A by summation).  indices: device int64 [offsets[T*batch]], table-local row ids;
  * offsets: device int64 [T*batch + 1], table-major CSR (bag (t, b) is
  * indices[offsets[t*batch+b] .. offsets[t*batch+b+1]) ), offsets[0] = 0, non-decreasing;
  * out: device fp32 [batch, T, E].  Enqueues exactly one kernel on `stream`; never
@@ -175,15 +187,21 @@ emb_status_t emb_lookup(emb_plan_t* plan, const int64_t* indices, const int64_t*
 emb_status_t emb_lookup_weighted(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets,
                                  const float* weights, int32_t batch, float* out, void* stream);
 
-/* Synchronizes `stream`, returns the number of out-of-range indices seen since the last
+/* Range errors.  Sec. III-B subtracts a chunk's first row from each index and clips the
+ * result so that every address stays inside the chunk; an index outside the table itself
+ * is never read here: it adds nothing and is counted on the device.  This call
+ * synchronizes `stream`, returns the number of out-of-range indices seen since the last
  * call in *n_bad (may be NULL) and resets the counter; EMB_ERR_INDEX_OUT_OF_RANGE if any. */
 emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_bad);
 
-/* Canonical text of the plan (one line per slice: worker, table, strategy, chunk, chunks,
- * first row, end row, split, slice, hot rows, cost in ps).  Writes at most cap bytes
+/* Canonical text of the plan: the policy of Eq. (1) (a data flow per table) and its
+ * mapping onto workers (Sec. III-B), one line per slice: worker, table, strategy, chunk,
+ * chunks, first row, end row, split, slice, hot rows, cost in ps.  Writes at most cap bytes
  * (NUL-terminated when it fits); *len_out = text length without the NUL. */
 emb_status_t emb_plan_serialize(const emb_plan_t* plan, char* buf, size_t cap, size_t* len_out);
 
+/* Plan summary (the same plan as emb_plan_serialize): shapes, launch shape, slices per
+ * strategy, the predicted makespan and the load imbalance factor of Sec. III-B step 4. */
 emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info);
 
 /* Per-slice timers for fitting the cost model (Sec. III-A: the coefficients of Eq. (2) are

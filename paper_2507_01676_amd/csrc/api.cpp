@@ -47,6 +47,7 @@ struct emb_plan {
   bool staged = false;                   // the plan has LDS / HOT / DEDUP / STREAM slices
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
   std::vector<int32_t> mean;             // per table: 1 = mean pooling
+  int32_t gather_runs[3] = {0, 0, 0};    // runs per gather queue class, over all workers
 };
 
 namespace {
@@ -342,14 +343,30 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     auto slice_bags = [&](const DevItem& d) -> int64_t {
       return (static_cast<int64_t>(d.j + 1) * max_batch) / d.k - (static_cast<int64_t>(d.j) * max_batch) / d.k;
     };
+    // Slice j of k holds floor((j+1)B/k) - floor(jB/k) bags at the runtime batch B, which
+    // for some B < max_batch is one more than at max_batch (e.g. k = 256, j = 10: 3 bags at
+    // B = 1000, 4 at B = 792).  Every B <= max_batch gives at most ceil(max_batch / k), so a
+    // run gets chunks for that many; chunks past the slice at the runtime batch are empty
+    // and skipped by the kernel's queue.
+    auto slice_bags_any = [&](const DevItem& d) -> int64_t {
+      return (static_cast<int64_t>(max_batch) + d.k - 1) / d.k;
+    };
     for (int w = 0; w < K; ++w) {
       double Ws = 0.0, Ww = 0.0;
+      // classes, in queue order: 0 wave mode, 1 single-lookup bags, 2 SW mode.  Only a
+      // table whose statistics state a maximum of one lookup per bag is single-lookup; an
+      // unknown maximum (0) walks in SW mode
+      auto class_of = [&](const DevItem& d) -> int {
+        if (d.mode) return 0;
+        return stats[d.table].max_pooling == 1 ? 1 : 2;
+      };
       for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
         if (items[i].strat != S_GATHER) continue;
         const double lk = static_cast<double>(slice_bags(items[i])) * std::max(1.0, stats[items[i].table].mean_pooling);
-        if (items[i].mode)
+        const int cls = class_of(items[i]);
+        if (cls == 0)
           Ww += lk;
-        else if (stats[items[i].table].max_pooling > 1)
+        else if (cls == 2)
           Ws += lk;
       }
       // SW-mode chunks are claimed dynamically: a chunk boundary costs about five lookups
@@ -359,11 +376,6 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
       const double target = std::min(128.0, std::max(8.0, std::floor(std::sqrt(5.0 * Ws / nsw))));
       const double wtarget = std::min(wave_chunk, std::max(1.0, std::floor(Ww / nwaves)));
       gr_ptr[w] = static_cast<int32_t>(gr.size());
-      // classes, in queue order: 0 wave mode, 1 single-lookup bags, 2 SW mode
-      auto class_of = [&](const DevItem& d) -> int {
-        if (d.mode) return 0;
-        return stats[d.table].max_pooling <= 1 ? 1 : 2;
-      };
       int64_t base[3] = {0, 0, 0};
       int32_t nrun[3] = {0, 0, 0};
       for (int cls = 0; cls < 3; ++cls) {
@@ -373,7 +385,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
           const double s_t = std::max(1.0, stats[d.table].mean_pooling);
           const int32_t cb = cls == 1 ? kChunkSingle
                                       : static_cast<int32_t>(std::max(1.0, std::floor((cls == 0 ? wtarget : target) / s_t)));
-          const int64_t nc = (slice_bags(d) + cb - 1) / cb;
+          const int64_t nc = (slice_bags_any(d) + cb - 1) / cb;
           if (nc == 0) continue;
           GatherRun r{};
           r.w = nullptr;
@@ -398,6 +410,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
         return EMB_ERR_UNSUPPORTED;
       }
       max_runs = std::max(max_runs, nrun[0] + nrun[1] + nrun[2]);
+      for (int cls = 0; cls < 3; ++cls) p->gather_runs[cls] += nrun[cls];
       GatherSlotHeader& hd = gr_head[w];
       std::memset(&hd, 0, sizeof hd);
       hd.n_wave = nrun[0];
@@ -471,7 +484,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   const int run_bytes = p->gr_slot * static_cast<int>(sizeof(GatherRun));
   p->staged = staged;
   p->lds_bytes = std::max(staged ? static_cast<int>(L) + kMetaReserve : 0, run_bytes);
-  if (prepare_lookup_kernels(std::max(p->lds_bytes, kMetaReserve)) != 0) {
+  if (prepare_lookup_kernels(dev, static_cast<int>(smem) - kStaticLdsReserve) != 0) {
     emb_plan_destroy(p);
     return EMB_ERR_DEVICE;
   }
@@ -593,6 +606,7 @@ emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info) {
   info->lif_milli = static_cast<int32_t>(plan->plan.lif_milli);
   info->r_symmetric = plan->plan.r_sym;
   for (const PSlice& x : plan->plan.slices) info->n_strategy[x.strat] += 1;
+  for (int cls = 0; cls < 3; ++cls) info->gather_runs[cls] = plan->gather_runs[cls];
   return EMB_OK;
 }
 
@@ -608,7 +622,11 @@ emb_status_t emb_plan_destroy(emb_plan_t* plan) {
 emb_status_t emb_debug_dedup_tile(const int64_t* idx, int32_t n, int32_t* uniq, int32_t* inv, int32_t* n_uniq,
                                   void* stream) {
   if (n < 0 || n > kTile || (n > 0 && (!idx || !uniq || !inv)) || !n_uniq) return EMB_ERR_INVALID_ARGUMENT;
-  if (prepare_lookup_kernels(kMetaReserve) != 0) return EMB_ERR_DEVICE;
+  int dev = 0;
+  hipDeviceProp_t prop;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) return EMB_ERR_DEVICE;
+  if (prepare_lookup_kernels(dev, static_cast<int>(prop.sharedMemPerBlock) - kStaticLdsReserve) != 0)
+    return EMB_ERR_DEVICE;
   return st(launch_dedup_probe(idx, n, uniq, inv, n_uniq, stream));
 }
 

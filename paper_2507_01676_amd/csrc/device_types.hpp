@@ -99,7 +99,9 @@ constexpr int kTraceWorker = 2 + kBlock / 64;
 // Host-callable launchers (defined in lookup.hip).
 int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
                   void* stream);
-int prepare_lookup_kernels(int lds_bytes);
+// once per device: lets every lookup kernel launch with up to max_dynamic_lds bytes of
+// dynamic LDS (0 = done, else an emb_status_t code)
+int prepare_lookup_kernels(int device, int max_dynamic_lds);
 int launch_dedup_probe(const int64_t* idx, int n, int32_t* uniq, int32_t* inv, int32_t* n_uniq, void* stream);
 int launch_hot_probe(const int32_t* keys, const uint16_t* slots, int hash_log2, const int64_t* idx, int n,
                      int32_t* slot, void* stream);

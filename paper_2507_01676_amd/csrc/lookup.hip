@@ -36,6 +36,9 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+#include <vector>
+
 #include "device_types.hpp"
 
 // The lookup kernels are compiled in parts so that a build can run the parts in
@@ -1702,20 +1705,28 @@ LookupKernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
 
 }  // namespace
 
-int prepare_lookup_kernels(int lds_bytes) {
-  // staged kernels hold rows and metadata; gather-only ones the worker's run queue,
-  // which may also pass the default 64 KiB
+int prepare_lookup_kernels(int device, int max_dynamic_lds) {
+  // Once per device, every lookup kernel may take up to the whole of a workgroup's LDS
+  // but the kernel's static variables: a plan's launch asks only for its own dynamic
+  // size, so no plan (nor a probe) ever lowers what another plan launches with.
+  static std::mutex mu;
+  static std::vector<char> done;
+  if (device < 0 || max_dynamic_lds < kMetaReserve) return 1;
+  std::lock_guard<std::mutex> lock(mu);
+  if (static_cast<size_t>(device) < done.size() && done[device]) return 0;
   for (int G = 1; G <= 64; G <<= 1) {
     for (int f = 0; f < 8; ++f) {
       LookupKernelFn k = pick_any(G, (f & 1) != 0, (f & 4) == 0, (f & 2) != 0);
       if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              lds_bytes) != hipSuccess)
+                              max_dynamic_lds) != hipSuccess)
         return 4;
     }
   }
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(&dedup_probe_kernel),
                           hipFuncAttributeMaxDynamicSharedMemorySize, kMetaReserve) != hipSuccess)
     return 4;
+  if (done.size() <= static_cast<size_t>(device)) done.resize(device + 1, 0);
+  done[device] = 1;
   return 0;
 }
 

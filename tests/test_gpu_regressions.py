@@ -1,0 +1,125 @@
+"""GPU regression tests of host-side launch preparation, each against the oracle:
+
+- a runtime batch below the plan's max batch can put one more bag in a batch slice than the
+  max batch does (slice j of k is bags [floor(jB/k), floor((j+1)B/k))): every bag must still
+  be walked and written;
+- a table whose statistics leave the maximum pooling unknown (0) is summed like any other,
+  not treated as single-lookup bags;
+- a plan launched with nearly all of a workgroup's LDS keeps working after smaller plans
+  and the dedup probe have been created and run.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+
+from gpu_helpers import check_full, host_tables, log, plan_for, to_device, upload_tables
+from test_gpu_parity import STRATS
+
+pytestmark = pytest.mark.gpu
+
+
+def fixed_pf_config(cfg_id, rows, pfs, E=64, dtype="f32", B=1000):
+    tabs = [W.TableSpec(m, "fixed", pf, pf, pf, "uniform") for m, pf in zip(rows, pfs)]
+    c = W.Config(cfg_id, f"fixed pooling {pfs}", E, dtype, -1.0, 1.0, B, tabs)
+    c.value_seeds = [W.value_seed(cfg_id, t) for t in range(c.T)]
+    return c
+
+
+# runtime batches below 1000 for which some slice of k = 256 (or 4, 64) holds one bag more
+# than at 1000, plus edge sizes
+RUNTIME_BATCHES = [792, 999, 1000, 513, 257, 256, 255, 100, 7, 1]
+
+
+@pytest.mark.parametrize("pfs", [[20] * 10, [3] * 10, [1] * 10, [20, 3, 1, 50, 8, 1, 2, 20, 1, 5]])
+def test_runtime_batch_below_max_batch_writes_every_bag(pfs):
+    import torch
+    log(f"max batch 1000, runtime batches {RUNTIME_BATCHES}, pooling {pfs}")
+    c = fixed_pf_config(140, [100_000] * 10, pfs)
+    hw = host_tables(c, W.VAL_INTEGER)
+    p = plan_for(c, 1000).bind(upload_tables(hw))
+    log(f"  gather runs per queue {p.info()['gather_runs']}")
+    for B in RUNTIME_BATCHES:
+        batch = W.gen_batch(c, B, B=B)
+        idx, off = to_device(batch)
+        out = torch.full((B, c.T, c.E), float("nan"), device="cuda")
+        p.lookup(idx, off, B, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert not np.isnan(got).any(), f"batch {B}: {int(np.isnan(got).any(axis=2).sum())} bags never written"
+        check_full(got, hw, batch, c.dtype, exact=True)
+    assert p.check_errors() == 0
+
+
+def test_runtime_batch_below_max_batch_mean_pooling():
+    import torch
+    log("mean pooling, max batch 1000, runtime batch 792 (a slice of 256 gains a bag)")
+    c = fixed_pf_config(141, [100_000] * 10, [20] * 10)
+    hw = host_tables(c)
+    p = plan_for(c, 1000, pooling="mean").bind(upload_tables(hw))
+    from oracle import pool as OP
+    for B in (792, 1000, 333):
+        batch = W.gen_batch(c, B, B=B)
+        idx, off = to_device(batch)
+        out = torch.full((B, c.T, c.E), float("nan"), device="cuda")
+        p.lookup(idx, off, B, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert not np.isnan(got).any()
+        ref, mag, _ = OP.pool_reference(hw, batch.indices, batch.offsets, B, pooling="mean")
+        assert OP.pooled_error(got, ref, mag) <= 1e-5
+
+
+def test_unknown_max_pooling_is_summed_not_single():
+    import torch
+    log("pooling-8 table with max_pooling 0 (unknown) and a pooling-1 table with max_pooling 1")
+    c = fixed_pf_config(142, [50_000, 50_000], [8, 1], B=512)
+    stats = W.history_stats(c)
+    stats[0].max_pooling = 0
+    hw = host_tables(c, W.VAL_INTEGER)
+    p = plan_for(c, c.batch, stats=stats).bind(upload_tables(hw))
+    runs = p.info()["gather_runs"]
+    log(f"  gather runs per queue {runs}")
+    # the pooling-1 table promises one lookup per bag (single queue); the other does not
+    text = p.serialize()
+    t1_slices = sum(1 for ln in text.splitlines() if ln.startswith("item ") and ln.split()[2] == "1")
+    assert runs["single"] == t1_slices > 0
+    assert runs["sw"] + runs["wave"] > 0
+    batch = W.gen_batch(c, 0)
+    idx, off = to_device(batch)
+    out = torch.full((c.batch, c.T, c.E), float("nan"), device="cuda")
+    p.lookup(idx, off, c.batch, out)
+    torch.cuda.synchronize()
+    check_full(out.cpu().numpy(), hw, batch, c.dtype, exact=True)
+    # every table unknown: no single-lookup queue at all, results unchanged
+    for s in stats:
+        s.max_pooling = 0
+    p0 = plan_for(c, c.batch, stats=stats).bind(upload_tables(hw))
+    assert p0.info()["gather_runs"]["single"] == 0
+    out0 = p0.lookup(idx, off, c.batch)
+    torch.cuda.synchronize()
+    check_full(out0.cpu().numpy(), hw, batch, c.dtype, exact=True)
+
+
+def test_large_lds_plan_after_smaller_plans_and_probe():
+    import torch
+
+    import paper_2507_01676_amd as embx
+    log("a plan using ~159 KiB of LDS, then a small plan and the dedup probe, then the first plan")
+    c = fixed_pf_config(143, [260, 5000, 40_000, 100_000], [4, 3, 2, 6], E=128, B=257)
+    hw = host_tables(c, W.VAL_INTEGER)
+    wd = upload_tables(hw)
+    big = plan_for(c, c.batch, force=[STRATS["lds"]] * c.T, lds_budget=133_888).bind(wd)
+    assert big.info()["lds_bytes"] > 160_000
+    small = plan_for(c, c.batch, force=[STRATS["gather"]] * c.T).bind(wd)
+    assert small.info()["lds_bytes"] < 16_384
+    ids = torch.from_numpy(np.arange(100, dtype=np.int64)[::-1].copy()).cuda()
+    uniq, _ = embx.dedup_tile(ids)
+    assert uniq.numel() == 100
+    batch = W.gen_batch(c, 0)
+    idx, off = to_device(batch)
+    for p in (big, small, big):
+        out = torch.full((c.batch, c.T, c.E), float("nan"), device="cuda")
+        p.lookup(idx, off, c.batch, out)
+        torch.cuda.synchronize()
+        check_full(out.cpu().numpy(), hw, batch, c.dtype, exact=True)

@@ -35,12 +35,12 @@ def test_p99_is_nearest_rank():
     assert p99(list(range(1, 1001))) == 990
 
 
-def _table2():
-    """The paper's Table II (Sec. IV-C) from tests/golden: (distribution, strategy, workload,
+def _table1():
+    """The paper's Table I (Sec. IV-A) from tests/golden: (distribution, strategy, workload,
     P99 us, queries/s, bold) per reported cell; bold when either value is printed in bold."""
     import csv
     import os
-    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "table2_p99_tps_batch8192.csv")
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "table1_p99_tps_batch8192.csv")
     with open(path) as f:
         rows = list(csv.DictReader(line for line in f if not line.startswith("#")))
     out = []
@@ -56,10 +56,10 @@ def _table2():
 
 
 def test_the_papers_best_entries_are_on_the_front():
-    """Table II prints each workload's best P99 and best throughput in bold. A point best
+    """Table I prints each workload's best P99 and best throughput in bold. A point best
     in either coordinate is dominated by none, so every bold cell of a (distribution,
     workload) column is on that column's front."""
-    cells = _table2()
+    cells = _table1()
     assert len(cells) == 51
     cols = {}
     for d, s, w, lat, tps, bold in cells:
@@ -81,7 +81,7 @@ def test_the_papers_best_entries_are_on_the_front():
 
 def test_a_front_that_keeps_dominated_points_is_caught():
     """Planted mistake: comparing throughput the wrong way keeps a dominated cell."""
-    cells = _table2()
+    cells = _table1()
     pts = [dict(lookups_per_s=t, p99_us=l, strategy=s) for d, s, w, l, t, b in cells
            if d == "uniform" and w == "Criteo-1TB"]
 

@@ -403,11 +403,37 @@ def history_stats(c: Config, B: Optional[int] = None, threads: Optional[int] = N
 
 
 def algorithmic_bytes(c: Config, n_lookups: int, B: Optional[int] = None) -> dict:
-    """Bytes one batch must move at minimum: rows + indices + offsets + output."""
+    """Bytes one batch names: every lookup's row + indices + offsets + output (a row read
+    twice counts twice; see ``compulsory_bytes`` for what must cross HBM)."""
     B = c.batch if B is None else B
     R = c.row_bytes
     rows = n_lookups * R
     idx = n_lookups * 8
+    offs = (c.T * B + 1) * 8
+    out = c.T * B * c.E * 4
+    return {"rows": rows, "indices": idx, "offsets": offs, "out": out, "total": rows + idx + offs + out}
+
+
+def distinct_rows(c: Config, batch: "Batch") -> List[int]:
+    """Distinct valid row ids each table's lookups of ``batch`` name."""
+    B = batch.B
+    out = []
+    for t, m in enumerate(c.rows):
+        ids = batch.indices[batch.offsets[t * B]: batch.offsets[(t + 1) * B]]
+        ids = ids[(ids >= 0) & (ids < m)]
+        seen = np.zeros(m, dtype=np.bool_)
+        seen[ids] = True
+        out.append(int(np.count_nonzero(seen)))
+    return out
+
+
+def compulsory_bytes(c: Config, batch: "Batch", weighted: bool = False) -> dict:
+    """Bytes one batch must move between HBM and the chip at the least: each distinct row
+    once, every index (and weight), every offset and the output once."""
+    B = batch.B
+    L = batch.n_lookups
+    rows = sum(distinct_rows(c, batch)) * c.row_bytes
+    idx = L * 8 + (L * 4 if weighted else 0)
     offs = (c.T * B + 1) * 8
     out = c.T * B * c.E * 4
     return {"rows": rows, "indices": idx, "offsets": offs, "out": out, "total": rows + idx + offs + out}
