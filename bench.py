@@ -54,7 +54,8 @@ METRIC = "embedding lookups/s + queries/s, P99 batch latency, % HBM peak (1 MI35
 DEFAULT_CONFIG = 5
 # what decides a launch's memory traffic: the kernels and the plan (planner + metadata);
 # a stored traffic measurement is used only while their hash is unchanged
-KERNEL_SOURCES = ["paper_2507_01676_amd/csrc/lookup.hip", "paper_2507_01676_amd/csrc/device_types.hpp",
+KERNEL_SOURCES = ["paper_2507_01676_amd/csrc/lookup.hip", "paper_2507_01676_amd/csrc/gather.hip",
+                  "paper_2507_01676_amd/csrc/device_types.hpp",
                   "paper_2507_01676_amd/csrc/planner.cpp", "paper_2507_01676_amd/csrc/planner.hpp",
                   "paper_2507_01676_amd/csrc/api.cpp"]
 

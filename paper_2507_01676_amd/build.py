@@ -42,6 +42,8 @@ def _run(cmd, verbose):
 # lookup.hip is compiled in parts (EMBX_PART): one per (row type, weighted) kernel
 # family, plus the probes, filler and launch code
 LOOKUP_PARTS = 5
+# gather.hip: one part per (row type, weighted) kernel family
+GATHER_PARTS = 4
 
 
 def _run_all(cmds, verbose):
@@ -68,6 +70,10 @@ def build(verbose: bool = False) -> str:
     for part in range(LOOKUP_PARTS):
         o = os.path.join(BUILD, f"lookup_{part}.o")
         cmds.append([hipcc, *HIP_FLAGS, f"-DEMBX_PART={part}", "-c", os.path.join(CSRC, "lookup.hip"), "-o", o])
+        objs.append(o)
+    for part in range(GATHER_PARTS):
+        o = os.path.join(BUILD, f"gather_{part}.o")
+        cmds.append([hipcc, *HIP_FLAGS, f"-DEMBX_GPART={part}", "-c", os.path.join(CSRC, "gather.hip"), "-o", o])
         objs.append(o)
     o = os.path.join(BUILD, "api.o")
     cmds.append([hipcc, *HIP_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, "api.cpp"), "-o", o])

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <climits>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -45,6 +46,7 @@ struct emb_plan {
   GatherRun* d_gr = nullptr;
   const char* d_zero_row = nullptr;      // R zero bytes
   bool staged = false;                   // the plan has LDS / HOT / DEDUP / STREAM slices
+  bool wave_gather = false;              // launches the wave-uniform gather kernel (gather.hip)
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
   std::vector<int32_t> mean;             // per table: 1 = mean pooling
   int32_t gather_runs[3] = {0, 0, 0};    // runs per gather queue class, over all workers
@@ -332,6 +334,17 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   // lookups (W: the worker's SW-mode lookups at the max batch), at least one full step
   // (8) and at most 128; wave-mode chunks carry about four wavefront steps of lookups,
   // fewer when that leaves some of the 16 wavefronts without one.
+  //
+  // A gather-only plan with rows of 16, 32 or 64 lanes runs the wave-uniform gather kernel
+  // instead (EMBX_GATHER_KERNEL=classic keeps the sub-wavefront walkers, for comparison):
+  // its queues are single-lookup bags (chunks of one wavefront step: 8 S bags) and all
+  // other bags (chunks of about sqrt(8 W / 16) expected lookups, W the worker's lookups
+  // in that queue, between two wavefront steps and 2048; EMBX_WAVE_CHUNK overrides it).
+  const char* env_kernel = std::getenv("EMBX_GATHER_KERNEL");
+  const bool wave_gather = !staged && (p->G == 16 || p->G == 32 || p->G == 64) &&
+                           !(env_kernel && std::strcmp(env_kernel, "classic") == 0);
+  const char* env_chunk = std::getenv("EMBX_WAVE_CHUNK");
+  const double wave_chunk_override = env_chunk ? std::atof(env_chunk) : 0.0;
   std::vector<GatherRun> gr;                       // runs, worker-major
   std::vector<int32_t> gr_ptr(K + 1, 0);
   std::vector<GatherSlotHeader> gr_head(K);
@@ -357,7 +370,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
       // table whose statistics state a maximum of one lookup per bag is single-lookup; an
       // unknown maximum (0) walks in SW mode
       auto class_of = [&](const DevItem& d) -> int {
-        if (d.mode) return 0;
+        if (d.mode && !wave_gather) return 0;
         return stats[d.table].max_pooling == 1 ? 1 : 2;
       };
       for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
@@ -373,7 +386,11 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
       // of a SW's time and the worker's tail is up to one chunk, so ~sqrt(5 W / NSW)
       // lookups per chunk balances the two; measured, chunks past ~128 lookups lose again
       // (the SWs then work on fewer tables at a time), hence the cap
-      const double target = std::min(128.0, std::max(8.0, std::floor(std::sqrt(5.0 * Ws / nsw))));
+      const double wstep = 8.0 * (64 / p->G);   // lookups of one wavefront step (wave kernel)
+      const double target =
+          !wave_gather ? std::min(128.0, std::max(8.0, std::floor(std::sqrt(5.0 * Ws / nsw))))
+          : wave_chunk_override > 0.0 ? wave_chunk_override
+                                      : std::min(2048.0, std::max(2.0 * wstep, std::floor(std::sqrt(8.0 * Ws / nwaves))));
       const double wtarget = std::min(wave_chunk, std::max(1.0, std::floor(Ww / nwaves)));
       gr_ptr[w] = static_cast<int32_t>(gr.size());
       int64_t base[3] = {0, 0, 0};
@@ -383,7 +400,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
           const DevItem& d = items[i];
           if (d.strat != S_GATHER || class_of(d) != cls) continue;
           const double s_t = std::max(1.0, stats[d.table].mean_pooling);
-          const int32_t cb = cls == 1 ? kChunkSingle
+          const int32_t cb = cls == 1 ? (wave_gather ? 512 / p->G : kChunkSingle)
                                       : static_cast<int32_t>(std::max(1.0, std::floor((cls == 0 ? wtarget : target) / s_t)));
           const int64_t nc = (slice_bags_any(d) + cb - 1) / cb;
           if (nc == 0) continue;
@@ -483,6 +500,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   // LDS: the staged slices' rows and metadata, and (after them) the worker's gather runs
   const int run_bytes = p->gr_slot * static_cast<int>(sizeof(GatherRun));
   p->staged = staged;
+  p->wave_gather = wave_gather;
   p->lds_bytes = std::max(staged ? static_cast<int>(L) + kMetaReserve : 0, run_bytes);
   if (prepare_lookup_kernels(dev, static_cast<int>(smem) - kStaticLdsReserve) != 0) {
     emb_plan_destroy(p);
@@ -545,6 +563,7 @@ emb_status_t lookup_impl(emb_plan_t* plan, const int64_t* indices, const int64_t
   a.zero_row = plan->d_zero_row;
   a.one = 1.0f;
   a.weights = weighted ? weights : nullptr;
+  if (plan->wave_gather) return st(launch_gather(a, plan->G, plan->f16, weighted, plan->K, plan->lds_bytes, stream));
   return st(launch_lookup(a, plan->G, plan->f16, plan->staged, weighted, plan->K, plan->lds_bytes, stream));
 }
 

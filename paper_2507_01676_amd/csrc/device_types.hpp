@@ -96,9 +96,18 @@ struct LookupArgs {
 //   slice i:   trace[K * kTraceWorker + 2 i + {0, 1}]  begin / end (staged slices)
 constexpr int kTraceWorker = 2 + kBlock / 64;
 
+// Gather-only kernels with wave-uniform control (gather.hip), for rows of G = 16, 32 or
+// 64 lanes; one family per (row type, weighted) pair, nullptr for other G.
+using GatherKernelFn = void (*)(LookupArgs);
+GatherKernelFn gather_kernel_f32(int G);
+GatherKernelFn gather_kernel_f32_weighted(int G);
+GatherKernelFn gather_kernel_f16(int G);
+GatherKernelFn gather_kernel_f16_weighted(int G);
+
 // Host-callable launchers (defined in lookup.hip).
 int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
                   void* stream);
+int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int lds_bytes, void* stream);
 // once per device: lets every lookup kernel launch with up to max_dynamic_lds bytes of
 // dynamic LDS (0 = done, else an emb_status_t code)
 int prepare_lookup_kernels(int device, int max_dynamic_lds);

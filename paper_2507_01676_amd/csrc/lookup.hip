@@ -1703,6 +1703,11 @@ LookupKernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
   return weighted ? lookup_kernel_f32_weighted(G, staged) : lookup_kernel_f32(G, staged);
 }
 
+GatherKernelFn pick_gather_any(int G, bool f16, bool weighted) {
+  if (f16) return weighted ? gather_kernel_f16_weighted(G) : gather_kernel_f16(G);
+  return weighted ? gather_kernel_f32_weighted(G) : gather_kernel_f32(G);
+}
+
 }  // namespace
 
 int prepare_lookup_kernels(int device, int max_dynamic_lds) {
@@ -1722,6 +1727,14 @@ int prepare_lookup_kernels(int device, int max_dynamic_lds) {
         return 4;
     }
   }
+  for (int G = 16; G <= 64; G <<= 1) {
+    for (int f = 0; f < 4; ++f) {
+      GatherKernelFn k = pick_gather_any(G, (f & 1) != 0, (f & 2) != 0);
+      if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                              max_dynamic_lds) != hipSuccess)
+        return 4;
+    }
+  }
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(&dedup_probe_kernel),
                           hipFuncAttributeMaxDynamicSharedMemorySize, kMetaReserve) != hipSuccess)
     return 4;
@@ -1733,6 +1746,13 @@ int prepare_lookup_kernels(int device, int max_dynamic_lds) {
 int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
                   void* stream) {
   LookupKernelFn k = pick_any(G, f16, staged, weighted);
+  if (!k) return 2;
+  hipLaunchKernelGGL(k, dim3(grid), dim3(kBlock), lds_bytes, static_cast<hipStream_t>(stream), a);
+  return hipGetLastError() == hipSuccess ? 0 : 4;
+}
+
+int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int lds_bytes, void* stream) {
+  GatherKernelFn k = pick_gather_any(G, f16, weighted);
   if (!k) return 2;
   hipLaunchKernelGGL(k, dim3(grid), dim3(kBlock), lds_bytes, static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? 0 : 4;

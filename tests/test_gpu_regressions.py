@@ -123,3 +123,38 @@ def test_large_lds_plan_after_smaller_plans_and_probe():
         p.lookup(idx, off, c.batch, out)
         torch.cuda.synchronize()
         check_full(out.cpu().numpy(), hw, batch, c.dtype, exact=True)
+
+
+def test_tables_beyond_4_gib_read_the_right_rows():
+    """Rows past byte 2^32 of a table: 9M rows of 512 bytes (4.6 GB), summed (pooling 3) and
+    single-lookup, with ids on both sides of the 4 GiB boundary; integer tables, bit-exact."""
+    import torch
+
+    from gpu_helpers import check_sampled, filled_tables
+    log("two 9M-row E128 fp32 tables (4.6 GB each) and a small one, ids around the 4 GiB boundary")
+    tabs = [W.TableSpec(9_000_000, "fixed", 3, 3, 3, "uniform"), W.TableSpec(9_000_000, "fixed", 1, 1, 1, "uniform"),
+            W.TableSpec(1000, "fixed", 2, 2, 2, "uniform")]
+    c = W.Config(144, "4 GiB tables", 128, "f32", -1.0, 1.0, 2048, tabs)
+    c.value_seeds = [W.value_seed(144, t) for t in range(c.T)]
+    wd = filled_tables(c, W.VAL_INTEGER)
+    batch = W.gen_batch(c, 0)
+    edge = (1 << 32) // 512
+    for t in (0, 1):
+        lo, hi = batch.offsets[t * c.batch], batch.offsets[(t + 1) * c.batch]
+        batch.indices[lo:lo + 6] = [edge - 1, edge, edge + 1, 0, c.rows[t] - 1, edge - 2]
+    p = plan_for(c, c.batch).bind(wd)
+    idx, off = to_device(batch)
+    out = torch.full((c.batch, c.T, c.E), float("nan"), device="cuda")
+    p.lookup(idx, off, c.batch, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    assert not np.isnan(got).any()
+    check_sampled(c, got, batch, 3 * c.batch, seed=5, mode=W.VAL_INTEGER, exact=True)
+    # the bags holding the boundary ids, checked one by one
+    for t in (0, 1):
+        bags = [0, 1] if t == 0 else list(range(6))
+        for b in bags:
+            a0, a1 = batch.offsets[t * c.batch + b], batch.offsets[t * c.batch + b + 1]
+            rows = W.table_rows_at(t, batch.indices[a0:a1], c.E, c.dtype, seed=c.value_seeds[t], mode=W.VAL_INTEGER)
+            assert np.array_equal(got[b, t], rows.astype(np.float64).sum(axis=0).astype(np.float32)), (t, b)
+    assert p.check_errors() == 0
