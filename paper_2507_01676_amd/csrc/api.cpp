@@ -47,6 +47,7 @@ struct emb_plan {
   const char* d_zero_row = nullptr;      // R zero bytes
   bool staged = false;                   // the plan has LDS / HOT / DEDUP / STREAM slices
   bool wave_gather = false;              // launches the wave-uniform gather kernel (gather.hip)
+  int block = kBlock;                    // threads per worker
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
   std::vector<int32_t> mean;             // per table: 1 = mean pooling
   int32_t gather_runs[3] = {0, 0, 0};    // runs per gather queue class, over all workers
@@ -203,6 +204,43 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
     delete p;
     return st(rc);
   }
+  // A gather-only plan with rows of 16, 32 or 64 lanes runs the wave-uniform gather kernel
+  // (EMBX_GATHER_KERNEL=classic keeps the sub-wavefront walkers, for comparison).  That
+  // kernel's workers are smaller workgroups (kWaveBlock threads, EMBX_WAVE_BLOCK overrides),
+  // as many per CU as its registers allow; unless the caller fixed the worker count, the
+  // plan is made again for that many workers, and kept if it is still gather-only.
+  const int G0 = lanes_per_row(p->plan.R);
+  auto gather_only = [](const PlanOut& P0) {
+    for (const PSlice& x : P0.slices)
+      if (x.strat != S_GATHER) return false;
+    return true;
+  };
+  const char* env_kernel = std::getenv("EMBX_GATHER_KERNEL");
+  bool wave_gather = (G0 == 16 || G0 == 32 || G0 == 64) && gather_only(p->plan) &&
+                     !(env_kernel && std::strcmp(env_kernel, "classic") == 0);
+  int block = kBlock;
+  if (wave_gather) {
+    const char* env_block = std::getenv("EMBX_WAVE_BLOCK");
+    block = env_block ? std::atoi(env_block) : kWaveBlock;
+    if (block < 64 || block > kBlock || block % 64 != 0) block = kWaveBlock;
+    if (!(opts && (opts->num_workers > 0 || opts->wg_per_cu > 0))) {
+      const int bpc = gather_blocks_per_cu(G0, dtype == EMB_DTYPE_F16, block);
+      if (bpc < 1) {
+        delete p;
+        return EMB_ERR_DEVICE;
+      }
+      const int K2 = cus * bpc;
+      if (K2 != K && K2 <= 65535) {
+        PlanIn in2 = in;
+        in2.K = K2;
+        PlanOut plan2;
+        if (build_plan(in2, &plan2, &err) == 0 && gather_only(plan2)) {
+          p->plan = plan2;
+          K = K2;
+        }
+      }
+    }
+  }
   const PlanOut& P = p->plan;
   p->device = dev;
   p->T = num_tables;
@@ -335,14 +373,13 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   // (8) and at most 128; wave-mode chunks carry about four wavefront steps of lookups,
   // fewer when that leaves some of the 16 wavefronts without one.
   //
-  // A gather-only plan with rows of 16, 32 or 64 lanes runs the wave-uniform gather kernel
-  // instead (EMBX_GATHER_KERNEL=classic keeps the sub-wavefront walkers, for comparison):
-  // its queues are single-lookup bags (chunks of one wavefront step: 8 S bags) and all
-  // other bags (chunks of about sqrt(8 W / 16) expected lookups, W the worker's lookups
-  // in that queue, between two wavefront steps and 2048; EMBX_WAVE_CHUNK overrides it).
-  const char* env_kernel = std::getenv("EMBX_GATHER_KERNEL");
-  const bool wave_gather = !staged && (p->G == 16 || p->G == 32 || p->G == 64) &&
-                           !(env_kernel && std::strcmp(env_kernel, "classic") == 0);
+  // The wave-uniform gather kernel's queues are single-lookup bags (chunks of one wavefront
+  // step: 8 S bags) and all other bags, in chunks of about 128 expected lookups, 192 when
+  // the worker's queue gives each wavefront at least 64 chunks (W / 16 >= 64 * 192, W the
+  // worker's lookups in that queue), and at least two wavefront steps (EMBX_WAVE_CHUNK
+  // overrides it).  Measured on workloads 3-5: shorter chunks keep a worker's wavefronts
+  // on fewer tables at a time, so their rows share L2; much shorter ones pay the per-chunk
+  // start (workload 5: 4358 us at 64 lookups, 4042 at 192, 4170 at 512).
   const char* env_chunk = std::getenv("EMBX_WAVE_CHUNK");
   const double wave_chunk_override = env_chunk ? std::atof(env_chunk) : 0.0;
   std::vector<GatherRun> gr;                       // runs, worker-major
@@ -351,7 +388,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   int max_runs = 0;
   {
     const int nsw = kBlock / p->G;
-    const int nwaves = kBlock / 64;
+    const int nwaves = block / 64;
     const double wave_chunk = 4.0 * 8.0 * (64 / p->G);
     auto slice_bags = [&](const DevItem& d) -> int64_t {
       return (static_cast<int64_t>(d.j + 1) * max_batch) / d.k - (static_cast<int64_t>(d.j) * max_batch) / d.k;
@@ -390,7 +427,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
       const double target =
           !wave_gather ? std::min(128.0, std::max(8.0, std::floor(std::sqrt(5.0 * Ws / nsw))))
           : wave_chunk_override > 0.0 ? wave_chunk_override
-                                      : std::min(2048.0, std::max(2.0 * wstep, std::floor(std::sqrt(8.0 * Ws / nwaves))));
+                                      : std::max(2.0 * wstep, Ws / nwaves >= 64.0 * 192.0 ? 192.0 : 128.0);
       const double wtarget = std::min(wave_chunk, std::max(1.0, std::floor(Ww / nwaves)));
       gr_ptr[w] = static_cast<int32_t>(gr.size());
       int64_t base[3] = {0, 0, 0};
@@ -501,6 +538,7 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   const int run_bytes = p->gr_slot * static_cast<int>(sizeof(GatherRun));
   p->staged = staged;
   p->wave_gather = wave_gather;
+  p->block = block;
   p->lds_bytes = std::max(staged ? static_cast<int>(L) + kMetaReserve : 0, run_bytes);
   if (prepare_lookup_kernels(dev, static_cast<int>(smem) - kStaticLdsReserve) != 0) {
     emb_plan_destroy(p);
@@ -563,7 +601,8 @@ emb_status_t lookup_impl(emb_plan_t* plan, const int64_t* indices, const int64_t
   a.zero_row = plan->d_zero_row;
   a.one = 1.0f;
   a.weights = weighted ? weights : nullptr;
-  if (plan->wave_gather) return st(launch_gather(a, plan->G, plan->f16, weighted, plan->K, plan->lds_bytes, stream));
+  if (plan->wave_gather)
+    return st(launch_gather(a, plan->G, plan->f16, weighted, plan->K, plan->block, plan->lds_bytes, stream));
   return st(launch_lookup(a, plan->G, plan->f16, plan->staged, weighted, plan->K, plan->lds_bytes, stream));
 }
 
@@ -615,7 +654,7 @@ emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info) {
   info->dtype = plan->f16 ? EMB_DTYPE_F16 : EMB_DTYPE_F32;
   info->row_bytes = plan->R;
   info->num_workers = plan->K;
-  info->block_threads = kBlock;
+  info->block_threads = plan->block;
   info->lds_bytes = plan->lds_bytes;
   info->num_items = static_cast<int32_t>(plan->plan.slices.size());
   info->max_batch = plan->Bmax;

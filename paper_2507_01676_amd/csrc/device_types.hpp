@@ -7,6 +7,7 @@
 namespace embx {
 
 constexpr int kBlock = 1024;        // threads per worker (16 wave64s: one worker per CU)
+constexpr int kWaveBlock = 1024;    // threads per worker of the wave-uniform gather kernel
 constexpr int kTile = 2048;         // DEDUP: lookups per sorted tile
 constexpr int kMetaReserve = 28928;   // LDS beyond the row budget: hot hash or dedup tile
 
@@ -107,7 +108,11 @@ GatherKernelFn gather_kernel_f16_weighted(int G);
 // Host-callable launchers (defined in lookup.hip).
 int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
                   void* stream);
-int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int lds_bytes, void* stream);
+int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int block, int lds_bytes,
+                  void* stream);
+// workgroups of `block` threads of the gather kernels for rows of G lanes that fit on one CU
+// at once (the smaller of the weighted and unweighted kernel's), 0 on error
+int gather_blocks_per_cu(int G, bool f16, int block);
 // once per device: lets every lookup kernel launch with up to max_dynamic_lds bytes of
 // dynamic LDS (0 = done, else an emb_status_t code)
 int prepare_lookup_kernels(int device, int max_dynamic_lds);

@@ -35,6 +35,9 @@
 #ifndef EMBX_GPART
 #define EMBX_GPART -1
 #endif
+#ifndef EMBX_NT_IDS
+#define EMBX_NT_IDS 0
+#endif
 #define EMBX_HAS_GPART(p) (EMBX_GPART < 0 || EMBX_GPART == (p))
 
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -46,21 +49,23 @@
 #endif
 
 namespace embx {
-namespace {
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // structured buffer load of 16 bytes: base + vindex * stride + voffset (buffer descriptor
 // in scalar registers; an access past num_records reads zeros)
 __device__ i32x4 buffer_load_row(i32x4 rsrc, int vindex, int voffset, int soffset, int aux)
     __asm("llvm.amdgcn.struct.buffer.load.v4i32");
 
+namespace {
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+
 constexpr int kSteps = 8;            // row loads in flight per lane per step
-constexpr int kWaves = kBlock / 64;  // wavefronts per worker
 constexpr int64_t kNoEnd = INT64_MAX;
 
 // Buffer descriptor of a table: rows of R bytes from base; num_records = rows (the
@@ -79,7 +84,7 @@ __device__ __forceinline__ i32x4 table_rsrc(const void* base, int R, uint32_t ro
 // lane u of this lane's row of 16 (DPP row_newbcast:u)
 template <int U>
 __device__ __forceinline__ int row_bcast(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, 0x150 + U, 0xF, 0xF, false);
+  return __builtin_amdgcn_mov_dpp(v, 0x150 + U, 0xF, 0xF, true);
 }
 
 __device__ __forceinline__ int64_t uni64(int64_t v) {
@@ -202,13 +207,14 @@ struct WaveQueue {
   int e, e_end, nchunks, B;
   LMEM int* ctr;
   int first;    // this wavefront's first chunk, -1 once taken
+  int waves;    // wavefronts of the worker
   __device__ __forceinline__ int claim() {
     if (first >= 0) {
       const int v = first;
       first = -1;
       return v;
     }
-    if (nchunks <= kWaves) return nchunks;
+    if (nchunks <= waves) return nchunks;
     int v = 0;
     if ((threadIdx.x & 63) == 0) v = atomicAdd(ctr, 1);
     return __builtin_amdgcn_readfirstlane(v);   // lane 0 (every lane is active here)
@@ -230,43 +236,91 @@ struct WaveQueue {
   }
 };
 
-// Per-chunk constants of a table, wave-uniform.  Tables of 4 GiB or more are read with
-// 64-bit addresses (the buffer unit's offset arithmetic is 32 bits wide).
+// Per-chunk constants of a table, wave-uniform: the buffer descriptor of its rows (base,
+// stride R, num_records = rows), the table id and flags.  Tables of 4 GiB or more are read
+// with 64-bit addresses (the buffer unit's offset arithmetic is 32 bits wide).
 struct RunInfo {
   i32x4 rsrc;
-  GMEM const char* wb;       // table base (global loads of big tables)
-  bool big;                  // rows * R >= 2^32
-  uint64_t rows;
-  GMEM const int64_t* off;   // the table's CSR offsets
-  GMEM float* ob;            // out + table * E
-  bool mean;
+  int table;
+  int flags;   // bit 0: mean pooling; bit 1: rows * R >= 2^32
+  __device__ __forceinline__ uint64_t rows() const { return static_cast<uint32_t>(rsrc.z); }
+  __device__ __forceinline__ bool mean() const { return (flags & 1) != 0; }
+  __device__ __forceinline__ bool big() const { return (flags & 2) != 0; }
+  __device__ __forceinline__ GMEM const char* base() const {
+    const uint64_t b = (static_cast<uint64_t>(static_cast<uint32_t>(rsrc.y) & 0xffffu) << 32) |
+                       static_cast<uint32_t>(rsrc.x);
+    return (GMEM const char*)b;
+  }
 };
 
-// row `row` of the table, this lane's 16 bytes (lane_c: byte offset in the row)
-__device__ __forceinline__ i32x4 load_row(const RunInfo& ri, int row, int lane_c, int R) {
-  if (ri.big)
-    return *reinterpret_cast<GMEM const i32x4*>(ri.wb + static_cast<uint64_t>(static_cast<uint32_t>(row)) * R + lane_c);
-  return buffer_load_row(ri.rsrc, row, lane_c, 0, 0);
-}
+#define CMEM __attribute__((address_space(4)))
 
 __device__ __forceinline__ RunInfo run_info(const LMEM GatherRun* runs, int e, const LookupArgs& a) {
   const LMEM GatherRun& g = runs[e];
-  RunInfo ri;
-  const uint64_t w = (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(
-                          static_cast<int>(reinterpret_cast<uint64_t>(g.w) >> 32))) << 32) |
+  const uint64_t w = (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(
+                          static_cast<int>(reinterpret_cast<uint64_t>(g.w) >> 32)))) << 32) |
                      static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(
                          static_cast<int>(reinterpret_cast<uint64_t>(g.w) & 0xffffffffu)));
-  const int64_t rows = (static_cast<int64_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(g.rows >> 32))) << 32) |
-                       static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(g.rows & 0xffffffff)));
-  const int table = __builtin_amdgcn_readfirstlane(g.table);
-  ri.rsrc = table_rsrc(reinterpret_cast<const void*>(w), a.R, static_cast<uint32_t>(rows));
-  ri.wb = (GMEM const char*)(reinterpret_cast<const char*>(w));
-  ri.big = static_cast<uint64_t>(rows) * static_cast<uint64_t>(a.R) >= (uint64_t(1) << 32);
-  ri.rows = static_cast<uint64_t>(rows);
-  ri.off = as_global(a.offsets) + static_cast<int64_t>(table) * a.B;
-  ri.ob = as_global(a.out) + static_cast<int64_t>(table) * a.E;
-  ri.mean = __builtin_amdgcn_readfirstlane(g.mean) != 0;
+  const uint32_t rows = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(g.rows & 0xffffffff)));
+  RunInfo ri;
+  ri.rsrc = table_rsrc(reinterpret_cast<const void*>(w), a.R, rows);
+  ri.table = __builtin_amdgcn_readfirstlane(g.table);
+  ri.flags = (__builtin_amdgcn_readfirstlane(g.mean) != 0 ? 1 : 0) |
+             (static_cast<uint64_t>(rows) * static_cast<uint64_t>(a.R) >= (uint64_t(1) << 32) ? 2 : 0);
   return ri;
+}
+
+// row `row` of the table, this lane's 16 bytes (lane_c: byte offset in the row)
+__device__ __forceinline__ i32x4 load_row(const RunInfo& ri, int row, int lane_c, int R) {
+  if (ri.big())
+    return *reinterpret_cast<GMEM const i32x4*>(ri.base() +
+                                                static_cast<uint64_t>(static_cast<uint32_t>(row)) * static_cast<uint32_t>(R) +
+                                                lane_c);
+  return buffer_load_row(ri.rsrc, row, lane_c, 0, 0);
+}
+
+// kSteps rows, one per instruction u, row id broadcast from lane u of this lane's row of 16
+#define EMBX_ISSUE_ROWS(RI, ROW, RAW)                                                                      \
+  if ((RI).big()) {                                                                                        \
+    GMEM const char* const wb_ = (RI).base() + lane_c;                                                    \
+    RAW[0] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<0>(ROW))) * static_cast<uint32_t>(R)); \
+    RAW[1] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<1>(ROW))) * static_cast<uint32_t>(R)); \
+    RAW[2] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<2>(ROW))) * static_cast<uint32_t>(R)); \
+    RAW[3] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<3>(ROW))) * static_cast<uint32_t>(R)); \
+    RAW[4] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<4>(ROW))) * static_cast<uint32_t>(R)); \
+    RAW[5] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<5>(ROW))) * static_cast<uint32_t>(R)); \
+    RAW[6] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<6>(ROW))) * static_cast<uint32_t>(R)); \
+    RAW[7] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<7>(ROW))) * static_cast<uint32_t>(R)); \
+  } else {                                                                                                 \
+    RAW[0] = buffer_load_row((RI).rsrc, row_bcast<0>(ROW), lane_c, 0, 0);                                  \
+    RAW[1] = buffer_load_row((RI).rsrc, row_bcast<1>(ROW), lane_c, 0, 0);                                  \
+    RAW[2] = buffer_load_row((RI).rsrc, row_bcast<2>(ROW), lane_c, 0, 0);                                  \
+    RAW[3] = buffer_load_row((RI).rsrc, row_bcast<3>(ROW), lane_c, 0, 0);                                  \
+    RAW[4] = buffer_load_row((RI).rsrc, row_bcast<4>(ROW), lane_c, 0, 0);                                  \
+    RAW[5] = buffer_load_row((RI).rsrc, row_bcast<5>(ROW), lane_c, 0, 0);                                  \
+    RAW[6] = buffer_load_row((RI).rsrc, row_bcast<6>(ROW), lane_c, 0, 0);                                  \
+    RAW[7] = buffer_load_row((RI).rsrc, row_bcast<7>(ROW), lane_c, 0, 0);                                  \
+  }
+static_assert(kSteps == 8, "EMBX_ISSUE_ROWS issues eight rows");
+
+// Lane constants of a walker.
+struct LaneConst {
+  int lane, sw, lane_sw, lane_c, pos_l;
+  bool active, loads, counts;
+};
+
+template <int G>
+__device__ __forceinline__ LaneConst lane_const(int R) {
+  LaneConst l;
+  l.lane = threadIdx.x & 63;
+  l.sw = l.lane / G;
+  l.lane_sw = l.lane & (G - 1);
+  l.active = l.lane_sw * 16 < R;
+  l.lane_c = l.active ? l.lane_sw * 16 : 0;
+  l.pos_l = (l.lane & 15) * (64 / G) + l.sw;   // lookup (or bag) u S + s of instruction u = lane & 15
+  l.loads = (l.lane & 15) < kSteps;
+  l.counts = l.loads && l.lane_sw < 16;         // one copy of each id is counted
+  return l;
 }
 
 // ---------------------------------------------------------------- multi-lookup bags
@@ -277,121 +331,98 @@ struct Multi {
   static constexpr int NA = F16 ? 8 : 4;
   static constexpr int N = S * kSteps;   // lookups per step
 
-  // lane constants
   int lane, sw, lane_sw, lane_c, pos_l;
   bool active, loads, counts;
-  GMEM const int64_t* indices;
-  GMEM const float* wts;
-  GMEM unsigned long long* err;
-  float one;
-  int64_t ostride;
   int R;
+  int64_t ostride;
 
   __device__ __forceinline__ void init(const LookupArgs& a) {
+    const LaneConst l = lane_const<G>(a.R);
+    lane = l.lane;
+    sw = l.sw;
+    lane_sw = l.lane_sw;
+    lane_c = l.lane_c;
+    pos_l = l.pos_l;
+    active = l.active;
+    loads = l.loads;
+    counts = l.counts;
     R = a.R;
-    lane = threadIdx.x & 63;
-    sw = lane / G;
-    lane_sw = lane & (G - 1);
-    active = lane_sw * 16 < a.R;
-    lane_c = active ? lane_sw * 16 : 0;
-    pos_l = (lane & 15) * S + sw;
-    loads = (lane & 15) < kSteps;
-    counts = loads && lane_sw < 16;   // one copy of each id is counted
-    indices = as_global(a.indices);
-    wts = as_global(a.weights);
-    err = as_global(a.err);
-    one = a.one;
     ostride = static_cast<int64_t>(a.T) * a.E;
   }
 
   // ids (and weights) of lookups p + pos_l, those below pend
-  __device__ __forceinline__ void load_ids(int64_t p, int64_t pend, int64_t& id, float& wt) const {
+  __device__ __forceinline__ void load_ids(const LookupArgs& a, int64_t p, int64_t pend, int64_t& id, float& wt) const {
     const bool ok = loads && p + pos_l < pend;
-    id = ok ? indices[p + pos_l] : int64_t(-1);
-    if constexpr (W) wt = ok ? wts[p + pos_l] : 0.0f;
+#if EMBX_NT_IDS
+    // a step's ids fill whole lines that no other step or wavefront reads
+    id = ok ? __builtin_nontemporal_load(as_global(a.indices) + p + pos_l) : int64_t(-1);
+    if constexpr (W) wt = ok ? __builtin_nontemporal_load(as_global(a.weights) + p + pos_l) : 0.0f;
+#else
+    id = ok ? as_global(a.indices)[p + pos_l] : int64_t(-1);
+    if constexpr (W) wt = ok ? as_global(a.weights)[p + pos_l] : 0.0f;
+#endif
   }
 
   __device__ void walk(const LookupArgs& a, const LMEM GatherRun* runs, WaveQueue& q) {
+    const CMEM int64_t* const coff = (const CMEM int64_t*)a.offsets;
     Chunk cur = q.next();
     if (cur.run < 0) return;
     RunInfo ri = run_info(runs, cur.run, a);
-    // head of the current chunk: its first and end positions, ends of its first bags
-    int64_t p = ri.off[cur.bs];
-    int64_t pend = ri.off[cur.be];
-    int wb = cur.bs;   // win: offsets[wb + 1 + lane]
-    int64_t win = ri.off[min(cur.bs + 1 + lane, cur.be)];
-    // the next chunk's head, loaded while this one is walked
+    // the chunk's head (scalar loads): first and end positions, end of its first bag
+    int64_t p = coff[static_cast<int64_t>(ri.table) * a.B + cur.bs];
+    int64_t pend = coff[static_cast<int64_t>(ri.table) * a.B + cur.be];
+    int64_t e = coff[static_cast<int64_t>(ri.table) * a.B + cur.bs + 1];
+    // win: ends of bags wb + 1 + lane (vector), for the steps' bag ends
+    int wb = cur.bs;
+    int64_t win = as_global(a.offsets)[static_cast<int64_t>(ri.table) * a.B + min(cur.bs + 1 + lane, cur.be)];
+    // the next chunk's head, loaded while this one is walked (its descriptor is formed
+    // again from the run record at the switch)
     Chunk nxt = q.next();
-    RunInfo rn;
-    int64_t np = 0, npend = 0, nwin = 0;
+    int64_t np = 0, npend = 0, ne = 0;
     if (nxt.run >= 0) {
-      rn = run_info(runs, nxt.run, a);
-      np = rn.off[nxt.bs];
-      npend = rn.off[nxt.be];
-      nwin = rn.off[min(nxt.bs + 1 + lane, nxt.be)];
+      const int64_t tb = static_cast<int64_t>(__builtin_amdgcn_readfirstlane(runs[nxt.run].table)) * a.B;
+      np = coff[tb + nxt.bs];
+      npend = coff[tb + nxt.be];
+      ne = coff[tb + nxt.bs + 1];
     }
-    wait_all();
-    p = uni64(p);
-    pend = uni64(pend);
     int64_t id;
     float wt = 0.0f;
-    load_ids(p, pend, id, wt);
-    bool ids_ready = false;   // the ids of the next step are already in flight
+    load_ids(a, p, pend, id, wt);
     Acc<F16> acc;
     acc_zero(acc);
     int b = cur.bs, be = cur.be;
     int64_t bstart = p;
-    int64_t e = lane64(win, 0);   // end of bag b
     wait_all();
     while (true) {
       // ---- chunk cur: bags [b, be), positions [p, pend); ids of [p, p + N) in `id`
+      bool ids_ready = false;   // the first ids of the next chunk are in flight
       while (p < pend) {
         const int n = static_cast<int>(min(static_cast<int64_t>(N), pend - p));
         const bool okp = loads && pos_l < n;
-        const bool ok = okp && static_cast<uint64_t>(id) < ri.rows;
+        const bool ok = okp && static_cast<uint64_t>(id) < ri.rows();
         const int row = ok ? static_cast<int>(id) : 0;
         const uint64_t badm = __ballot(okp && !ok && counts);
         float wl = 0.0f;
         if constexpr (W) wl = ok ? wt : 0.0f;
         i32x4 raw[kSteps];
-        float wu[kSteps];
-        if (ri.big) {
-#define EMBX_ISSUE(U)                                                                                    \
-  raw[U] = *reinterpret_cast<GMEM const i32x4*>(                                                         \
-      ri.wb + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<U>(row))) * R + lane_c);
-          EMBX_ISSUE(0) EMBX_ISSUE(1) EMBX_ISSUE(2) EMBX_ISSUE(3)
-          EMBX_ISSUE(4) EMBX_ISSUE(5) EMBX_ISSUE(6) EMBX_ISSUE(7)
-#undef EMBX_ISSUE
-        } else {
-#define EMBX_ISSUE(U) raw[U] = buffer_load_row(ri.rsrc, row_bcast<U>(row), lane_c, 0, 0);
-          EMBX_ISSUE(0) EMBX_ISSUE(1) EMBX_ISSUE(2) EMBX_ISSUE(3)
-          EMBX_ISSUE(4) EMBX_ISSUE(5) EMBX_ISSUE(6) EMBX_ISSUE(7)
-#undef EMBX_ISSUE
-        }
-#pragma unroll
-        for (int u = 0; u < kSteps; ++u) wu[u] = one;
-        if constexpr (W) {
-#define EMBX_W(U) wu[U] = __int_as_float(row_bcast<U>(__float_as_int(wl)));
-          EMBX_W(0) EMBX_W(1) EMBX_W(2) EMBX_W(3) EMBX_W(4) EMBX_W(5) EMBX_W(6) EMBX_W(7)
-#undef EMBX_W
-        }
-        const bool anybad = __ballot(okp && !ok) != 0;
+        EMBX_ISSUE_ROWS(ri, row, raw)
         // ids of the next step: more of this chunk, or the start of the next one
         const int64_t pn = p + n;
         if (pn < pend) {
-          load_ids(pn, pend, id, wt);
-          ids_ready = false;
+          load_ids(a, pn, pend, id, wt);
         } else if (nxt.run >= 0) {
-          load_ids(uni64(np), uni64(npend), id, wt);
+          load_ids(a, np, npend, id, wt);
           ids_ready = true;
         }
         // ends of the next 64 bags when the window runs short
         const bool slide = b - wb >= 32;
-        if (slide) win = ri.off[min(b + 1 + lane, be)];
+        if (slide) win = as_global(a.offsets)[static_cast<int64_t>(ri.table) * a.B + min(b + 1 + lane, be)];
         wait_all();   // the one wait of the step
         if (slide) wb = b;
-        if (badm != 0 && (lane & 63) == 0) atomicAdd(err, static_cast<unsigned long long>(__popcll(badm)));
-        if (anybad) {   // an out-of-range id adds nothing
+        if (badm != 0) {   // an out-of-range id is counted and adds nothing
+          if (lane == 0) atomicAdd(as_global(a.err), static_cast<unsigned long long>(__popcll(badm)));
+        }
+        if (__ballot(okp && !ok) != 0) {
           const int okv = ok ? 1 : 0;
 #define EMBX_MASK(U) if (!row_bcast<U>(okv)) raw[U] = zero4();
           EMBX_MASK(0) EMBX_MASK(1) EMBX_MASK(2) EMBX_MASK(3)
@@ -399,7 +430,10 @@ struct Multi {
 #undef EMBX_MASK
         }
         // additions in lookup order per SW; bag ends are wave-uniform
-#define EMBX_ADD(U) add_instr(acc, raw[U], wu[U], p + (U) * S, pn, ri, b, be, e, bstart, wb, win);
+        const int wlb = __float_as_int(wl);
+#define EMBX_ADD(U)                                                                              \
+  add_instr(a, acc, raw[U], W ? __int_as_float(row_bcast<U>(wlb)) : a.one, p + (U) * S, pn, ri, b, be, e, \
+            bstart, wb, win);
         EMBX_ADD(0) EMBX_ADD(1) EMBX_ADD(2) EMBX_ADD(3)
         EMBX_ADD(4) EMBX_ADD(5) EMBX_ADD(6) EMBX_ADD(7)
 #undef EMBX_ADD
@@ -408,41 +442,42 @@ struct Multi {
       // bags left at the chunk's end: one whose last lookup closed the final step (its
       // sum is in acc), then empty ones
       while (b < be) {
-        finish(acc, ri, b, pend - bstart);
+        finish(a, acc, ri, b, pend - bstart);
         bstart = pend;
         ++b;
       }
       // ---- next chunk
       if (nxt.run < 0) return;
       cur = nxt;
-      ri = rn;
-      p = uni64(np);
-      pend = uni64(npend);
-      win = nwin;
+      ri = run_info(runs, cur.run, a);
+      p = np;
+      pend = npend;
+      e = ne;
       wb = cur.bs;
       b = cur.bs;
       be = cur.be;
       bstart = p;
-      e = b < be ? lane64(win, 0) : kNoEnd;
-      if (!ids_ready) load_ids(p, pend, id, wt);
+      win = as_global(a.offsets)[static_cast<int64_t>(ri.table) * a.B + min(cur.bs + 1 + lane, cur.be)];
       nxt = q.next();
       if (nxt.run >= 0) {
-        rn = run_info(runs, nxt.run, a);
-        np = rn.off[nxt.bs];
-        npend = rn.off[nxt.be];
-        nwin = rn.off[min(nxt.bs + 1 + lane, nxt.be)];
+        const int64_t tb = static_cast<int64_t>(__builtin_amdgcn_readfirstlane(runs[nxt.run].table)) * a.B;
+        np = coff[tb + nxt.bs];
+        npend = coff[tb + nxt.be];
+        ne = coff[tb + nxt.bs + 1];
       }
-      wait_all();
-      ids_ready = false;
+      if (!ids_ready) {
+        load_ids(a, p, pend, id, wt);
+        wait_all();
+      }
     }
   }
 
   // Instruction u of a step: lookups qpos + s, one per SW s (those below pn).  Bags
   // ending inside it split its SWs: SWs before the end add to the ending bag, the others
   // to the next one.
-  __device__ __forceinline__ void add_instr(Acc<F16>& acc, const i32x4 x, float w, int64_t qpos, int64_t pn,
-                                            const RunInfo& ri, int& b, int be, int64_t& e, int64_t& bstart, int& wb,
-                                            int64_t& win) const {
+  __device__ __forceinline__ void add_instr(const LookupArgs& a, Acc<F16>& acc, const i32x4 x, float w, int64_t qpos,
+                                            int64_t pn, const RunInfo& ri, int& b, int be, int64_t& e,
+                                            int64_t& bstart, int& wb, int64_t& win) const {
     if (qpos >= pn) return;
     if (e >= qpos + S) {
       acc_add(acc, x, w);
@@ -452,7 +487,7 @@ struct Multi {
     while (e < qpos + S) {
       const int k = static_cast<int>(e - qpos);
       if (sw >= lo && sw < k) acc_add(acc, x, w);
-      finish(acc, ri, b, e - bstart);
+      finish(a, acc, ri, b, e - bstart);
       ++b;
       bstart = e;
       lo = k;
@@ -462,7 +497,7 @@ struct Multi {
       }
       if (b - wb >= 64) {   // more bag ends in this step than the window holds
         wb = b;
-        win = ri.off[min(b + 1 + lane, be)];
+        win = as_global(a.offsets)[static_cast<int64_t>(ri.table) * a.B + min(b + 1 + lane, be)];
         wait_all();
       }
       e = lane64(win, b - wb);
@@ -471,15 +506,19 @@ struct Multi {
   }
 
   // bag b is complete in acc (len lookups): combine the SWs, scale a mean, store, clear
-  __device__ __forceinline__ void finish(Acc<F16>& acc, const RunInfo& ri, int b, int64_t len) const {
+  __device__ __forceinline__ void finish(const LookupArgs& a, Acc<F16>& acc, const RunInfo& ri, int b,
+                                         int64_t len) const {
     reduce_scatter<S, NA>(acc.v);
     constexpr int P = NA / S;
-    if (ri.mean && len > 1) {
+    if (ri.mean() && len > 1) {
       const float s = 1.0f / static_cast<float>(len);
 #pragma unroll
       for (int i = 0; i < P; ++i) acc.v[i] *= s;
     }
-    if (active) store_part<P>(ri.ob + static_cast<int64_t>(b) * ostride + NA * lane_sw + P * sw, acc.v);
+    if (active)
+      store_part<P>(as_global(a.out) + static_cast<int64_t>(ri.table) * a.E + static_cast<int64_t>(b) * ostride +
+                        NA * lane_sw + P * sw,
+                    acc.v);
     acc_zero(acc);
   }
 };
@@ -487,8 +526,7 @@ struct Multi {
 // ---------------------------------------------------------------- single-lookup bags
 
 template <int G, bool F16, bool W>
-__device__ __forceinline__ void single_slow(const RunInfo& ri, int bs, int be, int64_t st_l, int64_t en_l,
-                                            const LookupArgs& a);
+__device__ __forceinline__ void single_slow(const LookupArgs& a, const RunInfo& ri, int bs, int be);
 
 template <int G, bool F16, bool W>
 struct Single {
@@ -498,120 +536,109 @@ struct Single {
 
   int lane, sw, lane_sw, lane_c, pos_l;
   bool active, loads, counts;
-  GMEM const int64_t* indices;
-  GMEM const float* wts;
-  GMEM unsigned long long* err;
-  float one;
-  int64_t ostride;
   int R;
+  int64_t ostride;
 
   __device__ __forceinline__ void init(const LookupArgs& a) {
+    const LaneConst l = lane_const<G>(a.R);
+    lane = l.lane;
+    sw = l.sw;
+    lane_sw = l.lane_sw;
+    lane_c = l.lane_c;
+    pos_l = l.pos_l;
+    active = l.active;
+    loads = l.loads;
+    counts = l.counts;
     R = a.R;
-    lane = threadIdx.x & 63;
-    sw = lane / G;
-    lane_sw = lane & (G - 1);
-    active = lane_sw * 16 < a.R;
-    lane_c = active ? lane_sw * 16 : 0;
-    pos_l = (lane & 15) * S + sw;
-    loads = (lane & 15) < kSteps;
-    counts = loads && lane_sw < 16;
-    indices = as_global(a.indices);
-    wts = as_global(a.weights);
-    err = as_global(a.err);
-    one = a.one;
     ostride = static_cast<int64_t>(a.T) * a.E;
   }
 
-  // a chunk in flight: its table and, per lane, bag bs + pos_l's first and end positions
-  struct Stage {
-    Chunk c;
-    RunInfo ri;
-    int64_t st, en;
-  };
-
-  __device__ __forceinline__ void head(const LMEM GatherRun* runs, const LookupArgs& a, WaveQueue& q, Stage& s) const {
-    s.c = q.next();
-    if (s.c.run < 0) return;
-    s.ri = run_info(runs, s.c.run, a);
-    const int bl = min(s.c.bs + pos_l, s.c.be);
-    s.st = s.ri.off[bl];
-    s.en = s.ri.off[min(bl + 1, s.c.be)];
-  }
-
-  // the first id of each lane's bag (when it has one)
-  __device__ __forceinline__ void load_id(const Stage& s, int64_t& id, float& wt) const {
-    const bool has = loads && s.c.bs + pos_l < s.c.be && s.en > s.st;
-    id = has ? indices[s.st] : int64_t(-1);
-    if constexpr (W) wt = has ? wts[s.st] : 0.0f;
+  // first and end position of this lane's bag of chunk c (vector loads)
+  __device__ __forceinline__ void head(const LookupArgs& a, const RunInfo& ri, const Chunk& c, int64_t& st,
+                                       int64_t& en) const {
+    GMEM const int64_t* off = as_global(a.offsets) + static_cast<int64_t>(ri.table) * a.B;
+    const int bl = min(c.bs + pos_l, c.be);
+    st = off[bl];
+    en = off[min(bl + 1, c.be)];
   }
 
   // A three-stage pipeline over chunks: rows of chunk i, ids of chunk i + 1 and the
-  // head of chunk i + 2 are in flight together, and each iteration waits once.
+  // head of chunk i + 2 are in flight together, and each iteration waits once.  Between
+  // stages a lane keeps only its bag's masks and id.
   __device__ void walk(const LookupArgs& a, const LMEM GatherRun* runs, WaveQueue& q) {
-    Stage s0, s1;
-    head(runs, a, q, s0);
-    if (s0.c.run < 0) return;
+    Chunk c0 = q.next();
+    if (c0.run < 0) return;
+    RunInfo r0 = run_info(runs, c0.run, a);
+    int64_t st, en;
+    head(a, r0, c0, st, en);
     wait_all();
-    int64_t id0 = -1;
+    bool inb0 = loads && c0.bs + pos_l < c0.be;
+    bool has0 = inb0 && en > st;
+    bool multi0 = inb0 && en - st > 1;
+    int64_t id0 = has0 ? as_global(a.indices)[st] : int64_t(-1);
     float w0 = 0.0f;
-    load_id(s0, id0, w0);
-    head(runs, a, q, s1);
+    if constexpr (W) w0 = has0 ? as_global(a.weights)[st] : 0.0f;
+    Chunk c1 = q.next();
+    RunInfo r1;
+    if (c1.run >= 0) {
+      r1 = run_info(runs, c1.run, a);
+      head(a, r1, c1, st, en);
+    }
     wait_all();
     while (true) {
-      // ---- chunk s0: its head and ids have landed
-      const bool inb = loads && s0.c.bs + pos_l < s0.c.be;
-      const bool has = inb && s0.en > s0.st;
-      const bool ok = has && static_cast<uint64_t>(id0) < s0.ri.rows;
-      const bool multi = inb && s0.en - s0.st > 1;
-      const uint64_t badm = __ballot(has && !ok && counts);
+      // ---- chunk c0: its id has landed; chunk c1's head has landed
+      const bool ok = has0 && static_cast<uint64_t>(id0) < r0.rows();
+      const uint64_t badm = __ballot(has0 && !ok && counts);
       const int row = ok ? static_cast<int>(id0) : 0;
       const int okv = ok ? 1 : 0;
       float wl = 0.0f;
       if constexpr (W) wl = ok ? w0 : 0.0f;
       i32x4 raw[kSteps];
-      if (s0.ri.big) {
-#define EMBX_ISSUE(U)                                                                                    \
-  raw[U] = *reinterpret_cast<GMEM const i32x4*>(                                                         \
-      s0.ri.wb + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<U>(row))) * R + lane_c);
-        EMBX_ISSUE(0) EMBX_ISSUE(1) EMBX_ISSUE(2) EMBX_ISSUE(3)
-        EMBX_ISSUE(4) EMBX_ISSUE(5) EMBX_ISSUE(6) EMBX_ISSUE(7)
-#undef EMBX_ISSUE
-      } else {
-#define EMBX_ISSUE(U) raw[U] = buffer_load_row(s0.ri.rsrc, row_bcast<U>(row), lane_c, 0, 0);
-        EMBX_ISSUE(0) EMBX_ISSUE(1) EMBX_ISSUE(2) EMBX_ISSUE(3)
-        EMBX_ISSUE(4) EMBX_ISSUE(5) EMBX_ISSUE(6) EMBX_ISSUE(7)
-#undef EMBX_ISSUE
-      }
+      EMBX_ISSUE_ROWS(r0, row, raw)
+      bool inb1 = false, has1 = false, multi1 = false;
       int64_t id1 = -1;
       float w1 = 0.0f;
-      Stage s2;
-      s2.c.run = -1;
-      if (s1.c.run >= 0) {
-        load_id(s1, id1, w1);
-        head(runs, a, q, s2);
+      Chunk c2;
+      c2.run = -1;
+      RunInfo r2;
+      if (c1.run >= 0) {
+        inb1 = loads && c1.bs + pos_l < c1.be;
+        has1 = inb1 && en > st;
+        multi1 = inb1 && en - st > 1;
+        id1 = has1 ? as_global(a.indices)[st] : int64_t(-1);
+        if constexpr (W) w1 = has1 ? as_global(a.weights)[st] : 0.0f;
+        c2 = q.next();
+        if (c2.run >= 0) {
+          r2 = run_info(runs, c2.run, a);
+          head(a, r2, c2, st, en);
+        }
       }
       wait_all();   // the one wait of the step
-      if (badm != 0 && lane == 0) atomicAdd(err, static_cast<unsigned long long>(__popcll(badm)));
+      if (badm != 0 && lane == 0) atomicAdd(as_global(a.err), static_cast<unsigned long long>(__popcll(badm)));
       // each SW stores its bag's row (zeros for an empty bag or an out-of-range id)
-      const int nb = s0.c.be - s0.c.bs;
-      GMEM float* const ob = s0.ri.ob + NA * lane_sw;
-#define EMBX_STORE(U)                                                                     \
-  {                                                                                       \
-    const int bi = U * S + sw;                                                            \
-    const i32x4 x = row_bcast<U>(okv) ? raw[U] : zero4();                                 \
-    const float wx = W ? __int_as_float(row_bcast<U>(__float_as_int(wl))) : one;          \
-    if (bi < nb && active) store_row(ob + static_cast<int64_t>(s0.c.bs + bi) * ostride, x, wx); \
+      const int nb = c0.be - c0.bs;
+      GMEM float* const ob = as_global(a.out) + static_cast<int64_t>(r0.table) * a.E + NA * lane_sw;
+      const int wlb = __float_as_int(wl);
+#define EMBX_STORE(U)                                                                               \
+  {                                                                                                 \
+    const int bi = U * S + sw;                                                                      \
+    const i32x4 x = row_bcast<U>(okv) ? raw[U] : zero4();                                           \
+    const float wx = W ? __int_as_float(row_bcast<U>(wlb)) : a.one;                                 \
+    if (bi < nb && active) store_row(ob + static_cast<int64_t>(c0.bs + bi) * ostride, x, wx);       \
   }
       EMBX_STORE(0) EMBX_STORE(1) EMBX_STORE(2) EMBX_STORE(3)
       EMBX_STORE(4) EMBX_STORE(5) EMBX_STORE(6) EMBX_STORE(7)
 #undef EMBX_STORE
-      if (__ballot(multi) != 0)
-        single_slow<G, F16, W>(s0.ri, s0.c.bs, s0.c.be, s0.st, s0.en, a);
-      if (s1.c.run < 0) return;
-      s0 = s1;
-      s1 = s2;
+      if (__ballot(multi0) != 0) single_slow<G, F16, W>(a, r0, c0.bs, c0.be);
+      if (c1.run < 0) return;
+      c0 = c1;
+      r0 = r1;
+      has0 = has1;
+      multi0 = multi1;
       id0 = id1;
       w0 = w1;
+      c1 = c2;
+      r1 = r2;
     }
   }
 
@@ -621,54 +648,52 @@ struct Single {
                        static_cast<unsigned>(r.w)};   // fp32 rows are their own output
       __builtin_nontemporal_store(v, reinterpret_cast<GMEM u32x4*>(q));
     } else {
-      Acc<F16> a;
-      acc_zero(a);
-      acc_add(a, r, wt);
-      store_part<NA>(q, a.v);
+      Acc<F16> x;
+      acc_zero(x);
+      acc_add(x, r, wt);
+      store_part<NA>(q, x.v);
     }
   }
 };
 
-// Bags of a single-lookup chunk that hold more than one lookup after all, summed again in
-// lookup order by the SW that stored their first row (the statistics promised at most one
-// lookup per bag).  st_l / en_l: lane 16 r + u holds bag u S + s's first and end position.
+// Bags [bs, be) of a single-lookup chunk that hold more than one lookup after all, summed
+// again in lookup order, each by the SW that stored its first row (the statistics promised
+// at most one lookup per bag).  Rare: the offsets are read again.
 template <int G, bool F16, bool W>
-__device__ __forceinline__ void single_slow(const RunInfo& ri, int bs, int be, int64_t st_l, int64_t en_l,
-                                            const LookupArgs& a) {
+__device__ __forceinline__ void single_slow(const LookupArgs& a, const RunInfo& ri, int bs, int be) {
   constexpr int S = 64 / G;
   constexpr int NA = F16 ? 8 : 4;
-  const int lane = threadIdx.x & 63;
-  const int sw = lane / G;
-  const int lane_sw = lane & (G - 1);
-  const bool active = lane_sw * 16 < a.R;
-  const int lane_c = active ? lane_sw * 16 : 0;
+  const LaneConst l = lane_const<G>(a.R);
   const int64_t ostride = static_cast<int64_t>(a.T) * a.E;
+  GMEM const int64_t* off = as_global(a.offsets) + static_cast<int64_t>(ri.table) * a.B;
   GMEM const int64_t* indices = as_global(a.indices);
   GMEM const float* wts = as_global(a.weights);
-  GMEM unsigned long long* err = as_global(a.err);
   for (int u = 0; u < kSteps; ++u) {
-    const int src = (lane & ~15) | u;
-    const int64_t st = __shfl(st_l, src);
-    const int64_t en = __shfl(en_l, src);
-    const int bi = u * S + sw;
-    if (bi < be - bs && en - st > 1) {
-      Acc<F16> acc;
-      acc_zero(acc);
-      for (int64_t k = st; k < en; ++k) {
-        const int64_t x = indices[k];
-        const bool ok = static_cast<uint64_t>(x) < ri.rows;
-        if (!ok && k > st && lane_sw == 0) atomicAdd(err, 1ull);   // the first id was counted
-        const float wk = W ? (ok ? wts[k] : 0.0f) : a.one;
-        i32x4 r = load_row(ri, ok ? static_cast<int>(x) : 0, lane_c, a.R);
-        if (!ok) r = zero4();
-        acc_add(acc, r, wk);
-      }
-      if (ri.mean) {
-        const float sc = 1.0f / static_cast<float>(en - st);
+    const int bi = u * S + l.sw;
+    if (bs + bi < be) {
+      const int64_t st = off[bs + bi], en = off[bs + bi + 1];
+      if (en - st > 1) {
+        Acc<F16> acc;
+        acc_zero(acc);
+        for (int64_t k = st; k < en; ++k) {
+          const int64_t x = indices[k];
+          const bool ok = static_cast<uint64_t>(x) < ri.rows();
+          if (!ok && k > st && l.lane_sw == 0) atomicAdd(as_global(a.err), 1ull);   // the first id was counted
+          const float wk = W ? (ok ? wts[k] : 0.0f) : a.one;
+          i32x4 r = load_row(ri, ok ? static_cast<int>(x) : 0, l.lane_c, a.R);
+          if (!ok) r = zero4();
+          acc_add(acc, r, wk);
+        }
+        if (ri.mean()) {
+          const float sc = 1.0f / static_cast<float>(en - st);
 #pragma unroll
-        for (int i = 0; i < NA; ++i) acc.v[i] *= sc;
+          for (int i = 0; i < NA; ++i) acc.v[i] *= sc;
+        }
+        if (l.active)
+          store_part<NA>(as_global(a.out) + static_cast<int64_t>(ri.table) * a.E + static_cast<int64_t>(bs + bi) * ostride +
+                             NA * l.lane_sw,
+                         acc.v);
       }
-      if (active) store_part<NA>(ri.ob + static_cast<int64_t>(bs + bi) * ostride + NA * lane_sw, acc.v);
     }
   }
 }
@@ -686,12 +711,13 @@ __global__ void __launch_bounds__(kBlock) gather_kernel(LookupArgs a) {
   if (tw && tid == 0) tw[0] = __builtin_amdgcn_s_memrealtime();
   {   // the worker's slot: a header record, then its runs
     GMEM const char* src = reinterpret_cast<GMEM const char*>(as_global(a.gr) + static_cast<int64_t>(wg) * a.gr_slot);
-    for (int q = tid; q < 3 * a.gr_slot; q += kBlock)
+    for (int q = tid; q < 3 * a.gr_slot; q += static_cast<int>(blockDim.x))
       *reinterpret_cast<LMEM uint4*>(lds + 16 * q) = *reinterpret_cast<GMEM const uint4*>(src + 16 * q);
   }
+  const int waves = static_cast<int>(blockDim.x) >> 6;
   if (tid == 0) {
-    s_ctr[0] = kWaves;
-    s_ctr[1] = kWaves;
+    s_ctr[0] = waves;
+    s_ctr[1] = waves;
   }
   if (tw && tid == 0) tw[1] = __builtin_amdgcn_s_memrealtime();
   __syncthreads();
@@ -703,13 +729,13 @@ __global__ void __launch_bounds__(kBlock) gather_kernel(LookupArgs a) {
   const LMEM GatherRun* runs = reinterpret_cast<const LMEM GatherRun*>(lds + sizeof(GatherRun));
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   if (n_single > 0) {
-    WaveQueue q{runs, 0, n_single, single_chunks, a.B, (LMEM int*)&s_ctr[0], wave};
+    WaveQueue q{runs, 0, n_single, single_chunks, a.B, (LMEM int*)&s_ctr[0], wave, waves};
     Single<G, F16, W> w;
     w.init(a);
     w.walk(a, runs, q);
   }
   if (nr > n_single) {
-    WaveQueue q{runs, n_single, nr, multi_chunks, a.B, (LMEM int*)&s_ctr[1], wave};
+    WaveQueue q{runs, n_single, nr, multi_chunks, a.B, (LMEM int*)&s_ctr[1], wave, waves};
     Multi<G, F16, W> w;
     w.init(a);
     w.walk(a, runs, q);

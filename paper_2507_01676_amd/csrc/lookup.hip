@@ -36,6 +36,7 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -1751,11 +1752,26 @@ int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weight
   return hipGetLastError() == hipSuccess ? 0 : 4;
 }
 
-int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int lds_bytes, void* stream) {
+int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int block, int lds_bytes,
+                  void* stream) {
   GatherKernelFn k = pick_gather_any(G, f16, weighted);
   if (!k) return 2;
-  hipLaunchKernelGGL(k, dim3(grid), dim3(kBlock), lds_bytes, static_cast<hipStream_t>(stream), a);
+  hipLaunchKernelGGL(k, dim3(grid), dim3(block), lds_bytes, static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? 0 : 4;
+}
+
+int gather_blocks_per_cu(int G, bool f16, int block) {
+  int best = 0;
+  for (int w = 0; w < 2; ++w) {
+    GatherKernelFn k = pick_gather_any(G, f16, w != 0);
+    if (!k) return 0;
+    int n = 0;
+    // the run queue's LDS is small against a CU's 160 KiB; 16 KiB is assumed here
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(k), block, 16384) != hipSuccess)
+      return 0;
+    best = w == 0 ? n : std::min(best, n);
+  }
+  return best;
 }
 
 int launch_dedup_probe(const int64_t* idx, int n, int32_t* uniq, int32_t* inv, int32_t* n_uniq, void* stream) {

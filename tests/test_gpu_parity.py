@@ -258,7 +258,9 @@ def test_many_tables_placed_whole(gpu):
     c.value_seeds = [W.value_seed(110, t) for t in range(c.T)]
     batch = W.gen_batch(c, 0)
     hw = host_tables(c, W.VAL_INTEGER)
-    p, got, nbad = run(c, batch, upload_tables(hw))
+    # 256 workers: at the occupancy-sized worker count of the wave gather kernel (several
+    # workgroups per CU) the per-worker share is small enough that these tables are split
+    p, got, nbad = run(c, batch, upload_tables(hw), num_workers=256)
     check_full(got, hw, batch, "f32", exact=True)
     assert nbad == 0
     ks = [int(ln.split()[8]) for ln in p.serialize().splitlines() if ln.startswith("item ")]
@@ -304,9 +306,9 @@ def test_more_gather_slices_per_worker_than_lds_holds_is_refused(gpu):
     T = 3500
     stats = [dict(mean_pooling=20.0, max_pooling=40, hot_rows=[], hot_freq=[], unique_frac=1.0)] * T
     with pytest.raises(gpu.EmbxError) as e:
-        gpu.Plan([100000] * T, 64, "f32", stats, 4096)
+        gpu.Plan([100000] * T, 64, "f32", stats, 4096, num_workers=256)
     assert e.value.code == gpu.ERR_UNSUPPORTED
-    p = gpu.Plan([100000] * T, 64, "f32", stats, 4096, sym_max=-1)
+    p = gpu.Plan([100000] * T, 64, "f32", stats, 4096, sym_max=-1, num_workers=256)
     assert p.info()["num_items"] >= T
     p.close()
 
@@ -325,7 +327,7 @@ def test_run_queue_beyond_64k_of_lds(gpu):
     idx, off = to_device(batch)
     for mode, exact in ((W.VAL_UNIFORM, False), (W.VAL_INTEGER, True)):
         ws = filled_tables(c, mode)
-        p = plan_for(c, c.batch, stats=stats).bind(ws)
+        p = plan_for(c, c.batch, stats=stats, num_workers=256).bind(ws)
         info = p.info()
         log(f"  {T} tables: {info['num_items']} slices, LDS {info['lds_bytes']} B")
         assert info["num_items"] == T * 256 and info["lds_bytes"] > 65536
