@@ -125,6 +125,9 @@ typedef struct {
                                table while the plan has at most this many; < 0: never            */
   const int32_t* pooling;   /* host, T entries of emb_pooling_t, or NULL (all SUM); does not change
                                the placement, only each bag's final scaling                       */
+  int32_t no_replication;   /* 1: no batch splits of any item (replication fixed to 1, as the
+                               paper's solver does, Sec. III-B); with order_mode 1 the plan is
+                               Sec. III-B steps 1-4 as printed; 0: splits allowed (default)       */
 } emb_plan_options_t;
 
 typedef struct emb_plan emb_plan_t;   /* opaque */

@@ -32,7 +32,10 @@ budget for rows):
       cost exceeds the sum of the chunk costs (the speed-up exceeds the number
       of chunks); chunks use the LDS strategy.
   P3  tau = ceil(sum of item costs / K), the ideal per-worker load.
-  P4  an unchunked GATHER item whose k = min(K, B) slices would each hold at
+  P4  (skipped with no_replication: the paper's solver fixes the replication
+      factor to 1, so with order_mode 1 the plan is Sec. III-B steps 1-4 as
+      printed)
+      an unchunked GATHER item whose k = min(K, B) slices would each hold at
       least 64 expected lookups (Lam_t / k >= 64) is split k ways (symmetric
       partitioning, Sec. III-A: a gather slice stages nothing, so every worker
       takes 1/k of every such table and the mix of cache-resident and
@@ -134,6 +137,7 @@ class Options:
     beta: Optional[Sequence[float]] = None
     force: Optional[Sequence[int]] = None
     sym_max: int = 0                  # > 0: GATHER items split symmetrically while at most this many; < 0: never
+    no_replication: bool = False      # True: no batch splits (P4 off), replication factor 1
 
 
 @dataclass
@@ -169,11 +173,13 @@ class Plan:
     lif_milli: int = 0
     r_sym: int = 0
     sym_max: int = 0
+    no_replication: bool = False
 
     def text(self) -> str:
         lines = ["embx-plan v1",
                  f"T {self.T} E {self.E} dtype {self.dtype} R {self.R} K {self.K} L {self.L} B {self.B} "
-                 f"theta {self.theta} order {self.order_mode} symmax {self.sym_max}"]
+                 f"theta {self.theta} order {self.order_mode} symmax {self.sym_max}"
+                 + (" norepl 1" if self.no_replication else "")]
         for s in sorted(self.slices, key=lambda x: (x.wg, x.seq)):
             lines.append(f"item {s.wg} {s.t} {s.strat} {s.chunk} {s.nchunks} {s.r0} {s.r1} {s.k} {s.j} {s.C} {s.cost}")
         lines.append(f"end max {self.max_ps} sum {self.sum_ps} lif {self.lif_milli} sym {self.r_sym}")
@@ -404,6 +410,8 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
     n_gather = sum(1 for g in groups if g[0].nchunks == 1 and g[0].strat == GATHER)
     few_gather = sym_max > 0 and n_gather <= sym_max
     for g in groups:
+        if opts.no_replication:
+            break
         sym = (sym_max >= 0 and g[0].nchunks == 1 and g[0].strat == GATHER and
                (few_gather or tabs[g[0].t].Lam / float(kmax) >= SYM_SHARE_MIN))
         if sym:
@@ -483,6 +491,7 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
 
     plan = Plan(T, E, dtype, R, K, L, B, opts.lif_milli, opts.order_mode)
     plan.sym_max = sym_max
+    plan.no_replication = bool(opts.no_replication)
     plan.slices = best_slices
     plan.max_ps = max(best_loads)
     plan.sum_ps = sum(best_loads)

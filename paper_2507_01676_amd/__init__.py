@@ -62,7 +62,7 @@ class _Opts(ctypes.Structure):
                 ("order_mode", ctypes.c_int32), ("chunk_max_bytes", ctypes.c_int64),
                 ("beta", ctypes.POINTER(ctypes.c_double)), ("force_strategy", ctypes.POINTER(ctypes.c_int32)),
                 ("num_workers", ctypes.c_int32), ("sym_max_gather", ctypes.c_int32),
-                ("pooling", ctypes.POINTER(ctypes.c_int32))]
+                ("pooling", ctypes.POINTER(ctypes.c_int32)), ("no_replication", ctypes.c_int32)]
 
 
 class _Info(ctypes.Structure):
@@ -158,6 +158,7 @@ class _Marshal:
         o.chunk_max_bytes = int(opts.get("chunk_max_bytes", 0))
         o.num_workers = int(opts.get("num_workers", 0))
         o.sym_max_gather = int(opts.get("sym_max", 0))
+        o.no_replication = 1 if opts.get("no_replication", False) else 0
         beta = opts.get("beta")
         if beta is not None:
             b = np.ascontiguousarray(np.asarray(beta, dtype=np.float64))

@@ -95,6 +95,8 @@ emb_status_t to_plan_in(int32_t T, const int64_t* rows, int32_t E, emb_dtype_t d
     in->chunk_max = opts->chunk_max_bytes;
     in->order_mode = opts->order_mode;
     in->sym_max = opts->sym_max_gather;
+    if (opts->no_replication != 0 && opts->no_replication != 1) return EMB_ERR_INVALID_ARGUMENT;
+    in->no_replication = opts->no_replication == 1;
     if (opts->beta) {
       in->has_beta = true;
       for (int i = 0; i < B_COUNT; ++i) in->beta[i] = opts->beta[i];

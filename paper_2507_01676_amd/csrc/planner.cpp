@@ -6,7 +6,9 @@
 //      row chunks of at most floor(min(chunk_max, L) / R) rows if its best unsplit cost
 //      exceeds the sum of the chunk costs;
 //   P3 tau = ceil(total cost / K);
-//   P4 a GATHER item is split k = min(K, B) ways (symmetric partitioning, Sec. III-A:
+//   P4 (skipped with no_replication: the paper's solver fixes replication to 1, so with
+//      order_mode 1 the plan is Sec. III-B steps 1-4 as printed)
+//      a GATHER item is split k = min(K, B) ways (symmetric partitioning, Sec. III-A:
 //      a gather slice stages nothing, so every worker takes 1/k of every such table)
 //      when its slices would hold at least kSymShareMin expected lookups each, or
 //      (sym_max > 0) while the plan has at most sym_max of them; sym_max < 0: never;
@@ -363,7 +365,9 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     for (const auto& g : P.groups) n_gather += (g[0].nchunks == 1 && g[0].strat == S_GATHER) ? 1 : 0;
     const bool few_gather = sym_max > 0 && n_gather <= sym_max;
     out->sym_max = sym_max;
+    out->no_replication = in.no_replication ? 1 : 0;
     for (auto& g : P.groups) {
+      if (in.no_replication) break;
       int32_t k = 1;
       const bool sym = sym_max >= 0 && g[0].nchunks == 1 && g[0].strat == S_GATHER &&
                        (few_gather || P.tabs[g[0].t].Lam / static_cast<double>(P.kmax) >= kSymShareMin);
@@ -461,8 +465,9 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
 std::string plan_text(const PlanOut& p) {
   std::string s = "embx-plan v1\n";
   char buf[512];
-  std::snprintf(buf, sizeof buf, "T %d E %d dtype %s R %d K %d L %lld B %d theta %d order %d symmax %d\n", p.T, p.E,
-                p.f16 ? "f16" : "f32", p.R, p.K, static_cast<long long>(p.L), p.B, p.theta, p.order_mode, p.sym_max);
+  std::snprintf(buf, sizeof buf, "T %d E %d dtype %s R %d K %d L %lld B %d theta %d order %d symmax %d%s\n", p.T, p.E,
+                p.f16 ? "f16" : "f32", p.R, p.K, static_cast<long long>(p.L), p.B, p.theta, p.order_mode, p.sym_max,
+                p.no_replication ? " norepl 1" : "");
   s += buf;
   for (const PSlice& x : p.slices) {
     std::snprintf(buf, sizeof buf, "item %d %d %d %d %d %lld %lld %d %d %d %lld\n", x.wg, x.t, x.strat, x.chunk,

@@ -41,6 +41,7 @@ struct PlanIn {
   bool has_beta = false;
   std::vector<int32_t> force;   // empty = all AUTO
   int32_t sym_max = 0;          // > 0: GATHER items split symmetrically while at most this many; < 0: never
+  bool no_replication = false;  // true: no batch splits (P4 off), the paper's replication factor of 1
 };
 constexpr double kSymShareMin = 64.0;   // GATHER tables split over all workers when each slice would hold
                                         // at least this many expected lookups
@@ -54,7 +55,7 @@ struct PSlice {
 };
 
 struct PlanOut {
-  int32_t T = 0, E = 0, R = 0, K = 0, B = 0, theta = 0, order_mode = 0, sym_max = 0;
+  int32_t T = 0, E = 0, R = 0, K = 0, B = 0, theta = 0, order_mode = 0, sym_max = 0, no_replication = 0;
   int64_t L = 0;
   bool f16 = false;
   std::vector<PSlice> slices;   // sorted by (wg, seq)

@@ -94,7 +94,7 @@ def _random_instance(seed, T=None, K=None):
     E = int(g.choice([32, 64, 128]))
     dtype = str(g.choice(["f32", "f16"]))
     opts = OPL.Options(lds_budget=int(g.choice([16384, 65536, 131072])), lif_milli=int(g.choice([1000, 1250, 2000])),
-                       order_mode=int(g.integers(0, 2)))
+                       order_mode=int(g.integers(0, 2)), no_replication=bool(g.integers(0, 4) == 0))
     return rows, E, dtype, stats, B, K, opts
 
 
@@ -435,3 +435,111 @@ def test_many_gather_tables_split_over_all_workers_only_when_their_slices_are_la
     assert n_full(q) < n_full(p) == T // 2
     r = OPL.plan_reference(rows, 64, "f32", stats, B, K, OPL.Options(sym_max=1000))
     assert all(int(ln.split()[8]) == K for ln in r.text().splitlines() if ln.startswith("item "))
+
+
+# ---------------------------------------------------------------- pins by hand-worked plans
+
+# A cost vector of exact binary values (ps): gather 1000 + 100 lam; LDS 2000 + S mu R + 10 lam
+# with S = 1/8 ps per byte; chunk adds I = 50 per lookup scanned; HOT and DEDUP priced out.
+WORKED_BETA = [0.0] * OPL.NBETA
+WORKED_BETA[OPL.G0], WORKED_BETA[OPL.G1] = 1000.0, 100.0
+WORKED_BETA[OPL.L0], WORKED_BETA[OPL.L1], WORKED_BETA[OPL.S], WORKED_BETA[OPL.I] = 2000.0, 10.0, 0.125, 50.0
+WORKED_BETA[OPL.H0], WORKED_BETA[OPL.D0] = 1e9, 1e9
+WORKED_ROWS = [100, 1000, 50, 10, 300, 20000]
+WORKED_S = [2.0, 5.0, 8.0, 1.0, 8.0, 100.0]
+
+
+def _worked(no_replication, lif_milli):
+    stats = [OPL.Stat(s_, 1, [], 1.0) for s_ in WORKED_S]
+    opts = OPL.Options(beta=WORKED_BETA, order_mode=1, lif_milli=lif_milli, no_replication=no_replication)
+    return WORKED_ROWS, 64, "f32", stats, 10, 2, opts
+
+
+def _items(text):
+    return [ln for ln in text.splitlines() if ln.startswith("item ") or ln.startswith("end ")]
+
+
+def test_literal_solver_worked_by_hand():
+    """The paper's solver (Sec. III-B steps 1-4: no replication, order (s desc, m asc)) on six
+    tables, K = 2 workers, B = 10, E = 64 fp32 (R = 256 B, L = 131072 B = 512 rows), with
+    WORKED_BETA.  Worked by hand:
+
+    Step 3 / P1, cost of each table at k = 1 (Lam = B s):
+      t0 m 100  s 2   Lam 20:   gather 1000 + 2000 = 3000;  LDS 2000 + 3200 + 200 = 5400   -> GATHER 3000
+      t1 m 1000 s 5   Lam 50:   gather 6000; does not fit L; step 1 would cut 2 chunks of 500
+                                 rows at 2000 + 16000 + 2500 + 250 = 20750 each, 41500 > 6000 -> GATHER 6000
+      t2 m 50   s 8   Lam 80:   gather 9000;  LDS 2000 + 1600 + 800 = 4400                  -> LDS 4400
+      t3 m 10   s 1   Lam 10:   gather 2000;  LDS 2000 + 320 + 100 = 2420                   -> GATHER 2000
+      t4 m 300  s 8   Lam 80:   gather 9000;  LDS 2000 + 9600 + 800 = 12400                 -> GATHER 9000
+      t5 m 20000 s 100 Lam 1000: gather 101000; 40 chunks > K, STREAM 2,652,000             -> GATHER 101000
+    Step 2, order (s desc, m asc, t): t5, t2, t4, t1, t0, t3; each to the least-loaded worker
+    (ties to worker 0): t5 -> 0 (101000), then t2, t4, t1, t0, t3 -> 1 (24400).
+    Step 4: LIF = floor(1000 * 2 * 101000 / 125400) = 1610: kept with threshold 2000.  With
+    replication (P4) t5 would be split over both workers (Lam / 2 = 500 >= 64 lookups), and with
+    the default threshold 1500 the fallback makes every table symmetric: last r tables of the
+    order for r = 1..5 give LIF 1621, 1640, 1682, 1746, 1759; r = 6 gives 67000 per worker, 1000.
+    """
+    cases = {
+        (True, 2000): ["item 0 5 3 0 1 0 20000 1 0 0 101000",
+                       "item 1 2 0 0 1 0 50 1 0 0 4400",
+                       "item 1 4 3 0 1 0 300 1 0 0 9000",
+                       "item 1 1 3 0 1 0 1000 1 0 0 6000",
+                       "item 1 0 3 0 1 0 100 1 0 0 3000",
+                       "item 1 3 3 0 1 0 10 1 0 0 2000",
+                       "end max 101000 sum 125400 lif 1610 sym 0"],
+        (False, 2000): ["item 0 5 3 0 1 0 20000 2 0 0 51000",
+                        "item 0 2 0 0 1 0 50 1 0 0 4400",
+                        "item 0 1 3 0 1 0 1000 1 0 0 6000",
+                        "item 0 3 3 0 1 0 10 1 0 0 2000",
+                        "item 1 5 3 0 1 0 20000 2 1 0 51000",
+                        "item 1 4 3 0 1 0 300 1 0 0 9000",
+                        "item 1 0 3 0 1 0 100 1 0 0 3000",
+                        "end max 63400 sum 126400 lif 1003 sym 0"],
+        (True, 1500): ["item 0 5 3 0 1 0 20000 2 0 0 51000",
+                       "item 0 2 0 0 1 0 50 2 0 0 4000",
+                       "item 0 4 3 0 1 0 300 2 0 0 5000",
+                       "item 0 1 3 0 1 0 1000 2 0 0 3500",
+                       "item 0 0 3 0 1 0 100 2 0 0 2000",
+                       "item 0 3 3 0 1 0 10 2 0 0 1500",
+                       "item 1 5 3 0 1 0 20000 2 1 0 51000",
+                       "item 1 2 0 0 1 0 50 2 1 0 4000",
+                       "item 1 4 3 0 1 0 300 2 1 0 5000",
+                       "item 1 1 3 0 1 0 1000 2 1 0 3500",
+                       "item 1 0 3 0 1 0 100 2 1 0 2000",
+                       "item 1 3 3 0 1 0 10 2 1 0 1500",
+                       "end max 67000 sum 134000 lif 1000 sym 6"],
+    }
+    for (norepl, lif), want in cases.items():
+        rows, E, dtype, stats, B, K, opts = _worked(norepl, lif)
+        text = OPL.plan_reference(rows, E, dtype, stats, B, K, opts).text()
+        assert _items(text) == want, (norepl, lif)
+        assert ("norepl 1" in text.splitlines()[1]) == norepl
+    # the built-in threshold is 1.5
+    assert OPL.Options().lif_milli == 1500
+
+
+@pytest.mark.parametrize("s,sym", [(63.0, False), (64.0, True), (65.0, True)])
+def test_symmetric_split_needs_64_expected_lookups_per_slice(s, sym):
+    """P4: an unchunked GATHER table is split over all min(K, B) workers exactly when each
+    slice would hold at least 64 expected lookups.  Eight identical 1M-row tables (GATHER is
+    their cheapest flow), K = B = 4, pooling s: Lam / 4 = s lookups per slice.  Every table
+    costs at most tau = 2 x its cost, so without the rule nothing is split."""
+    stats = [OPL.Stat(s, 100, [], 1.0)] * 8
+    p = OPL.plan_reference([1_000_000] * 8, 64, "f32", stats, 4, 4)
+    assert {sl.strat for sl in p.slices} == {OPL.GATHER}
+    ks = {sl.k for sl in p.slices}
+    assert ks == ({4} if sym else {1})
+    assert len(p.slices) == (32 if sym else 8)
+
+
+@pytest.mark.parametrize("m,stream", [(32768, True), (32769, False)])
+def test_stream_is_a_candidate_up_to_64_chunks(m, stream):
+    """P1: STREAM enters the automatic choice for tables of at most 64 chunks of floor(L / R)
+    rows.  L = 131072, R = 256: 512 rows a chunk, so 32768 rows are 64 chunks and 32769 are
+    65.  The cost vector makes STREAM far cheaper than a gather whenever it is allowed."""
+    beta = [0.0] * OPL.NBETA
+    beta[OPL.G1], beta[OPL.L1], beta[OPL.I], beta[OPL.D0] = 1e6, 1.0, 1.0, 1e10
+    opts = OPL.Options(beta=beta, no_replication=True)
+    p = OPL.plan_reference([m], 64, "f32", [OPL.Stat(1.0, 1, [], 1.0)], 16, 4, opts)
+    strats = {sl.strat for sl in p.slices}
+    assert strats == ({OPL.STREAM} if stream else {OPL.GATHER})

@@ -55,7 +55,7 @@ def _cpp(rows, E, dtype, stats, B, K, opts: OPL.Options):
            for s in stats]
     return embx.plan_text(rows, E, dtype, cst, B, K, lds_budget=opts.lds_budget, lif_milli=opts.lif_milli,
                           chunk_max_bytes=opts.chunk_max_bytes, order_mode=opts.order_mode, beta=opts.beta,
-                          force=opts.force, sym_max=opts.sym_max)
+                          force=opts.force, sym_max=opts.sym_max, no_replication=opts.no_replication)
 
 
 def _both(rows, E, dtype, stats, B, K, opts: OPL.Options):
@@ -165,4 +165,22 @@ def test_cpp_planner_equals_oracle_with_many_tables_of_mixed_shares(seed):
     B = int(g.choice([1024, 4096, 16384]))
     for sym_max in (0, -1, 80):
         got, want = _both(rows, 64, "f32", stats, B, 256, OPL.Options(sym_max=sym_max))
+        assert got == want
+
+
+def test_cpp_planner_equals_oracle_on_the_pinned_instances():
+    """The hand-worked literal-solver plans and the boundary instances of the P4 and STREAM
+    rules, through the C++ planner."""
+    from test_oracle_plan import _worked
+    for norepl, lif in ((True, 2000), (False, 2000), (True, 1500)):
+        got, want = _both(*_worked(norepl, lif))
+        assert got == want
+    for s in (63.0, 64.0, 65.0):
+        got, want = _both([1_000_000] * 8, 64, "f32", [OPL.Stat(s, 100, [], 1.0)] * 8, 4, 4, OPL.Options())
+        assert got == want
+    beta = [0.0] * OPL.NBETA
+    beta[OPL.G1], beta[OPL.L1], beta[OPL.I], beta[OPL.D0] = 1e6, 1.0, 1.0, 1e10
+    for m in (32768, 32769):
+        got, want = _both([m], 64, "f32", [OPL.Stat(1.0, 1, [], 1.0)], 16, 4,
+                          OPL.Options(beta=beta, no_replication=True))
         assert got == want
