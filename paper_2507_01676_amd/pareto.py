@@ -36,7 +36,12 @@ def pareto_front(points: List[Dict]) -> List[Dict]:
 
 
 def sweep(cfg: int, fractions: Sequence[float] = (1 / 16, 1 / 8, 1 / 4, 1 / 2, 1.0), steps: int = 100,
-          warmup: int = 10, n_p99: int = 500, n_batches: int = 0, log=print) -> List[Dict]:
+          warmup: int = 10, n_p99: int = 500, n_batches: int = 0, log=print, verify=None) -> List[Dict]:
+    """One point per batch size (a fraction of the workload's batch): a plan made for that
+    batch, its launch time back to back, the P99 of single launches, and whether the point
+    is on the Pareto front.  ``verify(config, batch, out)``, when given, is called once per
+    batch size with the workload at that batch, resident batch 0 and its pooled output
+    (a device tensor) from the plan that is timed."""
     import torch
     import workloads as W
     from . import Plan, fill_table
@@ -68,6 +73,10 @@ def sweep(cfg: int, fractions: Sequence[float] = (1 / 16, 1 / 8, 1 / 4, 1 / 2, 1
         for i in range(warmup):
             plan.lookup_ptr(*ptrs[i % n_batches], B, out.data_ptr(), sp)
         torch.cuda.synchronize()
+        if verify is not None:
+            plan.lookup_ptr(*ptrs[0], B, out.data_ptr(), sp)
+            torch.cuda.synchronize()
+            verify(c, batches[0], out)
         e0 = [torch.cuda.Event(enable_timing=True) for _ in range(n_p99)]
         e1 = [torch.cuda.Event(enable_timing=True) for _ in range(n_p99)]
         for i in range(n_p99):

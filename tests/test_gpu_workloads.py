@@ -1,8 +1,9 @@
 """Parity at the five workloads' full sizes, with the plan and launch the benchmark uses.
 
-The smallest workload is checked on every output element; the others on
-sampled bags whose rows the oracle regenerates on the host, plus properties
-that hold at any size (empty bags, integer-table exactness).
+Workloads 1-4 are checked on every output element (tables built on the host and
+uploaded); workload 5 (132.7 GB of tables) on sampled bags whose rows the oracle
+regenerates on the host, bit-exact on integer tables.  The batch-size sweep's plans
+are checked at two of its batch sizes.
 """
 import gc
 
@@ -51,23 +52,25 @@ def test_workload1_full():
 
 
 @pytest.mark.parametrize("cfg", [2, 3, 4])
-def test_workload_full_size_sampled(cfg):
-    log(f"workload {cfg}: full size, sampled bags")
+def test_workload_full_size_every_element(cfg):
+    """Workloads 2-4 at full size with the plan bench.py uses: every output element against
+    the oracle (tables built on the host by the generator and uploaded), uniform values to
+    the tolerance and integer values bit for bit."""
+    log(f"workload {cfg}: full size, every element")
     c = W.make_config(cfg)
     batch = W.gen_batch(c, 0)
     stats = W.history_stats(c)
-    wd = filled_tables(c)
-    got = _lookup(c, batch, wd, stats)
-    err = check_sampled(c, got, batch, 4000, seed=cfg)
-    log(f"  worst pooled error on 4000 bags {err:.2e}")
-    # integer-valued tables: sampled bags bit-exact
-    wi = filled_tables(c, W.VAL_INTEGER)
-    del wd
-    _free()
-    got = _lookup(c, batch, wi, stats)
-    check_sampled(c, got, batch, 4000, seed=100 + cfg, mode=W.VAL_INTEGER, exact=True)
-    del wi
-    _free()
+    for mode in (W.VAL_UNIFORM, W.VAL_INTEGER):
+        hw = host_tables(c, mode)
+        log(f"  tables built on the host ({sum(w.nbytes for w in hw) / 1e9:.2f} GB, mode {mode})")
+        wd = upload_tables(hw)
+        got = _lookup(c, batch, wd, stats)
+        del wd
+        _free()
+        err, _ = check_full(got, hw, batch, c.dtype, exact=mode == W.VAL_INTEGER)
+        log(f"  {batch.B * c.T * c.E} elements checked, pooled error {err:.2e}")
+        del hw, got
+        gc.collect()
 
 
 @pytest.mark.parametrize("cfg,dist", [(1, "fixed"), (2, "fixed"), (2, "uniform"), (4, "fixed")])
@@ -127,6 +130,10 @@ def test_workload_full_size_sampled_weighted_and_mean(cfg):
 
 
 def test_workload5_full_size_sampled():
+    """Workload 5 at full size (132.7 GB of tables, 131M lookups) with the plan bench.py uses:
+    uniform tables to the tolerance on 3000 sampled bags; integer tables bit-exact on 20000
+    sampled bags; then weighted lookups with mean and sum tables alternating on the same
+    integer tables, to the tolerance on 4000 sampled bags."""
     import torch
     log("workload 5 (100 tables <= 150 GB, E128 fp32, B65536): full size, sampled bags")
     c = W.make_config(5)
@@ -140,3 +147,46 @@ def test_workload5_full_size_sampled():
     log(f"  worst pooled error on 3000 bags {err:.2e}")
     del wd, got
     _free()
+    wi = filled_tables(c, W.VAL_INTEGER)
+    torch.cuda.synchronize()
+    got = _lookup(c, batch, wi, stats)
+    check_sampled(c, got, batch, 20000, seed=55, mode=W.VAL_INTEGER, exact=True)
+    log("  integer tables: 20000 sampled bags bit-exact")
+    del got
+    pooling = ["mean" if t % 2 == 0 else "sum" for t in range(c.T)]
+    psw = np.random.default_rng(1005).uniform(0.5, 1.5, size=batch.indices.size).astype(np.float32)
+    p = plan_for(c, c.batch, stats=stats, pooling=pooling)
+    p.bind(wi)
+    idx, off = to_device(batch)
+    out = p.lookup(idx, off, batch.B, weights=torch.from_numpy(psw).cuda())
+    torch.cuda.synchronize()
+    assert p.check_errors() == 0
+    got = out.cpu().numpy()
+    del out, idx, off
+    err = check_sampled(c, got, batch, 4000, seed=56, mode=W.VAL_INTEGER, pooling=pooling, psw=psw)
+    log(f"  weighted, mean/sum tables: worst pooled error on 4000 bags {err:.2e}")
+    del wi, got
+    _free()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_batch_sweep_plans_match_the_oracle(cfg):
+    """The batch-size sweep's own plans (made for 1/16 and 1/2 of the workload's batch):
+    the output of the plan each point times is checked on sampled bags (every bag for
+    workload 1), uniform tables to the tolerance."""
+    from paper_2507_01676_amd import pareto
+
+    seen = []
+
+    def verify(cw, batch, out):
+        got = out.cpu().numpy()
+        n = batch.B * cw.T if cfg == 1 else 3000
+        err = check_sampled(cw, got, batch, n, seed=700 + batch.B)
+        log(f"  workload {cfg} batch {batch.B}: worst pooled error {err:.2e}")
+        seen.append(batch.B)
+
+    pts = pareto.sweep(cfg, fractions=(1 / 16, 1 / 2), steps=5, warmup=2, n_p99=5, n_batches=2,
+                       log=lambda m: log("  " + m), verify=verify)
+    full = W.make_config(cfg).batch
+    assert seen == [max(1, round(full / 16)), max(1, round(full / 2))]
+    assert len(pts) == 2 and all(p["lookups_per_s"] > 0 for p in pts)
