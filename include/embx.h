@@ -164,6 +164,24 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
                              const emb_table_stats_t* stats, int32_t max_batch,
                              const emb_plan_options_t* opts);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): emb_plan_create with the plan's device
+ * data -- run queues, slice list, hot-row hashes, combine and error counters, row-chunk
+ * partial sums -- placed in a fixed array of EMB_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every GPU it runs on until the process ends; no hipMalloc or hipFree is called
+ * (the plan's metadata is copied into the array, synchronously).  The array is one per GPU
+ * and shared by every such call: a later emb_plan_create_noalloc on the same device
+ * replaces the plan in it, and the earlier handle then fails with EMB_ERR_INVALID_ARGUMENT
+ * (emb_plan_destroy still frees its host part).  Lookups of such a plan must not overlap
+ * another call that uses the array on that device.  EMB_ERR_UNSUPPORTED when the plan's
+ * device data exceed the array; otherwise the same arguments, results and errors as
+ * emb_plan_create. */
+#define EMB_NOALLOC_SCRATCH_BYTES (64u << 20)
+emb_status_t emb_plan_create_noalloc(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows,
+                                     int32_t embedding_dim, emb_dtype_t dtype,
+                                     const emb_table_stats_t* stats, int32_t max_batch,
+                                     const emb_plan_options_t* opts);
+
 /* Records the T device pointers of the tables: the paper's lookup tables of m_i rows of E
  * elements (Sec. II-B), weights[t] -> rows[t] x E contiguous, row-major, 16-byte aligned.
  * The caller keeps ownership and keeps them alive.  Copies the pointers into the plan's

@@ -39,7 +39,7 @@ POOLING_CODES = {"sum": POOL_SUM, "mean": POOL_MEAN}
 BETA_COUNT = 11
 MAX_HOT_STATS = 4096
 
-EXPORTED = ["emb_plan_create", "emb_plan_bind_weights", "emb_lookup", "emb_lookup_weighted", "emb_plan_check_errors",
+EXPORTED = ["emb_plan_create", "emb_plan_create_noalloc", "emb_plan_bind_weights", "emb_lookup", "emb_lookup_weighted", "emb_plan_check_errors",
             "emb_plan_serialize", "emb_plan_get_info", "emb_plan_destroy", "emb_plan_text",
             "emb_status_string", "emb_debug_dedup_tile", "emb_debug_hot_probe", "embx_fill_table",
             "emb_plan_set_trace", "emb_default_beta"]
@@ -79,6 +79,7 @@ _lib.emb_status_string.restype = ctypes.c_char_p
 _lib.emb_status_string.argtypes = [_i32]
 _lib.emb_plan_create.argtypes = [ctypes.POINTER(_vp), _i32, ctypes.POINTER(_i64), _i32, _i32,
                                  ctypes.POINTER(_Stats), _i32, ctypes.POINTER(_Opts)]
+_lib.emb_plan_create_noalloc.argtypes = _lib.emb_plan_create.argtypes
 _lib.emb_plan_bind_weights.argtypes = [_vp, ctypes.POINTER(_vp)]
 _lib.emb_lookup.argtypes = [_vp, _vp, _vp, _i32, _vp, _vp]
 _lib.emb_lookup_weighted.argtypes = [_vp, _vp, _vp, _vp, _i32, _vp, _vp]
@@ -220,15 +221,18 @@ def plan_text(rows: Sequence[int], E: int, dtype, stats, max_batch: int, num_wor
 class Plan:
     """A lookup plan on the current HIP device (emb_plan_create .. emb_plan_destroy)."""
 
-    def __init__(self, rows: Sequence[int], E: int, dtype, stats, max_batch: int, **opts):
+    def __init__(self, rows: Sequence[int], E: int, dtype, stats, max_batch: int, noalloc: bool = False, **opts):
+        """``noalloc``: emb_plan_create_noalloc (device data in the library's fixed per-GPU
+        array; a later such plan on the device replaces this one)."""
         self.T = len(rows)
         self.E = int(E)
         self.dtype = _dtype_code(dtype)
         self.max_batch = int(max_batch)
         m = _Marshal(rows, stats, opts, self.T)
         h = _vp()
-        _check(_lib.emb_plan_create(ctypes.byref(h), self.T, m.rows, self.E, self.dtype, m.stats, self.max_batch,
-                                    ctypes.byref(m.opts)), "emb_plan_create")
+        fn = _lib.emb_plan_create_noalloc if noalloc else _lib.emb_plan_create
+        _check(fn(ctypes.byref(h), self.T, m.rows, self.E, self.dtype, m.stats, self.max_batch,
+                  ctypes.byref(m.opts)), "emb_plan_create_noalloc" if noalloc else "emb_plan_create")
         self._h = h
         self._weights = None
 

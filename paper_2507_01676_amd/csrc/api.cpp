@@ -4,10 +4,12 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -51,6 +53,8 @@ struct emb_plan {
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
   std::vector<int32_t> mean;             // per table: 1 = mean pooling
   int32_t gather_runs[3] = {0, 0, 0};    // runs per gather queue class, over all workers
+  bool in_scratch = false;               // device data in the device's scratch array (no allocation)
+  uint64_t scratch_gen = 0;              // which creation in the scratch array this plan is
 };
 
 namespace {
@@ -118,6 +122,59 @@ size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace
 
+// Device data of the plans made by emb_plan_create_noalloc: one fixed array per GPU,
+// held until the process ends.  Host code never uses the array's name as an address (it
+// is a host-side stand-in): each device's address comes from hipGetSymbolAddress, taken
+// once per device with that device current.
+static __device__ __align__(256) char scratch[EMB_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+struct ScratchState {
+  std::mutex mu;
+  std::vector<char*> ptr;                        // per device; nullptr until looked up
+  std::vector<std::atomic<uint64_t>*> gen;       // per device: creations so far
+};
+
+ScratchState& scratch_state() {
+  static ScratchState s;
+  return s;
+}
+
+// The scratch array's address on device `dev` (current) and the generation of a new plan
+// placed in it.
+emb_status_t scratch_acquire(int dev, char** base, uint64_t* gen) {
+  ScratchState& st = scratch_state();
+  std::lock_guard<std::mutex> lock(st.mu);
+  if (dev < 0) return EMB_ERR_DEVICE;
+  if (st.ptr.size() <= static_cast<size_t>(dev)) {
+    st.ptr.resize(dev + 1, nullptr);
+    while (st.gen.size() <= static_cast<size_t>(dev)) st.gen.push_back(new std::atomic<uint64_t>(0));
+  }
+  if (!st.ptr[dev]) {
+    void* a = nullptr;
+    if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || !a) return EMB_ERR_DEVICE;
+    st.ptr[dev] = static_cast<char*>(a);
+  }
+  *base = st.ptr[dev];
+  *gen = st.gen[dev]->fetch_add(1) + 1;
+  return EMB_OK;
+}
+
+// A plan in the scratch array is usable while no later one has replaced it.
+bool scratch_current(const emb_plan* p) {
+  if (!p->in_scratch) return true;
+  ScratchState& st = scratch_state();
+  std::lock_guard<std::mutex> lock(st.mu);
+  return static_cast<size_t>(p->device) < st.gen.size() && st.gen[p->device]->load() == p->scratch_gen;
+}
+
+emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows, int32_t embedding_dim,
+                         emb_dtype_t dtype, const emb_table_stats_t* stats, int32_t max_batch,
+                         const emb_plan_options_t* opts, bool in_scratch);
+
+}  // namespace
+
 extern "C" {
 
 const char* emb_status_string(emb_status_t s) {
@@ -164,6 +221,22 @@ emb_status_t emb_default_beta(int32_t row_bytes, double* out, int32_t n) {
 emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows, int32_t embedding_dim,
                              emb_dtype_t dtype, const emb_table_stats_t* stats, int32_t max_batch,
                              const emb_plan_options_t* opts) {
+  return plan_create(plan_out, num_tables, rows, embedding_dim, dtype, stats, max_batch, opts, false);
+}
+
+emb_status_t emb_plan_create_noalloc(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows,
+                                     int32_t embedding_dim, emb_dtype_t dtype, const emb_table_stats_t* stats,
+                                     int32_t max_batch, const emb_plan_options_t* opts) {
+  return plan_create(plan_out, num_tables, rows, embedding_dim, dtype, stats, max_batch, opts, true);
+}
+
+}  // extern "C"
+
+namespace {
+
+emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows, int32_t embedding_dim,
+                         emb_dtype_t dtype, const emb_table_stats_t* stats, int32_t max_batch,
+                         const emb_plan_options_t* opts, bool in_scratch) {
   if (!plan_out) return EMB_ERR_INVALID_ARGUMENT;
   *plan_out = nullptr;
   int dev = 0;
@@ -502,14 +575,35 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   size_t o_gr = align_up(o_err + sizeof(unsigned long long), 256);
   size_t o_zero = align_up(o_gr + p->h_gr.size() * sizeof(GatherRun), 256);
   size_t total = align_up(o_zero + static_cast<size_t>(p->R), 256);
-  if (hipMalloc(&p->d_meta, total) != hipSuccess) {
-    delete p;
-    return EMB_ERR_OUT_OF_MEMORY;
-  }
-  if (part_floats > 0 && hipMalloc(&p->d_partials, part_floats * sizeof(float)) != hipSuccess) {
-    (void)hipFree(p->d_meta);
-    delete p;
-    return EMB_ERR_OUT_OF_MEMORY;
+  if (in_scratch) {
+    // metadata, then the partial-sum slabs, in the device's scratch array
+    const size_t o_part = align_up(total, 256);
+    const size_t need = o_part + static_cast<size_t>(part_floats) * sizeof(float);
+    if (need > EMB_NOALLOC_SCRATCH_BYTES) {
+      delete p;
+      return EMB_ERR_UNSUPPORTED;
+    }
+    char* base = nullptr;
+    uint64_t gen = 0;
+    const emb_status_t sa = scratch_acquire(dev, &base, &gen);
+    if (sa != EMB_OK) {
+      delete p;
+      return sa;
+    }
+    p->in_scratch = true;
+    p->scratch_gen = gen;
+    p->d_meta = base;
+    p->d_partials = part_floats > 0 ? reinterpret_cast<float*>(base + o_part) : nullptr;
+  } else {
+    if (hipMalloc(&p->d_meta, total) != hipSuccess) {
+      delete p;
+      return EMB_ERR_OUT_OF_MEMORY;
+    }
+    if (part_floats > 0 && hipMalloc(&p->d_partials, part_floats * sizeof(float)) != hipSuccess) {
+      (void)hipFree(p->d_meta);
+      delete p;
+      return EMB_ERR_OUT_OF_MEMORY;
+    }
   }
   p->d_items = reinterpret_cast<DevItem*>(p->d_meta + o_items);
   p->d_wg_ptr = reinterpret_cast<int32_t*>(p->d_meta + o_wg);
@@ -550,8 +644,12 @@ emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const in
   return EMB_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
 emb_status_t emb_plan_bind_weights(emb_plan_t* plan, const void* const* weights) {
-  if (!plan || !weights) return EMB_ERR_INVALID_ARGUMENT;
+  if (!plan || !weights || !scratch_current(plan)) return EMB_ERR_INVALID_ARGUMENT;
   for (int32_t t = 0; t < plan->T; ++t) {
     if (!weights[t] || (reinterpret_cast<uintptr_t>(weights[t]) & 15u) != 0) return EMB_ERR_INVALID_ARGUMENT;
   }
@@ -570,7 +668,7 @@ namespace {
 
 emb_status_t lookup_impl(emb_plan_t* plan, const int64_t* indices, const int64_t* offsets, const float* weights,
                          bool weighted, int32_t batch, float* out, void* stream) {
-  if (!plan) return EMB_ERR_INVALID_ARGUMENT;
+  if (!plan || !scratch_current(plan)) return EMB_ERR_INVALID_ARGUMENT;
   if (batch < 0 || batch > plan->Bmax) return EMB_ERR_INVALID_ARGUMENT;
   if (!plan->bound) return EMB_ERR_NOT_BOUND;
   if (batch == 0) return EMB_OK;
@@ -621,7 +719,7 @@ emb_status_t emb_lookup_weighted(emb_plan_t* plan, const int64_t* indices, const
 }
 
 emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_bad) {
-  if (!plan) return EMB_ERR_INVALID_ARGUMENT;
+  if (!plan || !scratch_current(plan)) return EMB_ERR_INVALID_ARGUMENT;
   if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return EMB_ERR_DEVICE;
   unsigned long long v = 0;
   if (hipMemcpy(&v, plan->d_err, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return EMB_ERR_DEVICE;
@@ -631,7 +729,7 @@ emb_status_t emb_plan_check_errors(emb_plan_t* plan, void* stream, int64_t* n_ba
 }
 
 emb_status_t emb_plan_set_trace(emb_plan_t* plan, uint64_t* trace, size_t capacity, size_t* needed) {
-  if (!plan) return EMB_ERR_INVALID_ARGUMENT;
+  if (!plan || !scratch_current(plan)) return EMB_ERR_INVALID_ARGUMENT;
   const size_t need = static_cast<size_t>(plan->K) * kTraceWorker + 2 * plan->plan.slices.size();
   if (needed) *needed = need;
   if (!trace) {
@@ -673,8 +771,10 @@ emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info) {
 emb_status_t emb_plan_destroy(emb_plan_t* plan) {
   if (!plan) return EMB_OK;
   emb_status_t s = EMB_OK;
-  if (plan->d_partials && hipFree(plan->d_partials) != hipSuccess) s = EMB_ERR_DEVICE;
-  if (plan->d_meta && hipFree(plan->d_meta) != hipSuccess) s = EMB_ERR_DEVICE;
+  if (!plan->in_scratch) {   // a plan in the scratch array owns no device memory
+    if (plan->d_partials && hipFree(plan->d_partials) != hipSuccess) s = EMB_ERR_DEVICE;
+    if (plan->d_meta && hipFree(plan->d_meta) != hipSuccess) s = EMB_ERR_DEVICE;
+  }
   delete plan;
   return s;
 }
