@@ -421,12 +421,13 @@ def main():
                      "compulsory_rows_bytes_per_launch": sum(comp_batch[i % R]["rows"] for i in range(K)) / K,
                      "per_lookup_bytes_per_launch": alg_mean,
                      "per_lookup_frac": alg_mean / (launch_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-                     "kernel": "lookup_kernel"},
+                     "kernel": info["kernel"]},
         "p99_batches": len(lat_ms),
         "cold_cache": cold,
         "copy_gbps": copy_gbps,
         "launch_floor_us": floor_us,
-        "plan": {"strategies": info["n_strategy"], "items": info["num_items"], "lif_milli": info["lif_milli"],
+        "plan": {"kernel": info["kernel"], "strategies": info["n_strategy"], "items": info["num_items"],
+                 "lif_milli": info["lif_milli"],
                  "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms},
         "kernel_source_hash": src_hash,
         "cpu_baseline": cpu,

@@ -145,6 +145,9 @@ typedef struct {
   int32_t n_strategy[5];    /* slices per strategy (emb_strategy_t order)      */
   int32_t gather_runs[3];   /* gather slices over all workers' queues: a wavefront per bag
                                (long bags), single-lookup bags (max_pooling == 1), SW sums */
+  int32_t kernel;           /* 0: the staged kernel (lookup_kernel, any plan); 1: the
+                               wave-uniform gather kernel (gather_kernel; gather-only plans
+                               with rows of 256, 512 or 1024 bytes)                        */
 } emb_plan_info_t;
 
 /* Builds a plan for T tables of rows[t] x E elements of `dtype`, for batches of up to

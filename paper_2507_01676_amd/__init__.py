@@ -71,7 +71,7 @@ class _Info(ctypes.Structure):
                 ("lds_bytes", ctypes.c_int32), ("num_items", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("lds_budget_bytes", ctypes.c_int32), ("max_load_ps", ctypes.c_int64),
                 ("sum_load_ps", ctypes.c_int64), ("lif_milli", ctypes.c_int32), ("r_symmetric", ctypes.c_int32),
-                ("n_strategy", ctypes.c_int32 * 5), ("gather_runs", ctypes.c_int32 * 3)]
+                ("n_strategy", ctypes.c_int32 * 5), ("gather_runs", ctypes.c_int32 * 3), ("kernel", ctypes.c_int32)]
 
 
 _vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
@@ -320,6 +320,7 @@ class Plan:
         d = {k: getattr(i, k) for k, _ in _Info._fields_ if k not in ("n_strategy", "gather_runs")}
         d["n_strategy"] = {STRATEGY_NAMES[s]: i.n_strategy[s] for s in range(5)}
         d["gather_runs"] = {"wave": i.gather_runs[0], "single": i.gather_runs[1], "sw": i.gather_runs[2]}
+        d["kernel"] = "gather_kernel" if i.kernel == 1 else "lookup_kernel"
         return d
 
     def hot_probe(self, table: int, idx, stream=None):

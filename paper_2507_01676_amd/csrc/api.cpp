@@ -280,10 +280,11 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
     return st(rc);
   }
   // A gather-only plan with rows of 16, 32 or 64 lanes runs the wave-uniform gather kernel
-  // (EMBX_GATHER_KERNEL=classic keeps the sub-wavefront walkers, for comparison).  That
-  // kernel's workers are smaller workgroups (kWaveBlock threads, EMBX_WAVE_BLOCK overrides),
-  // as many per CU as its registers allow; unless the caller fixed the worker count, the
-  // plan is made again for that many workers, and kept if it is still gather-only.
+  // (EMBX_GATHER_KERNEL=classic keeps the sub-wavefront walkers, for comparison).  Its
+  // workers are 1024-thread workgroups, as many per CU as its registers allow; unless the
+  // caller fixed the worker count, the plan is made again for that many workers, and kept
+  // if it is still gather-only.  (Measured: 256- and 512-thread workers at the same
+  // occupancy are slower -- more, smaller slices and fewer wavefronts sharing a queue.)
   const int G0 = lanes_per_row(p->plan.R);
   auto gather_only = [](const PlanOut& P0) {
     for (const PSlice& x : P0.slices)
@@ -293,11 +294,8 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
   const char* env_kernel = std::getenv("EMBX_GATHER_KERNEL");
   bool wave_gather = (G0 == 16 || G0 == 32 || G0 == 64) && gather_only(p->plan) &&
                      !(env_kernel && std::strcmp(env_kernel, "classic") == 0);
-  int block = kBlock;
+  const int block = kBlock;
   if (wave_gather) {
-    const char* env_block = std::getenv("EMBX_WAVE_BLOCK");
-    block = env_block ? std::atoi(env_block) : kWaveBlock;
-    if (block < 64 || block > kBlock || block % 64 != 0) block = kWaveBlock;
     if (!(opts && (opts->num_workers > 0 || opts->wg_per_cu > 0))) {
       const int bpc = gather_blocks_per_cu(G0, dtype == EMB_DTYPE_F16, block);
       if (bpc < 1) {
@@ -449,7 +447,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
   // fewer when that leaves some of the 16 wavefronts without one.
   //
   // The wave-uniform gather kernel's queues are single-lookup bags (chunks of one wavefront
-  // step: 8 S bags) and all other bags, in chunks of about 128 expected lookups, 192 when
+  // step: kGatherSteps S bags) and all other bags, in chunks of about 128 expected lookups, 192 when
   // the worker's queue gives each wavefront at least 64 chunks (W / 16 >= 64 * 192, W the
   // worker's lookups in that queue), and at least two wavefront steps (EMBX_WAVE_CHUNK
   // overrides it).  Measured on workloads 3-5: shorter chunks keep a worker's wavefronts
@@ -498,7 +496,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
       // of a SW's time and the worker's tail is up to one chunk, so ~sqrt(5 W / NSW)
       // lookups per chunk balances the two; measured, chunks past ~128 lookups lose again
       // (the SWs then work on fewer tables at a time), hence the cap
-      const double wstep = 8.0 * (64 / p->G);   // lookups of one wavefront step (wave kernel)
+      const double wstep = static_cast<double>(kGatherSteps) * (64 / p->G);   // lookups of one wave kernel step
       const double target =
           !wave_gather ? std::min(128.0, std::max(8.0, std::floor(std::sqrt(5.0 * Ws / nsw))))
           : wave_chunk_override > 0.0 ? wave_chunk_override
@@ -512,7 +510,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
           const DevItem& d = items[i];
           if (d.strat != S_GATHER || class_of(d) != cls) continue;
           const double s_t = std::max(1.0, stats[d.table].mean_pooling);
-          const int32_t cb = cls == 1 ? (wave_gather ? 512 / p->G : kChunkSingle)
+          const int32_t cb = cls == 1 ? (wave_gather ? kGatherSteps * (64 / p->G) : kChunkSingle)
                                       : static_cast<int32_t>(std::max(1.0, std::floor((cls == 0 ? wtarget : target) / s_t)));
           const int64_t nc = (slice_bags_any(d) + cb - 1) / cb;
           if (nc == 0) continue;
@@ -765,6 +763,7 @@ emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info) {
   info->r_symmetric = plan->plan.r_sym;
   for (const PSlice& x : plan->plan.slices) info->n_strategy[x.strat] += 1;
   for (int cls = 0; cls < 3; ++cls) info->gather_runs[cls] = plan->gather_runs[cls];
+  info->kernel = plan->wave_gather ? 1 : 0;
   return EMB_OK;
 }
 

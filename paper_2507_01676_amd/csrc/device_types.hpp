@@ -7,7 +7,15 @@
 namespace embx {
 
 constexpr int kBlock = 1024;        // threads per worker (16 wave64s: one worker per CU)
-constexpr int kWaveBlock = 1024;    // threads per worker of the wave-uniform gather kernel
+#ifndef EMBX_KSTEPS
+#define EMBX_KSTEPS 12
+#endif
+// Wave-uniform gather kernel: row loads in flight per lane per step.  A step covers
+// kGatherSteps * 64 / G lookups (or, for single-lookup bags, bags), and a chunk of
+// single-lookup bags is one step.  Measured on MI355X (one 1024-thread worker per CU):
+// 6 -> 8 -> 12 -> 16 gave workload 5 4288 / 4120 / 3972 / 3936 us and workload 3
+// 123.8 / 120.6 / 115.1 / 119.3 us; two workers per CU at 64 VGPRs lost on every workload.
+constexpr int kGatherSteps = EMBX_KSTEPS;
 constexpr int kTile = 2048;         // DEDUP: lookups per sorted tile
 constexpr int kMetaReserve = 28928;   // LDS beyond the row budget: hot hash or dedup tile
 

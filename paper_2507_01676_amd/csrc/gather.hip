@@ -30,6 +30,8 @@
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <utility>
+
 #include "device_types.hpp"
 
 #ifndef EMBX_GPART
@@ -65,7 +67,19 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 
-constexpr int kSteps = 8;            // row loads in flight per lane per step
+constexpr int kSteps = kGatherSteps;   // row loads in flight per lane per step
+static_assert(kSteps >= 1 && kSteps <= 16, "one id per lane of a row of 16 for each step");
+
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>): a loop whose index
+// is a compile-time constant (register arrays stay in registers, DPP controls are immediates)
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 constexpr int64_t kNoEnd = INT64_MAX;
 
 // Buffer descriptor of a table: rows of R bytes from base; num_records = rows (the
@@ -280,28 +294,18 @@ __device__ __forceinline__ i32x4 load_row(const RunInfo& ri, int row, int lane_c
 }
 
 // kSteps rows, one per instruction u, row id broadcast from lane u of this lane's row of 16
-#define EMBX_ISSUE_ROWS(RI, ROW, RAW)                                                                      \
-  if ((RI).big()) {                                                                                        \
-    GMEM const char* const wb_ = (RI).base() + lane_c;                                                    \
-    RAW[0] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<0>(ROW))) * static_cast<uint32_t>(R)); \
-    RAW[1] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<1>(ROW))) * static_cast<uint32_t>(R)); \
-    RAW[2] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<2>(ROW))) * static_cast<uint32_t>(R)); \
-    RAW[3] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<3>(ROW))) * static_cast<uint32_t>(R)); \
-    RAW[4] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<4>(ROW))) * static_cast<uint32_t>(R)); \
-    RAW[5] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<5>(ROW))) * static_cast<uint32_t>(R)); \
-    RAW[6] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<6>(ROW))) * static_cast<uint32_t>(R)); \
-    RAW[7] = *reinterpret_cast<GMEM const i32x4*>(wb_ + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<7>(ROW))) * static_cast<uint32_t>(R)); \
-  } else {                                                                                                 \
-    RAW[0] = buffer_load_row((RI).rsrc, row_bcast<0>(ROW), lane_c, 0, 0);                                  \
-    RAW[1] = buffer_load_row((RI).rsrc, row_bcast<1>(ROW), lane_c, 0, 0);                                  \
-    RAW[2] = buffer_load_row((RI).rsrc, row_bcast<2>(ROW), lane_c, 0, 0);                                  \
-    RAW[3] = buffer_load_row((RI).rsrc, row_bcast<3>(ROW), lane_c, 0, 0);                                  \
-    RAW[4] = buffer_load_row((RI).rsrc, row_bcast<4>(ROW), lane_c, 0, 0);                                  \
-    RAW[5] = buffer_load_row((RI).rsrc, row_bcast<5>(ROW), lane_c, 0, 0);                                  \
-    RAW[6] = buffer_load_row((RI).rsrc, row_bcast<6>(ROW), lane_c, 0, 0);                                  \
-    RAW[7] = buffer_load_row((RI).rsrc, row_bcast<7>(ROW), lane_c, 0, 0);                                  \
+__device__ __forceinline__ void issue_rows(const RunInfo& ri, int row, int lane_c, int R, i32x4 (&raw)[kSteps]) {
+  if (ri.big()) {
+    GMEM const char* const wb = ri.base() + lane_c;
+    static_for<kSteps>([&](auto u) __attribute__((always_inline)) {
+      raw[u] = *reinterpret_cast<GMEM const i32x4*>(
+          wb + static_cast<uint64_t>(static_cast<uint32_t>(row_bcast<decltype(u)::value>(row))) *
+                   static_cast<uint32_t>(R));
+    });
+  } else {
+    static_for<kSteps>([&](auto u) __attribute__((always_inline)) { raw[u] = buffer_load_row(ri.rsrc, row_bcast<decltype(u)::value>(row), lane_c, 0, 0); });
   }
-static_assert(kSteps == 8, "EMBX_ISSUE_ROWS issues eight rows");
+}
 
 // Lane constants of a walker.
 struct LaneConst {
@@ -405,7 +409,7 @@ struct Multi {
         float wl = 0.0f;
         if constexpr (W) wl = ok ? wt : 0.0f;
         i32x4 raw[kSteps];
-        EMBX_ISSUE_ROWS(ri, row, raw)
+        issue_rows(ri, row, lane_c, R, raw);
         // ids of the next step: more of this chunk, or the start of the next one
         const int64_t pn = p + n;
         if (pn < pend) {
@@ -424,19 +428,17 @@ struct Multi {
         }
         if (__ballot(okp && !ok) != 0) {
           const int okv = ok ? 1 : 0;
-#define EMBX_MASK(U) if (!row_bcast<U>(okv)) raw[U] = zero4();
-          EMBX_MASK(0) EMBX_MASK(1) EMBX_MASK(2) EMBX_MASK(3)
-          EMBX_MASK(4) EMBX_MASK(5) EMBX_MASK(6) EMBX_MASK(7)
-#undef EMBX_MASK
+          static_for<kSteps>([&](auto u) __attribute__((always_inline)) {
+            if (!row_bcast<decltype(u)::value>(okv)) raw[u] = zero4();
+          });
         }
         // additions in lookup order per SW; bag ends are wave-uniform
         const int wlb = __float_as_int(wl);
-#define EMBX_ADD(U)                                                                              \
-  add_instr(a, acc, raw[U], W ? __int_as_float(row_bcast<U>(wlb)) : a.one, p + (U) * S, pn, ri, b, be, e, \
-            bstart, wb, win);
-        EMBX_ADD(0) EMBX_ADD(1) EMBX_ADD(2) EMBX_ADD(3)
-        EMBX_ADD(4) EMBX_ADD(5) EMBX_ADD(6) EMBX_ADD(7)
-#undef EMBX_ADD
+        static_for<kSteps>([&](auto u) __attribute__((always_inline)) {
+          constexpr int U = decltype(u)::value;
+          add_instr(a, acc, raw[U], W ? __int_as_float(row_bcast<U>(wlb)) : a.one, p + U * S, pn, ri, b, be, e,
+                    bstart, wb, win);
+        });
         p = pn;
       }
       // bags left at the chunk's end: one whose last lookup closed the final step (its
@@ -594,7 +596,7 @@ struct Single {
       float wl = 0.0f;
       if constexpr (W) wl = ok ? w0 : 0.0f;
       i32x4 raw[kSteps];
-      EMBX_ISSUE_ROWS(r0, row, raw)
+      issue_rows(r0, row, lane_c, R, raw);
       bool inb1 = false, has1 = false, multi1 = false;
       int64_t id1 = -1;
       float w1 = 0.0f;
@@ -619,16 +621,13 @@ struct Single {
       const int nb = c0.be - c0.bs;
       GMEM float* const ob = as_global(a.out) + static_cast<int64_t>(r0.table) * a.E + NA * lane_sw;
       const int wlb = __float_as_int(wl);
-#define EMBX_STORE(U)                                                                               \
-  {                                                                                                 \
-    const int bi = U * S + sw;                                                                      \
-    const i32x4 x = row_bcast<U>(okv) ? raw[U] : zero4();                                           \
-    const float wx = W ? __int_as_float(row_bcast<U>(wlb)) : a.one;                                 \
-    if (bi < nb && active) store_row(ob + static_cast<int64_t>(c0.bs + bi) * ostride, x, wx);       \
-  }
-      EMBX_STORE(0) EMBX_STORE(1) EMBX_STORE(2) EMBX_STORE(3)
-      EMBX_STORE(4) EMBX_STORE(5) EMBX_STORE(6) EMBX_STORE(7)
-#undef EMBX_STORE
+      static_for<kSteps>([&](auto u) __attribute__((always_inline)) {
+        constexpr int U = decltype(u)::value;
+        const int bi = U * S + sw;
+        const i32x4 x = row_bcast<U>(okv) ? raw[U] : zero4();
+        const float wx = W ? __int_as_float(row_bcast<U>(wlb)) : a.one;
+        if (bi < nb && active) store_row(ob + static_cast<int64_t>(c0.bs + bi) * ostride, x, wx);
+      });
       if (__ballot(multi0) != 0) single_slow<G, F16, W>(a, r0, c0.bs, c0.be);
       if (c1.run < 0) return;
       c0 = c1;
@@ -698,9 +697,15 @@ __device__ __forceinline__ void single_slow(const LookupArgs& a, const RunInfo& 
   }
 }
 
+#ifdef EMBX_WAVES_PER_EU
+#define EMBX_OCCUPANCY __attribute__((amdgpu_waves_per_eu(EMBX_WAVES_PER_EU, EMBX_WAVES_PER_EU)))
+#else
+#define EMBX_OCCUPANCY
+#endif
+
 // W: every lookup carries a weight (a.weights).
 template <int G, bool F16, bool W>
-__global__ void __launch_bounds__(kBlock) gather_kernel(LookupArgs a) {
+__global__ void __launch_bounds__(kBlock) EMBX_OCCUPANCY gather_kernel(LookupArgs a) {
   extern __shared__ __align__(16) char smem_raw[];
   __shared__ int s_ctr[2];
   LMEM char* lds = (LMEM char*)smem_raw;
@@ -711,10 +716,10 @@ __global__ void __launch_bounds__(kBlock) gather_kernel(LookupArgs a) {
   if (tw && tid == 0) tw[0] = __builtin_amdgcn_s_memrealtime();
   {   // the worker's slot: a header record, then its runs
     GMEM const char* src = reinterpret_cast<GMEM const char*>(as_global(a.gr) + static_cast<int64_t>(wg) * a.gr_slot);
-    for (int q = tid; q < 3 * a.gr_slot; q += static_cast<int>(blockDim.x))
+    for (int q = tid; q < 3 * a.gr_slot; q += kBlock)
       *reinterpret_cast<LMEM uint4*>(lds + 16 * q) = *reinterpret_cast<GMEM const uint4*>(src + 16 * q);
   }
-  const int waves = static_cast<int>(blockDim.x) >> 6;
+  constexpr int waves = kBlock >> 6;   // (a compile-time count: read from blockDim it costs ~35 VGPRs)
   if (tid == 0) {
     s_ctr[0] = waves;
     s_ctr[1] = waves;
