@@ -148,6 +148,10 @@ typedef struct {
   int32_t kernel;           /* 0: the staged kernel (lookup_kernel, any plan); 1: the
                                wave-uniform gather kernel (gather_kernel; gather-only plans
                                with rows of 256, 512 or 1024 bytes)                        */
+  int32_t debug_checks;     /* 1: made with EMBX_DEBUG_CHECKS set -- every launch first checks
+                               its offsets (offsets[0] = 0, non-decreasing, within the indices'
+                               and weights' allocations; else EMB_ERR_INVALID_ARGUMENT, nothing
+                               launched) and reports out-of-range ids on stderr; synchronous  */
 } emb_plan_info_t;
 
 /* Builds a plan for T tables of rows[t] x E elements of `dtype`, for batches of up to
@@ -257,6 +261,20 @@ emb_status_t emb_plan_text(int32_t num_tables, const int64_t* rows, int32_t embe
 emb_status_t emb_default_beta(int32_t row_bytes, double* out, int32_t n);
 
 const char* emb_status_string(emb_status_t s);
+
+/* ---- input checks (debugging) ----------------------------------------------------------
+ * The checks every launch of a plan made with the environment variable EMBX_DEBUG_CHECKS
+ * set (not "0") runs first (emb_plan_info_t.debug_checks = 1), callable on their own: the
+ * launch's input as emb_lookup (weights NULL) or emb_lookup_weighted takes it.  Returns
+ * EMB_ERR_INVALID_ARGUMENT, with the first fault on stderr, if offsets[0] != 0, offsets
+ * decrease, or offsets[T*batch] indices (or weights) run past the device allocation that
+ * holds them (the extent hipMemGetAddressRange reports: a caching allocator's whole
+ * segment); ids outside their table are listed on stderr (first five) and not an error
+ * (the kernels skip and count them).  Synchronises `stream`, copies offsets and indices to
+ * the host, launches nothing.  EMB_ERR_INVALID_ARGUMENT also for a NULL plan, indices or
+ * offsets, or batch outside [1, max_batch]. */
+emb_status_t emb_debug_check_input(const emb_plan_t* plan, const int64_t* indices, const int64_t* offsets,
+                                   const float* weights, int32_t batch, void* stream);
 
 /* ---- index-handling probes (tests of the exact integer work) ---------------------------
  * Both run the same device functions as emb_lookup on one workgroup. */

@@ -20,9 +20,11 @@ budget for rows):
   P1  strategy choice per table at split k: minimum cost among the feasible
       strategies in the fixed order LDS, HOT, DEDUP, GATHER, STREAM (ties ->
       earlier).  LDS is feasible iff m_t R <= L; HOT iff C_t >= 1 with C_t =
-      min(hot rows listed, floor(L / R), 2048) the hot rows staged, h_t the
-      fraction of lookups they catch (summed in list order); u_t = unique
-      fraction (1 if unknown).  STREAM (the GM-UB flow of Sec. II-B: the table
+      min(hot rows listed, floor(L / R), 2048) the most hot rows one slice may
+      stage.  HOT stages the first C listed rows, C taken among 1, 2, 4, ...
+      below C_t and C_t itself, the one of least cost at the slice's lookups
+      (ties -> the smaller C); h(C) is the fraction of lookups those rows catch
+      (summed in list order).  u_t = unique fraction (1 if unknown).  STREAM (the GM-UB flow of Sec. II-B: the table
       moves through the buffer in chunks, each chunk serving the lookups that
       fall in it) takes c_t = ceil(m_t / floor(L / R)) chunks on one worker; it
       is a candidate when forced, or when c_t <= 64 and its cost stays below the
@@ -235,10 +237,14 @@ class _Table:
         self.s = float(st.mean_pooling)
         self.Lam = float(B) * self.s
         self.C = min(st.n_hot, L // R, MAX_HOT_SLOTS)
+        # HOT candidates (C, h(C)): C = 1, 2, 4, ... below the cap, and the cap
+        self.hot_sizes = []
         h = 0.0
         for k in range(self.C):
             h = h + float(st.hot_freq[k])
-        self.h = h
+            n = k + 1
+            if (n & (n - 1)) == 0 or n == self.C:
+                self.hot_sizes.append((n, h))
         u = float(st.unique_frac)
         self.u = u if (u > 0.0 and u <= 1.0) else 1.0
         self.fits = m * R <= L
@@ -267,24 +273,30 @@ class _Table:
         return math.isfinite(x) and x < COST_CAP
 
     def cost(self, b, strat, k):
+        """(cost, fixed cost, hot rows staged) of one slice at split k."""
         lam = self.Lam / float(k)
         if strat == LDS:
-            return cost_lds(b, self.m, self.R, lam)
+            return cost_lds(b, self.m, self.R, lam) + (0,)
         if strat == HOT:
-            return cost_hot(b, self.C, self.R, self.h, lam)
+            best = None
+            for C, h in self.hot_sizes:
+                c, f = cost_hot(b, C, self.R, h, lam)
+                if best is None or c < best[0]:
+                    best = (c, f, C)
+            return best
         if strat == DEDUP:
-            return cost_dedup(b, self.u, lam)
+            return cost_dedup(b, self.u, lam) + (0,)
         if strat == STREAM:
-            return cost_stream(b, self.m, self.R, lam, self.sc)
-        return cost_gather(b, lam)
+            return cost_stream(b, self.m, self.R, lam, self.sc) + (0,)
+        return cost_gather(b, lam) + (0,)
 
     def best(self, b, k):
-        """(strategy, cost, fixed cost) -- P1, ties to the earlier strategy."""
+        """(strategy, cost, fixed cost, hot rows staged) -- P1, ties to the earlier strategy."""
         best = None
         for s in self.allowed(b, k):
-            c, f = self.cost(b, s, k)
+            c, f, C = self.cost(b, s, k)
             if best is None or c < best[1]:
-                best = (s, c, f)
+                best = (s, c, f, C)
         return best
 
 
@@ -298,6 +310,7 @@ class _Item:
     strat: int = GATHER
     k: int = 1
     cost: int = 0          # cost of one slice at split k
+    C: int = 0             # HOT: hot rows staged
 
 
 def _validate(rows, E, dtype, stats, B, K, opts: Options):
@@ -379,8 +392,8 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
                 it = _Item(tb.t, i, c, r0, r1, LDS, 1, cost_chunk(b, r1 - r0, R, tb.Lam, c)[0])
                 g.append(it)
         else:
-            s, cst, _ = tb.best(b, 1)
-            g.append(_Item(tb.t, 0, 1, 0, tb.m, s, 1, cst))
+            s, cst, _, C = tb.best(b, 1)
+            g.append(_Item(tb.t, 0, 1, 0, tb.m, s, 1, cst, C))
         groups.append(g)
         items.extend(g)
 
@@ -394,7 +407,7 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
         """smallest k in [2, kmax] with cost_k <= max(tau, 2 fixed_k), else kmax."""
         tb = tabs[it.t]
         for k in range(2, kmax + 1):
-            s, cst, fx = _item_best(tb, it, k)
+            s, cst, fx, _ = _item_best(tb, it, k)
             if cst <= max(tau, 2 * fx):
                 return k
         return kmax
@@ -403,7 +416,7 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
         if it.nchunks > 1:
             lam = tb.Lam / float(k)
             c, f = cost_chunk(b, it.r1 - it.r0, R, lam, it.nchunks)
-            return LDS, c, f
+            return LDS, c, f, 0
         return tb.best(b, k)
 
     sym_max = opts.sym_max
@@ -420,11 +433,11 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
             ks = [1 if it.cost <= tau else split_k(it) for it in g]
         k = max(ks)
         for it in g:
-            s, cst, _ = _item_best(tabs[it.t], it, k)
-            it.strat, it.k, it.cost = s, k, cst
+            s, cst, _, C = _item_best(tabs[it.t], it, k)
+            it.strat, it.k, it.cost, it.C = s, k, cst, C
 
     def slices_of(it: _Item) -> List[Slice]:
-        C = tabs[it.t].C if it.strat == HOT else 0
+        C = it.C if it.strat == HOT else 0
         return [Slice(-1, it.t, it.strat, it.chunk, it.nchunks, it.r0, it.r1, it.k, j, C, it.cost)
                 for j in range(it.k)]
 
@@ -445,8 +458,8 @@ def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat
         for t in [x for x in paper_order if x in dem]:
             for it in groups[t]:
                 tb = tabs[t]
-                s, cst, _ = _item_best(tb, it, kmax)
-                sym = _Item(it.t, it.chunk, it.nchunks, it.r0, it.r1, s, kmax, cst)
+                s, cst, _, C = _item_best(tb, it, kmax)
+                sym = _Item(it.t, it.chunk, it.nchunks, it.r0, it.r1, s, kmax, cst, C)
                 for sl in slices_of(sym):
                     sl.wg = sl.j
                     sl.seq = seq

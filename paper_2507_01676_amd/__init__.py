@@ -42,7 +42,7 @@ MAX_HOT_STATS = 4096
 EXPORTED = ["emb_plan_create", "emb_plan_create_noalloc", "emb_plan_bind_weights", "emb_lookup", "emb_lookup_weighted", "emb_plan_check_errors",
             "emb_plan_serialize", "emb_plan_get_info", "emb_plan_destroy", "emb_plan_text",
             "emb_status_string", "emb_debug_dedup_tile", "emb_debug_hot_probe", "embx_fill_table",
-            "emb_plan_set_trace", "emb_default_beta"]
+            "emb_plan_set_trace", "emb_default_beta", "emb_debug_check_input"]
 
 
 class EmbxError(RuntimeError):
@@ -71,7 +71,8 @@ class _Info(ctypes.Structure):
                 ("lds_bytes", ctypes.c_int32), ("num_items", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("lds_budget_bytes", ctypes.c_int32), ("max_load_ps", ctypes.c_int64),
                 ("sum_load_ps", ctypes.c_int64), ("lif_milli", ctypes.c_int32), ("r_symmetric", ctypes.c_int32),
-                ("n_strategy", ctypes.c_int32 * 5), ("gather_runs", ctypes.c_int32 * 3), ("kernel", ctypes.c_int32)]
+                ("n_strategy", ctypes.c_int32 * 5), ("gather_runs", ctypes.c_int32 * 3), ("kernel", ctypes.c_int32),
+                ("debug_checks", ctypes.c_int32)]
 
 
 _vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
@@ -93,6 +94,7 @@ _lib.emb_plan_set_trace.argtypes = [_vp, _vp, _sz, ctypes.POINTER(_sz)]
 _lib.emb_default_beta.argtypes = [_i32, ctypes.POINTER(ctypes.c_double), _i32]
 _lib.emb_debug_dedup_tile.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp]
 _lib.emb_debug_hot_probe.argtypes = [_vp, _i32, _vp, _i32, _vp, _vp]
+_lib.emb_debug_check_input.argtypes = [_vp, _vp, _vp, _vp, _i32, _vp]
 _lib.embx_fill_table.argtypes = [_vp, _i64, _i64, _i32, _i32, _i32, ctypes.c_uint64, ctypes.c_double,
                                  ctypes.c_double, _i32, _vp]
 for _f in EXPORTED:
@@ -322,6 +324,12 @@ class Plan:
         d["gather_runs"] = {"wave": i.gather_runs[0], "single": i.gather_runs[1], "sw": i.gather_runs[2]}
         d["kernel"] = "gather_kernel" if i.kernel == 1 else "lookup_kernel"
         return d
+
+    def check_input(self, indices, offsets, batch: int, weights=None, stream=None):
+        """The input checks of EMBX_DEBUG_CHECKS on one launch's input (launches nothing)."""
+        _check(_lib.emb_debug_check_input(self._h, indices.data_ptr(), offsets.data_ptr(),
+                                          weights.data_ptr() if weights is not None else None, int(batch),
+                                          _stream_ptr(stream)), "emb_debug_check_input")
 
     def hot_probe(self, table: int, idx, stream=None):
         import torch

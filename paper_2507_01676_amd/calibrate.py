@@ -34,7 +34,10 @@ coefficients are times, and the planner refuses negative ones.
 device and needs the extension.  ``python -m paper_2507_01676_amd.calibrate``
 runs both on the synthetic workloads and prints the fitted vector; with
 ``--report`` it re-plans the workloads with that vector and sets each plan's
-predicted makespan beside the measured one.
+predicted makespan beside the measured one, and with ``--loop N`` it closes the
+loop: plan, run the plan with its timers on, add the plan's own timings to the
+samples, fit again and re-plan, for up to N rounds or until the plans stop
+changing (``loop``).
 """
 from __future__ import annotations
 
@@ -167,13 +170,8 @@ def _plan_items(text: str):
     return out
 
 
-def measure(plan, indices, offsets, batch: int, out, host_offsets: np.ndarray, stats, R: int,
-            warm: int = 3) -> Samples:
-    """Runs one traced launch of ``plan`` and turns its timers into samples.
-
-    ``host_offsets`` is the batch's CSR offsets on the host (to count each
-    slice's lookups); ``stats`` the per-table statistics the plan was made from.
-    """
+def traced_launch(plan, indices, offsets, batch: int, out, warm: int = 3) -> np.ndarray:
+    """``warm`` untimed launches, then one with the kernel timers on; returns the timers."""
     import torch
     for _ in range(warm):
         plan.lookup(indices, offsets, batch, out)
@@ -183,14 +181,20 @@ def measure(plan, indices, offsets, batch: int, out, host_offsets: np.ndarray, s
     plan.lookup(indices, offsets, batch, out)
     torch.cuda.synchronize()
     plan.set_trace(None)
-    tr = buf.cpu().numpy()
+    return buf.cpu().numpy()
+
+
+def samples_of(plan, tr: np.ndarray, batch: int, host_offsets: np.ndarray, stats, R: int) -> Samples:
+    """The samples one traced launch gives: each staged slice's time, and each worker's
+    gather phase (its gather slices run merged).  ``host_offsets`` is the batch's CSR
+    offsets on the host (to count each slice's lookups); ``stats`` the per-table
+    statistics the plan was made from."""
     info = plan.info()
     K = info["num_workers"]
     per = 2 + 1024 // 64
     tw = tr[:K * per].reshape(K, per)
     ti = tr[K * per:].reshape(-1, 2)
     items = _plan_items(plan.serialize())
-    T = len(stats)
     s = Samples()
     gcount = np.zeros(K, dtype=np.int64)
     glam = np.zeros(K, dtype=np.float64)
@@ -218,14 +222,30 @@ def measure(plan, indices, offsets, batch: int, out, host_offsets: np.ndarray, s
     return s
 
 
+def measure(plan, indices, offsets, batch: int, out, host_offsets: np.ndarray, stats, R: int,
+            warm: int = 3) -> Samples:
+    """Runs one traced launch of ``plan`` and turns its timers into samples."""
+    return samples_of(plan, traced_launch(plan, indices, offsets, batch, out, warm), batch, host_offsets, stats, R)
+
+
 def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("gather", "lds", "hot", "dedup"),
-            lds_max_bytes: int = 32 << 20, log=print, dists: Sequence[str] = ("config",)) -> Samples:
+            lds_max_bytes: int = 32 << 20, log=print, dists: Sequence[str] = ("config",),
+            hot_sizes: Sequence[int] = (1, 8, 64, 512)) -> Samples:
     """Measures the synthetic workloads with each strategy forced on every table, under
-    each query distribution of ``dists`` (the workload's own, 'uniform', 'fixed')."""
+    each query distribution of ``dists`` (the workload's own, 'uniform', 'fixed').
+
+    HOT runs once per size in ``hot_sizes``: each table's statistics list only its C
+    hottest rows, and the plan is made with a vector that prices staging and LDS reads at
+    nothing (SH = L1 = 0), so that every listed row is staged and the samples span C."""
+    import dataclasses
+
     import torch
     import workloads as W
-    from . import Plan, fill_table
+    from . import Plan, default_beta, fill_table
     code = {"lds": LDS, "hot": HOT, "dedup": DEDUP, "gather": GATHER}
+    stage_all = list(default_beta(256))
+    stage_all[SH] = 0.0
+    stage_all[L1] = 0.0
     allS = Samples()
     for cfg, dist in [(cfg, d) for cfg in configs for d in dists]:
         c = W.with_distribution(W.make_config(cfg), dist)
@@ -240,6 +260,7 @@ def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("ga
         idx = torch.from_numpy(bt.indices).cuda()
         off = torch.from_numpy(bt.offsets).cuda()
         out = torch.empty((c.batch, c.T, c.E), device="cuda")
+        runs = []
         for name in strategies:
             force = [code[name]] * c.T
             if name == "lds":
@@ -247,8 +268,16 @@ def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("ga
                 # gather, and those gather workers are not samples (their time follows
                 # the staged slices on the same workers)
                 force = [LDS if m * c.row_bytes <= lds_max_bytes else GATHER for m in c.rows]
-            plan = Plan(c.rows, c.E, c.dtype, stats, c.batch, force=force).bind(ws)
-            s = measure(plan, idx, off, c.batch, out, bt.offsets, stats, c.row_bytes)
+            if name == "hot":
+                for C in hot_sizes:
+                    st_c = [dataclasses.replace(x, hot_rows=x.hot_rows[:C], hot_freq=x.hot_freq[:C]) for x in stats]
+                    runs.append((f"hot C<={C}", force, st_c, stage_all))
+            else:
+                runs.append((name, force, stats, None))
+        for name, force, st_r, plan_beta in runs:
+            extra = {} if plan_beta is None else {"beta": plan_beta}
+            plan = Plan(c.rows, c.E, c.dtype, st_r, c.batch, force=force, **extra).bind(ws)
+            s = measure(plan, idx, off, c.batch, out, bt.offsets, st_r, c.row_bytes)
             plan.close()
             if name == "lds":
                 s.workers = []
@@ -260,11 +289,14 @@ def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("ga
     return allS
 
 
-def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=print) -> List[Dict]:
+def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=print,
+           samples: Optional[Samples] = None) -> List[Dict]:
     """Re-plans each workload with ``beta`` and sets the plan's predicted makespan (the
     most loaded worker, in the cost model's units) beside the measured one: the slowest
     worker's span from the kernel timers and the mean launch time of back-to-back
-    launches."""
+    launches.  With ``samples``, the traced launch's own slices and workers are added to it."""
+    import hashlib
+
     import torch
     import workloads as W
     from . import Plan, fill_table
@@ -289,32 +321,110 @@ def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=pri
         torch.cuda.synchronize()
         # raw-pointer launches, as bench.py times them (no per-call argument checks)
         ip, op, rp, sp = idx.data_ptr(), off.data_ptr(), out.data_ptr(), torch.cuda.current_stream().cuda_stream
+        n_launch = 50 if cfg != 5 else 10
         a.record()
-        for _ in range(50):
+        for _ in range(n_launch):
             plan.lookup_ptr(ip, op, c.batch, rp, sp)
         b.record()
         torch.cuda.synchronize()
-        launch_us = a.elapsed_time(b) * 1e3 / 50
-        n = plan.trace_size()
-        buf = torch.zeros(n, dtype=torch.int64, device="cuda")
-        plan.set_trace(buf)
-        plan.lookup(idx, off, c.batch, out)
-        torch.cuda.synchronize()
-        plan.set_trace(None)
+        launch_us = a.elapsed_time(b) * 1e3 / n_launch
+        tr = traced_launch(plan, idx, off, c.batch, out, warm=0)
         info = plan.info()
         K = info["num_workers"]
         per = 2 + 1024 // 64
-        tw = buf.cpu().numpy()[:K * per].reshape(K, per)
+        tw = tr[:K * per].reshape(K, per)
         span_us = float((tw[:, 2:].max() - tw[:, 0].min()) * TICK_PS / 1e6)
-        r = dict(workload=cfg, strategies=info["n_strategy"], lif_milli=info["lif_milli"],
-                 predicted_us=info["max_load_ps"] / 1e6, measured_span_us=span_us, launch_us=launch_us)
-        log(f"workload {cfg}: plan {r['strategies']} lif {r['lif_milli']}; predicted makespan "
+        if samples is not None:
+            s = samples_of(plan, tr, c.batch, bt.offsets, stats, c.row_bytes)
+            samples.slices += s.slices
+            samples.workers += s.workers
+        text = plan.serialize()
+        r = dict(workload=cfg, strategies=info["n_strategy"], kernel=info["kernel"], lif_milli=info["lif_milli"],
+                 predicted_us=info["max_load_ps"] / 1e6, measured_span_us=span_us, launch_us=launch_us,
+                 plan_sha=hashlib.sha256(text.encode()).hexdigest()[:16])
+        log(f"workload {cfg}: plan {r['strategies']} ({r['kernel']}) lif {r['lif_milli']}; predicted makespan "
             f"{r['predicted_us']:.1f} us, measured worker span {span_us:.1f} us, launch {launch_us:.1f} us")
         rows_out.append(r)
         plan.close()
         del ws
         torch.cuda.empty_cache()
     return rows_out
+
+
+def loop(beta: Sequence[float], samples: Samples, configs: Sequence[int] = (1, 2, 3, 4), rounds: int = 3,
+         base: Optional[Sequence[float]] = None, log=print) -> Dict:
+    """The calibration loop closed (Sec. III-A): plan every workload with the current
+    coefficients, run each plan with its timers on, add the plan's own slice and worker
+    times to the samples, fit again and re-plan; stops after ``rounds`` rounds or as soon
+    as a fit leaves every plan as it was.  Returns the final vector and each round's
+    predicted and measured makespans."""
+    beta = list(beta)
+    history = []
+    prev = None
+    for r in range(rounds):
+        rows = report(beta, configs, log=log, samples=samples)
+        history.append(dict(round=r, beta=dict(zip(BETA_NAMES, beta)), workloads=rows))
+        shas = [x["plan_sha"] for x in rows]
+        beta = fit_beta(samples, base)
+        log(f"round {r}: refit on {len(samples.slices)} slices and {len(samples.workers)} workers: "
+            + " ".join(f"{n}={v:.4g}" for n, v in zip(BETA_NAMES, beta)))
+        if shas == prev:
+            break
+        prev = shas
+    return dict(beta=dict(zip(BETA_NAMES, beta)), rounds=history)
+
+
+def write_samples_csv(s: Samples, path: str, max_rows: int = 1200, seed: int = 0) -> None:
+    """The samples as CSV (one header line of column names; kind = worker or slice), at
+    most ``max_rows`` of each kind, picked at random with ``seed`` when there are more."""
+    g = np.random.default_rng(seed)
+
+    def pick(xs):
+        if len(xs) <= max_rows:
+            return list(xs)
+        keep = np.sort(g.choice(len(xs), size=max_rows, replace=False))
+        return [xs[i] for i in keep]
+
+    with open(path, "w") as f:
+        f.write("kind,strat,lam,mu,R,c,h,u,n_slices,ps\n")
+        for w in pick(s.workers):
+            f.write(f"worker,{GATHER},{w.lam:.17g},0,0,1,0,1,{w.n_slices},{w.ps:.17g}\n")
+        for st in (LDS, HOT, DEDUP):
+            for x in pick([x for x in s.slices if x.strat == st]):
+                f.write(f"slice,{x.strat},{x.lam:.17g},{x.mu:.17g},{x.R},{x.c},{x.h:.17g},{x.u:.17g},0,{x.ps:.17g}\n")
+
+
+def read_samples_csv(path: str) -> Samples:
+    s = Samples()
+    with open(path) as f:
+        head = None
+        for ln in f:
+            if ln.startswith("#") or not ln.strip():
+                continue
+            v = ln.strip().split(",")
+            if head is None:
+                head = v
+                continue
+            d = dict(zip(head, v))
+            if d["kind"] == "worker":
+                s.workers.append(WorkerSample(int(d["n_slices"]), float(d["lam"]), float(d["ps"])))
+            else:
+                s.slices.append(SliceSample(int(d["strat"]), float(d["lam"]), float(d["mu"]), int(d["R"]),
+                                            int(d["c"]), float(d["h"]), float(d["u"]), float(d["ps"])))
+    return s
+
+
+def _residuals(b, s: Samples, log):
+    for st, nm in ((LDS, "LDS"), (HOT, "HOT"), (DEDUP, "DEDUP")):
+        xs = [x for x in s.slices if x.strat == st]
+        if xs:
+            err = np.array([predict(b, x) - x.ps for x in xs])
+            rel = np.abs(err) / np.maximum(np.array([x.ps for x in xs]), 1e6)
+            log(f"{nm}: {len(xs)} slices, rms residual {np.sqrt(np.mean(err ** 2)) / 1e6:.2f} us, "
+                f"median relative {np.median(rel):.2f}")
+    if s.workers:
+        err = np.array([predict(b, x) - x.ps for x in s.workers])
+        log(f"GATHER: {len(s.workers)} workers, rms residual {np.sqrt(np.mean(err ** 2)) / 1e6:.2f} us")
 
 
 def main(argv=None) -> int:
@@ -324,14 +434,26 @@ def main(argv=None) -> int:
     ap.add_argument("--strategies", nargs="+", default=["gather", "lds", "hot", "dedup"])
     ap.add_argument("--dists", nargs="+", default=["config"],
                     help="query distributions to measure under (config, uniform, fixed)")
+    ap.add_argument("--hot-sizes", type=int, nargs="+", default=[1, 8, 64, 512],
+                    help="hot rows listed per table in the HOT runs (one run per size)")
     ap.add_argument("--base", default=None,
                     help="coefficients kept where no sample fits them: 'builtin' (the library's own), "
                          "or a JSON file of {name: value}")
+    ap.add_argument("--samples-in", default=None, help="start from these samples (CSV) instead of measuring")
+    ap.add_argument("--samples-csv", default=None, help="write the forced-strategy samples as CSV")
     ap.add_argument("--out", default=None, help="write the samples and the fit as JSON")
     ap.add_argument("--report", type=int, nargs="*", default=None,
                     help="re-plan these workloads with the fitted beta and compare predicted and measured makespans")
+    ap.add_argument("--loop", type=int, default=0,
+                    help="rounds of plan -> traced run -> refit -> re-plan over the --report workloads")
     a = ap.parse_args(argv)
-    s = collect(a.configs, a.strategies, log=lambda m: print(m, file=sys.stderr, flush=True), dists=a.dists)
+    log = lambda m: print(m, file=sys.stderr, flush=True)   # noqa: E731
+    if a.samples_in:
+        s = read_samples_csv(a.samples_in)
+    else:
+        s = collect(a.configs, a.strategies, log=log, dists=a.dists, hot_sizes=a.hot_sizes)
+    if a.samples_csv:
+        write_samples_csv(s, a.samples_csv)
     base = None
     if a.base == "builtin":
         from . import default_beta
@@ -341,24 +463,19 @@ def main(argv=None) -> int:
             given = json.load(f)
         base = [float(given.get(n, 0.0)) for n in BETA_NAMES]
     b = fit_beta(s, base)
-    names = BETA_NAMES
-    for st, nm in ((LDS, "LDS"), (HOT, "HOT"), (DEDUP, "DEDUP")):
-        xs = [x for x in s.slices if x.strat == st]
-        if xs:
-            err = np.array([predict(b, x) - x.ps for x in xs])
-            print(f"{nm}: {len(xs)} slices, rms residual {np.sqrt(np.mean(err ** 2)) / 1e6:.2f} us", file=sys.stderr)
-    if s.workers:
-        err = np.array([predict(b, x) - x.ps for x in s.workers])
-        print(f"GATHER: {len(s.workers)} workers, rms residual {np.sqrt(np.mean(err ** 2)) / 1e6:.2f} us",
-              file=sys.stderr)
-    print(json.dumps(dict(zip(names, b))))
-    rep = None
-    if a.report is not None:
-        rep = report(b, a.report or (1, 2, 3, 4), log=lambda m: print(m, file=sys.stderr, flush=True))
+    _residuals(b, s, log)
+    print(json.dumps(dict(zip(BETA_NAMES, b))))
+    rep = lp = None
+    configs = a.report if a.report else (1, 2, 3, 4)
+    if a.loop > 0:
+        lp = loop(b, s, configs, rounds=a.loop, base=base, log=log)
+        print(json.dumps(lp["beta"]))
+    elif a.report is not None:
+        rep = report(b, configs, log=log)
     if a.out:
         with open(a.out, "w") as f:
-            json.dump(dict(beta=dict(zip(names, b)), report=rep, slices=[x.__dict__ for x in s.slices],
-                           workers=[x.__dict__ for x in s.workers]), f)
+            json.dump(dict(beta=dict(zip(BETA_NAMES, b)), report=rep, loop=lp,
+                           n_slices=len(s.slices), n_workers=len(s.workers)), f)
     return 0
 
 

@@ -7,6 +7,7 @@
 #include <atomic>
 #include <climits>
 #include <cmath>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <mutex>
@@ -54,6 +55,8 @@ struct emb_plan {
   std::vector<int32_t> mean;             // per table: 1 = mean pooling
   int32_t gather_runs[3] = {0, 0, 0};    // runs per gather queue class, over all workers
   bool in_scratch = false;               // device data in the device's scratch array (no allocation)
+  bool debug_checks = false;             // EMBX_DEBUG_CHECKS: host-side checks of every launch's input
+  std::vector<int64_t> rows;             // per table
   uint64_t scratch_gen = 0;              // which creation in the scratch array this plan is
 };
 
@@ -107,7 +110,23 @@ emb_status_t to_plan_in(int32_t T, const int64_t* rows, int32_t E, emb_dtype_t d
     }
     if (opts->force_strategy) in->force.assign(opts->force_strategy, opts->force_strategy + T);
   }
+  // EMBX_FORCE_STRATEGY (debugging): every table to one strategy, over the options
+  if (const char* fs = std::getenv("EMBX_FORCE_STRATEGY")) {
+    if (*fs) {
+      static const char* const names[] = {"lds", "hot", "dedup", "gather", "stream"};
+      int code = -1;
+      for (int i = 0; i < 5; ++i)
+        if (std::strcmp(fs, names[i]) == 0) code = i;
+      if (code < 0) return EMB_ERR_INVALID_ARGUMENT;
+      in->force.assign(T, code);
+    }
+  }
   return EMB_OK;
+}
+
+bool env_on(const char* name) {
+  const char* v = std::getenv(name);
+  return v && *v && std::strcmp(v, "0") != 0;
 }
 
 emb_status_t write_text(const std::string& s, char* buf, size_t cap, size_t* len_out) {
@@ -638,9 +657,91 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
     emb_plan_destroy(p);
     return EMB_ERR_DEVICE;
   }
+  p->rows.assign(rows, rows + T);
+  p->debug_checks = env_on("EMBX_DEBUG_CHECKS");
+  if (env_on("EMBX_LOG")) {
+    // the plan in one line: strategies, load balance and predicted makespan (Sec. III-B)
+    int32_t ns[5] = {0, 0, 0, 0, 0};
+    for (const PSlice& x : P.slices) ns[x.strat] += 1;
+    std::fprintf(stderr,
+                 "embx plan: T %d E %d %s R %d K %d B %d; slices %zu (LDS %d HOT %d DEDUP %d GATHER %d STREAM %d); "
+                 "LIF %.3f, %d tables symmetric; predicted makespan %.2f us; kernel %s, %d threads, LDS %d B%s\n",
+                 T, embedding_dim, p->f16 ? "f16" : "f32", P.R, K, max_batch, P.slices.size(), ns[0], ns[1], ns[2],
+                 ns[3], ns[4], P.lif_milli / 1000.0, P.r_sym, P.max_ps / 1e6,
+                 wave_gather ? "gather_kernel" : "lookup_kernel", block, p->lds_bytes,
+                 p->debug_checks ? "; debug checks on" : "");
+  }
   *plan_out = p;
   return EMB_OK;
 }
+
+}  // namespace
+
+extern "C" {
+
+// The checks of EMBX_DEBUG_CHECKS: the launch's CSR offsets must start at 0, never
+// decrease, and stay within the allocations that hold the indices (and weights);
+// out-of-range ids are reported (the kernel skips and counts them as usual).
+// Synchronises the stream; launches nothing.
+emb_status_t emb_debug_check_input(const emb_plan_t* plan, const int64_t* indices, const int64_t* offsets,
+                                   const float* weights, int32_t batch, void* stream) {
+  if (!plan || !indices || !offsets || batch < 1 || batch > plan->Bmax) return EMB_ERR_INVALID_ARGUMENT;
+  if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return EMB_ERR_DEVICE;
+  const size_t n_off = static_cast<size_t>(plan->T) * batch + 1;
+  std::vector<int64_t> off(n_off);
+  if (hipMemcpy(off.data(), offsets, n_off * sizeof(int64_t), hipMemcpyDeviceToHost) != hipSuccess)
+    return EMB_ERR_DEVICE;
+  if (off[0] != 0) {
+    std::fprintf(stderr, "embx debug check: offsets[0] = %lld, must be 0\n", static_cast<long long>(off[0]));
+    return EMB_ERR_INVALID_ARGUMENT;
+  }
+  for (size_t i = 1; i < n_off; ++i)
+    if (off[i] < off[i - 1]) {
+      std::fprintf(stderr, "embx debug check: offsets[%zu] = %lld < offsets[%zu] = %lld\n", i,
+                   static_cast<long long>(off[i]), i - 1, static_cast<long long>(off[i - 1]));
+      return EMB_ERR_INVALID_ARGUMENT;
+    }
+  const int64_t n = off[n_off - 1];
+  auto within = [](const void* p, size_t bytes, const char* what) {
+    void* base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess || !base) {
+      std::fprintf(stderr, "embx debug check: %s is not a device allocation\n", what);
+      return false;
+    }
+    const uintptr_t end = reinterpret_cast<uintptr_t>(base) + size;
+    if (reinterpret_cast<uintptr_t>(p) + bytes > end) {
+      std::fprintf(stderr, "embx debug check: offsets[T*batch] = %zu %s run past their allocation (%zu bytes left)\n",
+                   bytes / (what[0] == 'i' ? 8 : 4), what, static_cast<size_t>(end - reinterpret_cast<uintptr_t>(p)));
+      return false;
+    }
+    return true;
+  };
+  if (n > 0 && (!within(indices, static_cast<size_t>(n) * 8, "indices") ||
+                (weights && !within(weights, static_cast<size_t>(n) * 4, "weights"))))
+    return EMB_ERR_INVALID_ARGUMENT;
+  if (n == 0) return EMB_OK;
+  std::vector<int64_t> ids(static_cast<size_t>(n));
+  if (hipMemcpy(ids.data(), indices, static_cast<size_t>(n) * 8, hipMemcpyDeviceToHost) != hipSuccess)
+    return EMB_ERR_DEVICE;
+  int64_t bad = 0;
+  for (int32_t t = 0; t < plan->T; ++t)
+    for (int64_t q = off[static_cast<size_t>(t) * batch]; q < off[static_cast<size_t>(t + 1) * batch]; ++q)
+      if (ids[q] < 0 || ids[q] >= plan->rows[t]) {
+        if (bad < 5)
+          std::fprintf(stderr, "embx debug check: table %d, indices[%lld] = %lld outside [0, %lld)\n", t,
+                       static_cast<long long>(q), static_cast<long long>(ids[q]),
+                       static_cast<long long>(plan->rows[t]));
+        ++bad;
+      }
+  if (bad) std::fprintf(stderr, "embx debug check: %lld ids out of range (skipped and counted)\n",
+                        static_cast<long long>(bad));
+  return EMB_OK;
+}
+
+}  // extern "C"
+
+namespace {
 
 }  // namespace
 
@@ -674,6 +775,10 @@ emb_status_t lookup_impl(emb_plan_t* plan, const int64_t* indices, const int64_t
   if ((reinterpret_cast<uintptr_t>(out) & 15u) != 0 || (reinterpret_cast<uintptr_t>(indices) & 7u) != 0 ||
       (reinterpret_cast<uintptr_t>(offsets) & 7u) != 0 || (reinterpret_cast<uintptr_t>(weights) & 3u) != 0)
     return EMB_ERR_INVALID_ARGUMENT;
+  if (plan->debug_checks) {
+    const emb_status_t dc = emb_debug_check_input(plan, indices, offsets, weighted ? weights : nullptr, batch, stream);
+    if (dc != EMB_OK) return dc;
+  }
   LookupArgs a;
   a.items = plan->d_items;
   a.wg_ptr = plan->d_wg_ptr;
@@ -753,6 +858,7 @@ emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info) {
   info->row_bytes = plan->R;
   info->num_workers = plan->K;
   info->block_threads = plan->block;
+  info->debug_checks = plan->debug_checks ? 1 : 0;
   info->lds_bytes = plan->lds_bytes;
   info->num_items = static_cast<int32_t>(plan->plan.slices.size());
   info->max_batch = plan->Bmax;

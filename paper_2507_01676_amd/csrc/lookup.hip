@@ -656,42 +656,53 @@ __device__ __forceinline__ void walk_wave(GMEM const int64_t* __restrict__ indic
 
 // ---------------------------------------------------------------- staging
 
+// Every thread keeps kStageU 16-byte loads in flight (a 1024-thread worker moves 128 KiB
+// per round trip); the last partial round is issued whole before any of its stores.
+#ifndef EMBX_STAGE_U
+#define EMBX_STAGE_U 8
+#endif
+constexpr int kStageU = EMBX_STAGE_U;
+
 __device__ __forceinline__ void stage_linear(lchar* dst, gchar* src, int64_t bytes, int tid) {
   const int64_t n16 = bytes >> 4;
   int64_t q = tid;
-  for (; q + 3 * kBlock < n16; q += 4 * kBlock) {
-    const uint4 a = ldg16(src + q * 16);
-    const uint4 b = ldg16(src + (q + kBlock) * 16);
-    const uint4 c = ldg16(src + (q + 2 * kBlock) * 16);
-    const uint4 d = ldg16(src + (q + 3 * kBlock) * 16);
-    sts16(dst + q * 16, a);
-    sts16(dst + (q + kBlock) * 16, b);
-    sts16(dst + (q + 2 * kBlock) * 16, c);
-    sts16(dst + (q + 3 * kBlock) * 16, d);
+  for (; q + (kStageU - 1) * kBlock < n16; q += kStageU * kBlock) {
+    uint4 v[kStageU];
+#pragma unroll
+    for (int i = 0; i < kStageU; ++i) v[i] = ldg16(src + (q + i * kBlock) * 16);
+#pragma unroll
+    for (int i = 0; i < kStageU; ++i) sts16(dst + (q + i * kBlock) * 16, v[i]);
   }
-  for (; q < n16; q += kBlock) sts16(dst + q * 16, ldg16(src + q * 16));
+  uint4 v[kStageU];
+#pragma unroll
+  for (int i = 0; i < kStageU; ++i)
+    if (q + i * kBlock < n16) v[i] = ldg16(src + (q + i * kBlock) * 16);
+#pragma unroll
+  for (int i = 0; i < kStageU; ++i)
+    if (q + i * kBlock < n16) sts16(dst + (q + i * kBlock) * 16, v[i]);
 }
 
-// rows ids[0..n) of the table -> dst rows 0..n (16-byte pieces spread over the workgroup)
+// rows ids[0..n) of the table -> dst rows 0..n (16-byte pieces spread over the workgroup):
+// each round loads its pieces' ids, then all their row pieces, then stores them
 template <class IdPtr>
 __device__ __forceinline__ void stage_rows(lchar* dst, gchar* w, IdPtr ids, int n, int R, int tid) {
   const int RP = R >> 4;
   const int total = n * RP;
-  int q = tid;
-  for (; q + 3 * kBlock < total; q += 4 * kBlock) {
-    uint4 v[4];
+  for (int q = tid; q < total; q += kStageU * kBlock) {
+    int64_t src[kStageU];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kStageU; ++i) {
       const int qq = q + i * kBlock;
-      const int s = qq / RP;
-      v[i] = ldg16(w + static_cast<int64_t>(ids[s]) * R + (qq - s * RP) * 16);
+      const int s2 = qq < total ? qq / RP : 0;
+      src[i] = static_cast<int64_t>(ids[s2]) * R + (qq - s2 * RP) * 16;
     }
+    uint4 v[kStageU];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) sts16(dst + static_cast<int64_t>(q + i * kBlock) * 16, v[i]);
-  }
-  for (; q < total; q += kBlock) {
-    const int s = q / RP;
-    sts16(dst + static_cast<int64_t>(q) * 16, ldg16(w + static_cast<int64_t>(ids[s]) * R + (q - s * RP) * 16));
+    for (int i = 0; i < kStageU; ++i)
+      if (q + i * kBlock < total) v[i] = ldg16(w + src[i]);
+#pragma unroll
+    for (int i = 0; i < kStageU; ++i)
+      if (q + i * kBlock < total) sts16(dst + static_cast<int64_t>(q + i * kBlock) * 16, v[i]);
   }
 }
 

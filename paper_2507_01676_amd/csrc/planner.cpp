@@ -1,7 +1,8 @@
 // Planner: cost model (Eq. (2) extended to the four GPU data flows) and the
 // greedy asymmetric mapping of Sec. III-B.  Steps:
 //   P1 per-table strategy at split k: cheapest feasible of LDS, HOT, DEDUP, GATHER,
-//      STREAM (that order breaks ties);
+//      STREAM (that order breaks ties); HOT at the cheapest hot-set size C among
+//      1, 2, 4, ... below the cap and the cap itself (ties to the smaller C);
 //   P2 (Sec. III-B step 1) a table larger than the LDS budget L is cut into the fewest
 //      row chunks of at most floor(min(chunk_max, L) / R) rows if its best unsplit cost
 //      exceeds the sum of the chunk costs;
@@ -84,8 +85,9 @@ CF cost_stream(const std::array<double, B_COUNT>& b, int64_t m, int64_t R, doubl
 struct Tab {
   int32_t t;
   int64_t m;
-  double s, Lam, h, u;
-  int32_t C;
+  double s, Lam, u;
+  int32_t C;             // hot rows that may be staged: min(listed, L / R, kMaxHotSlots)
+  std::vector<std::pair<int32_t, double>> hc;   // HOT candidates (C, h(C)), C ascending
   bool fits;
   int64_t sc;            // STREAM chunks: ceil(m / floor(L / R))
   int32_t force;
@@ -94,6 +96,7 @@ struct Tab {
 struct Best {
   int32_t strat;
   int64_t cost, fixed;
+  int32_t C;             // HOT: hot rows staged
 };
 
 struct Item {
@@ -102,6 +105,7 @@ struct Item {
   int32_t strat;
   int32_t k;
   int64_t cost;
+  int32_t C;             // HOT: hot rows staged
 };
 
 struct Planner {
@@ -115,11 +119,26 @@ struct Planner {
 
   explicit Planner(const PlanIn& i) : in(i) {}
 
-  CF cost_of(const Tab& tb, int32_t strat, int32_t k) const {
+  // HOT at the cheapest of the table's hot-set sizes (ties to the smaller)
+  CF hot_best(const Tab& tb, double lam, int32_t* C) const {
+    CF out{0, 0};
+    *C = 0;
+    for (const auto& ch : tb.hc) {
+      CF c = cost_hot(b, ch.first, R, ch.second, lam);
+      if (*C == 0 || c.cost < out.cost) {
+        out = c;
+        *C = ch.first;
+      }
+    }
+    return out;
+  }
+
+  CF cost_of(const Tab& tb, int32_t strat, int32_t k, int32_t* C) const {
     const double lam = tb.Lam / static_cast<double>(k);
+    *C = 0;
     switch (strat) {
       case S_LDS: return cost_lds(b, tb.m, R, lam);
-      case S_HOT: return cost_hot(b, tb.C, R, tb.h, lam);
+      case S_HOT: return hot_best(tb, lam, C);
       case S_DEDUP: return cost_dedup(b, tb.u, lam);
       case S_STREAM: return cost_stream(b, tb.m, R, lam, tb.sc);
       default: return cost_gather(b, lam);
@@ -137,14 +156,15 @@ struct Planner {
   }
 
   Best best(const Tab& tb, int32_t k) const {
-    Best out{-1, 0, 0};
+    Best out{-1, 0, 0, 0};
     for (int32_t s = S_LDS; s <= S_STREAM; ++s) {
       if (tb.force != S_AUTO && s != tb.force) continue;
       if (s == S_LDS && !tb.fits) continue;
       if (s == S_HOT && tb.C < 1) continue;
       if (s == S_STREAM && tb.force == S_AUTO && !stream_ok(tb, k)) continue;
-      CF c = cost_of(tb, s, k);
-      if (out.strat < 0 || c.cost < out.cost) out = {s, c.cost, c.fixed};
+      int32_t C = 0;
+      CF c = cost_of(tb, s, k, &C);
+      if (out.strat < 0 || c.cost < out.cost) out = {s, c.cost, c.fixed, C};
     }
     return out;
   }
@@ -154,7 +174,7 @@ struct Planner {
     if (it.nchunks > 1) {
       const double lam = tb.Lam / static_cast<double>(k);
       CF c = cost_chunk(b, it.r1 - it.r0, R, lam, it.nchunks);
-      return {S_LDS, c.cost, c.fixed};
+      return {S_LDS, c.cost, c.fixed, 0};
     }
     return best(tb, k);
   }
@@ -180,7 +200,7 @@ struct Planner {
   }
 
   void slices_of(const Item& it, std::vector<PSlice>* out) const {
-    const int32_t C = it.strat == S_HOT ? tabs[it.t].C : 0;
+    const int32_t C = it.strat == S_HOT ? it.C : 0;
     for (int32_t j = 0; j < it.k; ++j)
       out->push_back({-1, it.t, it.strat, it.chunk, it.nchunks, it.r0, it.r1, it.k, j, C, it.cost, 0});
   }
@@ -201,6 +221,7 @@ struct Planner {
         sym.strat = bb.strat;
         sym.k = kmax;
         sym.cost = bb.cost;
+        sym.C = bb.C;
         std::vector<PSlice> tmp;
         slices_of(sym, &tmp);
         for (PSlice& sl : tmp) {
@@ -308,9 +329,17 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     tb.s = ti.mean_pooling;
     tb.Lam = static_cast<double>(in.B) * tb.s;
     tb.C = static_cast<int32_t>(std::min<int64_t>(std::min<int64_t>(ti.n_hot, P.L / P.R), kMaxHotSlots));
-    double h = 0.0;
-    for (int32_t k = 0; k < tb.C; ++k) h = h + ti.hot_freq[k];
-    tb.h = h;
+    {   // h(C): share of the lookups on the first C listed rows, summed in list order
+      double h = 0.0;
+      int32_t next = 1;
+      for (int32_t k = 0; k < tb.C; ++k) {
+        h = h + ti.hot_freq[k];
+        if (k + 1 == next || k + 1 == tb.C) {
+          tb.hc.emplace_back(k + 1, h);
+          while (next <= k + 1) next *= 2;
+        }
+      }
+    }
     tb.u = (ti.unique_frac > 0.0 && ti.unique_frac <= 1.0) ? ti.unique_frac : 1.0;
     tb.fits = tb.m * P.R <= P.L;
     tb.sc = (tb.m + P.L / P.R - 1) / (P.L / P.R);
@@ -344,11 +373,11 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
         for (int64_t i = 0; i < c; ++i) {
           const int64_t r0 = (i * tb.m) / c, r1 = ((i + 1) * tb.m) / c;
           g.push_back({tb.t, static_cast<int32_t>(i), static_cast<int32_t>(c), r0, r1, S_LDS, 1,
-                       cost_chunk(P.b, r1 - r0, P.R, tb.Lam, c).cost});
+                       cost_chunk(P.b, r1 - r0, P.R, tb.Lam, c).cost, 0});
         }
       } else {
         Best bb = P.best(tb, 1);
-        g.push_back({tb.t, 0, 1, 0, tb.m, bb.strat, 1, bb.cost});
+        g.push_back({tb.t, 0, 1, 0, tb.m, bb.strat, 1, bb.cost, bb.C});
       }
       for (const Item& it : g) all.push_back(it);
       P.groups.push_back(std::move(g));
@@ -380,6 +409,7 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
         it.strat = bb.strat;
         it.k = k;
         it.cost = bb.cost;
+        it.C = bb.C;
       }
     }
 
@@ -454,8 +484,9 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     out->sum_ps = static_cast<int64_t>(sum);
     out->lif_milli = P.lif_of(best_ld);
     out->r_sym = best_r;
-    out->C_of_table.assign(T, 0);
-    for (int32_t t = 0; t < T; ++t) out->C_of_table[t] = P.tabs[t].C;
+    out->C_of_table.assign(T, 0);   // one k per table, hence one hot-set size
+    for (const PSlice& x : out->slices)
+      if (x.strat == S_HOT) out->C_of_table[x.t] = x.C;
   } catch (const CostErr&) {
     return fail(1, "cost model out of range (non-finite or above 2^40 ps) or too many slices");
   }

@@ -62,7 +62,7 @@ struct PlanOut {
   int64_t max_ps = 0, sum_ps = 0;
   int64_t lif_milli = 0;
   int32_t r_sym = 0;
-  std::vector<int32_t> C_of_table;   // hot rows staged per table (HOT items)
+  std::vector<int32_t> C_of_table;   // hot rows staged per table (its HOT slices' C; 0: none)
 };
 
 // Built-in coefficients (picoseconds), fitted on MI355X by OLS over synthetic workloads

@@ -543,3 +543,36 @@ def test_stream_is_a_candidate_up_to_64_chunks(m, stream):
     p = OPL.plan_reference([m], 64, "f32", [OPL.Stat(1.0, 1, [], 1.0)], 16, 4, opts)
     strats = {sl.strat for sl in p.slices}
     assert strats == ({OPL.STREAM} if stream else {OPL.GATHER})
+
+
+def _hot_worked(hot_freq, SH):
+    """One table of 10^6 rows (beyond L: no LDS; 123 STREAM chunks: no STREAM), E = 4 fp32
+    (R = 16 B), B = 64, pooling 1 (lam = 64 lookups), K = 1; gather 100 ps a lookup, LDS and
+    DEDUP priced out, HOT = SH x C x R + lam (1 - h(C)) G1."""
+    beta = [0.0] * OPL.NBETA
+    beta[OPL.G1], beta[OPL.SH] = 100.0, SH
+    beta[OPL.L0], beta[OPL.D0] = 1e9, 1e9
+    stats = [OPL.Stat(1.0, 1, list(hot_freq), 1.0)]
+    return [1_000_000], 4, "f32", stats, 64, 1, OPL.Options(beta=beta)
+
+
+HOT_WORKED = {
+    # hot_freq 2^-1 .. 2^-10: cap 10, candidates C = 1, 2, 4, 8, 10; cost 16 C + 6400 (1 - h(C)):
+    #   3216, 1632, 464, 128 + 25 = 153, 160 + 6.25 = 166.25 -> C = 8, cost 153 (gather: 6400)
+    "ten": ([2.0 ** -(i + 1) for i in range(10)], 1.0, 8, 153),
+    # the first six of them: candidates 1, 2, 4, 6 -> 3216, 1632, 464, 96 + 100 = 196 -> C = 6 (the cap)
+    "six": ([2.0 ** -(i + 1) for i in range(6)], 1.0, 6, 196),
+    # nothing past the second row and no staging cost: h(2) = h(4) = h(5) = 0.75, cost 1600 for
+    # each, against 3200 at C = 1 -> the tie goes to the smaller size, C = 2
+    "tie": ([0.5, 0.25, 0.0, 0.0, 0.0], 0.0, 2, 1600),
+}
+
+
+@pytest.mark.parametrize("case", sorted(HOT_WORKED))
+def test_hot_stages_the_cheapest_hot_set_worked_by_hand(case):
+    """P1 prices HOT at each hot-set size C = 1, 2, 4, ... below the cap and at the cap, and
+    stages the cheapest (ties to the smaller C), with h(C) the share of the first C listed
+    rows; values worked by hand in HOT_WORKED."""
+    freq, SH, C, cost = HOT_WORKED[case]
+    p = OPL.plan_reference(*_hot_worked(freq, SH))
+    assert [(sl.strat, sl.C, sl.cost) for sl in p.slices] == [(OPL.HOT, C, cost)]

@@ -169,8 +169,8 @@ def test_cpp_planner_equals_oracle_with_many_tables_of_mixed_shares(seed):
 
 
 def test_cpp_planner_equals_oracle_on_the_pinned_instances():
-    """The hand-worked literal-solver plans and the boundary instances of the P4 and STREAM
-    rules, through the C++ planner."""
+    """The hand-worked literal-solver and hot-set plans and the boundary instances of the P4
+    and STREAM rules, through the C++ planner."""
     from test_oracle_plan import _worked
     for norepl, lif in ((True, 2000), (False, 2000), (True, 1500)):
         got, want = _both(*_worked(norepl, lif))
@@ -184,3 +184,25 @@ def test_cpp_planner_equals_oracle_on_the_pinned_instances():
         got, want = _both([m], 64, "f32", [OPL.Stat(1.0, 1, [], 1.0)], 16, 4,
                           OPL.Options(beta=beta, no_replication=True))
         assert got == want
+    from test_oracle_plan import HOT_WORKED, _hot_worked
+    for freq, SH, _, _ in HOT_WORKED.values():
+        got, want = _both(*_hot_worked(freq, SH))
+        assert got == want
+
+
+def test_force_strategy_environment_variable(monkeypatch):
+    """EMBX_FORCE_STRATEGY (a debugging switch) forces every table to one strategy, as the
+    force_strategy option does; an unknown name is refused."""
+    rows, E, dtype, stats, B, K, opts = _random_instance(3)
+    embx = _lib()
+    for name, code in (("gather", OPL.GATHER), ("dedup", OPL.DEDUP), ("stream", OPL.STREAM)):
+        monkeypatch.setenv("EMBX_FORCE_STRATEGY", name)
+        got = _cpp(rows, E, dtype, stats, B, K, opts)
+        forced = OPL.Options(**{**opts.__dict__, "force": [code] * len(rows)})
+        assert got == OPL.plan_reference(rows, E, dtype, stats, B, K, forced).text()
+        assert {int(ln.split()[3]) for ln in got.splitlines() if ln.startswith("item ")} == {code}
+    monkeypatch.setenv("EMBX_FORCE_STRATEGY", "fastest")
+    with pytest.raises(embx.EmbxError):
+        _cpp(rows, E, dtype, stats, B, K, opts)
+    monkeypatch.setenv("EMBX_FORCE_STRATEGY", "")
+    assert _cpp(rows, E, dtype, stats, B, K, opts) == OPL.plan_reference(rows, E, dtype, stats, B, K, opts).text()
