@@ -92,29 +92,30 @@ class PlanError(ValueError):
 
 
 def default_beta(R: int) -> List[float]:
-    """Built-in coefficients (picoseconds), fitted on MI355X by OLS (Eq. (2)).
+    """Built-in coefficients (picoseconds): the least-squares fit (Eq. (2), Sec. III-A) of the
+    MI355X calibration samples in tests/golden/calibration_samples.csv, each rounded to three
+    significant digits.
 
-    Measured with every strategy forced in turn on the synthetic workloads with
-    R = 256 B rows (uniform, Zipf and single-hot-table mixes); the per-lookup
-    terms are latency-bound there and serve unchanged for other row sizes.
-    HOT (H0, SH, P) and DEDUP (D0, D1) were fitted again, with the other
-    coefficients held, on workloads 1-4 under their own and under fixed queries,
-    which vary the staged hot rows C from 1 to 512, with residuals relative to each
-    slice's predicted time (so that short slices set the fixed costs).
+    The fit is sequential, each stage on what the earlier ones leave, and every stage is
+    reweighted once so that residuals count relative to each sample's predicted time:
+    GATHER (G0 per slice, G1 per lookup) on the workers' gather phases; LDS (L0, S per staged
+    byte, L1 per lookup) on whole-table slices; I on the row-chunk slices; HOT (H0, SH per
+    staged byte, P per lookup) and DEDUP (D0, D1 per lookup).  The samples use R = 256 B
+    rows; the per-lookup terms serve unchanged for other row sizes.
     """
     del R
     b = [0.0] * NBETA
-    b[G0] = 131000.0
-    b[G1] = 10900.0
-    b[L0] = 1670000.0
-    b[L1] = 10950.0
-    b[S] = 477.0
-    b[I] = 8280.0
-    b[H0] = 3990000.0
-    b[P] = 1180.0
-    b[D0] = 6690000.0
-    b[D1] = 26720.0
-    b[SH] = 45.0
+    b[G0] = 480000.0
+    b[G1] = 6370.0
+    b[L0] = 997000.0
+    b[L1] = 11100.0
+    b[S] = 41.1
+    b[I] = 38500.0
+    b[H0] = 4110000.0
+    b[P] = 5790.0
+    b[D0] = 8190000.0
+    b[D1] = 24600.0
+    b[SH] = 35.5
     return b
 
 

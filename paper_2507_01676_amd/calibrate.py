@@ -44,6 +44,7 @@ from __future__ import annotations
 import json
 import sys
 from dataclasses import dataclass, field
+from types import SimpleNamespace
 from typing import Dict, List, Optional, Sequence
 
 import numpy as np
@@ -289,6 +290,33 @@ def collect(configs: Sequence[int] = (2, 3, 4), strategies: Sequence[str] = ("ga
     return allS
 
 
+def collect_staging(sizes: Sequence[int] = (16, 64, 128, 256, 512), E: int = 64, K: int = 256, B: int = 256,
+                    log=print) -> Samples:
+    """Whole-table LDS slices that differ only in the bytes they stage: K tables of m rows
+    (E fp32), one slice per worker (no batch splits, K workers), B bags of one lookup each,
+    for each m in ``sizes`` -- the workloads' few small tables alone leave the per-byte
+    staging term S undetermined."""
+    import torch
+    from . import Plan
+    s_all = Samples()
+    g = np.random.default_rng(7)
+    for m in sizes:
+        ws = [torch.empty((m, E), device="cuda").uniform_(-1.0, 1.0) for _ in range(K)]
+        st = [dict(mean_pooling=1.0, max_pooling=1) for _ in range(K)]
+        plan = Plan([m] * K, E, "f32", st, B, force=[LDS] * K, num_workers=K, no_replication=True).bind(ws)
+        ids = g.integers(0, m, size=K * B).astype(np.int64)
+        off = np.arange(K * B + 1, dtype=np.int64)
+        out = torch.empty((B, K, E), device="cuda")
+        s = measure(plan, torch.from_numpy(ids).cuda(), torch.from_numpy(off).cuda(), B, out, off,
+                    [SimpleNamespace(unique_frac=1.0, hot_freq=None)] * K, E * 4)
+        plan.close()
+        log(f"staging sweep, {m} rows a table: {len(s.slices)} slices")
+        s_all.slices += s.slices
+        del ws
+        torch.cuda.empty_cache()
+    return s_all
+
+
 def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=print,
            samples: Optional[Samples] = None) -> List[Dict]:
     """Re-plans each workload with ``beta`` and sets the plan's predicted makespan (the
@@ -374,9 +402,10 @@ def loop(beta: Sequence[float], samples: Samples, configs: Sequence[int] = (1, 2
     return dict(beta=dict(zip(BETA_NAMES, beta)), rounds=history)
 
 
-def write_samples_csv(s: Samples, path: str, max_rows: int = 1200, seed: int = 0) -> None:
+def write_samples_csv(s: Samples, path: str, max_rows: int = 250, seed: int = 0) -> None:
     """The samples as CSV (one header line of column names; kind = worker or slice), at
-    most ``max_rows`` of each kind, picked at random with ``seed`` when there are more."""
+    most ``max_rows`` of each group (gather workers; whole-table LDS; LDS row chunks; HOT;
+    DEDUP), picked at random with ``seed`` when there are more."""
     g = np.random.default_rng(seed)
 
     def pick(xs):
@@ -388,10 +417,12 @@ def write_samples_csv(s: Samples, path: str, max_rows: int = 1200, seed: int = 0
     with open(path, "w") as f:
         f.write("kind,strat,lam,mu,R,c,h,u,n_slices,ps\n")
         for w in pick(s.workers):
-            f.write(f"worker,{GATHER},{w.lam:.17g},0,0,1,0,1,{w.n_slices},{w.ps:.17g}\n")
-        for st in (LDS, HOT, DEDUP):
-            for x in pick([x for x in s.slices if x.strat == st]):
-                f.write(f"slice,{x.strat},{x.lam:.17g},{x.mu:.17g},{x.R},{x.c},{x.h:.17g},{x.u:.17g},0,{x.ps:.17g}\n")
+            f.write(f"worker,{GATHER},{w.lam:.8g},0,0,1,0,1,{w.n_slices},{w.ps:.8g}\n")
+        groups = [[x for x in s.slices if x.strat == LDS and x.c == 1], [x for x in s.slices if x.strat == LDS and x.c > 1],
+                  [x for x in s.slices if x.strat == HOT], [x for x in s.slices if x.strat == DEDUP]]
+        for grp in groups:
+            for x in pick(grp):
+                f.write(f"slice,{x.strat},{x.lam:.8g},{x.mu:.8g},{x.R},{x.c},{x.h:.8g},{x.u:.8g},0,{x.ps:.8g}\n")
 
 
 def read_samples_csv(path: str) -> Samples:
@@ -452,6 +483,9 @@ def main(argv=None) -> int:
         s = read_samples_csv(a.samples_in)
     else:
         s = collect(a.configs, a.strategies, log=log, dists=a.dists, hot_sizes=a.hot_sizes)
+        if "lds" in a.strategies:
+            st = collect_staging(log=log)
+            s.slices += st.slices
     if a.samples_csv:
         write_samples_csv(s, a.samples_csv)
     base = None

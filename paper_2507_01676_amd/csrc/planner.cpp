@@ -269,17 +269,17 @@ struct Planner {
 
 std::array<double, B_COUNT> default_beta(int32_t) {
   std::array<double, B_COUNT> b{};
-  b[B_G0] = 131000.0;
-  b[B_G1] = 10900.0;
-  b[B_L0] = 1670000.0;
-  b[B_L1] = 10950.0;
-  b[B_S] = 477.0;
-  b[B_I] = 8280.0;
-  b[B_H0] = 3990000.0;
-  b[B_P] = 1180.0;
-  b[B_D0] = 6690000.0;
-  b[B_D1] = 26720.0;
-  b[B_SH] = 45.0;
+  b[B_G0] = 480000.0;
+  b[B_G1] = 6370.0;
+  b[B_L0] = 997000.0;
+  b[B_L1] = 11100.0;
+  b[B_S] = 41.1;
+  b[B_I] = 38500.0;
+  b[B_H0] = 4110000.0;
+  b[B_P] = 5790.0;
+  b[B_D0] = 8190000.0;
+  b[B_D1] = 24600.0;
+  b[B_SH] = 35.5;
   return b;
 }
 

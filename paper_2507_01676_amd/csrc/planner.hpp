@@ -65,8 +65,9 @@ struct PlanOut {
   std::vector<int32_t> C_of_table;   // hot rows staged per table (its HOT slices' C; 0: none)
 };
 
-// Built-in coefficients (picoseconds), fitted on MI355X by OLS over synthetic workloads
-// with R = 256 B rows and every strategy forced in turn; used for every row size.
+// Built-in coefficients (picoseconds): the least-squares fit of MI355X calibration samples
+// (synthetic workloads, R = 256 B rows, every strategy forced in turn, plus a staging-size
+// sweep), rounded to three significant digits; used for every row size.
 std::array<double, B_COUNT> default_beta(int32_t R);
 
 // Returns 0 on success, otherwise an emb_status_t code with a message in *err.

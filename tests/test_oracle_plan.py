@@ -188,8 +188,10 @@ def test_gather_tables_are_partitioned_symmetrically():
     # fewer samples than workers: k = B (with sym_max > 0 every gather table is split)
     p = OPL.plan_reference(rows, 64, "f32", stats, 5, K, OPL.Options(force=[OPL.GATHER] * 3, sym_max=10))
     assert all(s.k == 5 for s in p.slices)
-    # by default slices of 1..8 lookups are too small to split a table into
-    p = OPL.plan_reference(rows, 64, "f32", stats, 5, K, OPL.Options(force=[OPL.GATHER] * 3))
+    # by default slices of 1..8 lookups are too small to split a table into symmetrically
+    # (the LIF fallback, which may still do so, is held off here)
+    p = OPL.plan_reference(rows, 64, "f32", stats, 5, K,
+                           OPL.Options(force=[OPL.GATHER] * 3, lif_milli=1_000_000))
     assert not any(s.k == 5 for s in p.slices if s.t == 0)
 
 
