@@ -362,6 +362,9 @@ def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=pri
         per = 2 + 1024 // 64
         tw = tr[:K * per].reshape(K, per)
         span_us = float((tw[:, 2:].max() - tw[:, 0].min()) * TICK_PS / 1e6)
+        # each worker's busy time (start to its last wavefront's end), and the skew of starts
+        busy = (tw[:, 2:].max(axis=1) - tw[:, 0]).astype(np.float64) * TICK_PS / 1e6
+        skew_us = float((tw[:, 0].max() - tw[:, 0].min()) * TICK_PS / 1e6)
         if samples is not None:
             s = samples_of(plan, tr, c.batch, bt.offsets, stats, c.row_bytes)
             samples.slices += s.slices
@@ -369,9 +372,11 @@ def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=pri
         text = plan.serialize()
         r = dict(workload=cfg, strategies=info["n_strategy"], kernel=info["kernel"], lif_milli=info["lif_milli"],
                  predicted_us=info["max_load_ps"] / 1e6, measured_span_us=span_us, launch_us=launch_us,
+                 busy_mean_us=float(busy.mean()), busy_max_us=float(busy.max()), start_skew_us=skew_us,
                  plan_sha=hashlib.sha256(text.encode()).hexdigest()[:16])
         log(f"workload {cfg}: plan {r['strategies']} ({r['kernel']}) lif {r['lif_milli']}; predicted makespan "
-            f"{r['predicted_us']:.1f} us, measured worker span {span_us:.1f} us, launch {launch_us:.1f} us")
+            f"{r['predicted_us']:.1f} us, measured worker span {span_us:.1f} us (start skew {skew_us:.2f}, busy "
+            f"mean {busy.mean():.2f} max {busy.max():.2f}), launch {launch_us:.1f} us")
         rows_out.append(r)
         plan.close()
         del ws
