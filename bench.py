@@ -249,6 +249,10 @@ def main():
                     help="load-imbalance threshold x 1000 of the symmetric fallback (0: the library default)")
     ap.add_argument("--sym-max", type=int, default=0,
                     help="gather tables split over all workers while at most this many (0: the library default)")
+    ap.add_argument("--order-mode", type=int, default=0, choices=[0, 1],
+                    help="slice order of the placement: 0 longest first, 1 the paper's (s desc, m asc)")
+    ap.add_argument("--no-replication", action="store_true",
+                    help="no batch splits (replication 1); with --order-mode 1 the paper's solver as printed")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the lookup runs on a single MI355X "
@@ -295,6 +299,10 @@ def main():
         opts["sym_max"] = args.sym_max
     if args.lif_milli:
         opts["lif_milli"] = args.lif_milli
+    if args.order_mode:
+        opts["order_mode"] = args.order_mode
+    if args.no_replication:
+        opts["no_replication"] = True
     tp = time.time()
     plan = embx.Plan(c.rows, c.E, c.dtype, stats, c.batch, **opts).bind(weights)
     plan_ms = (time.time() - tp) * 1e3
@@ -428,7 +436,9 @@ def main():
         "launch_floor_us": floor_us,
         "plan": {"kernel": info["kernel"], "strategies": info["n_strategy"], "items": info["num_items"],
                  "lif_milli": info["lif_milli"],
-                 "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms},
+                 "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms,
+                 "options": {k: opts[k] for k in ("lif_milli", "sym_max", "order_mode", "no_replication")
+                             if k in opts}},
         "kernel_source_hash": src_hash,
         "cpu_baseline": cpu,
     }

@@ -165,7 +165,13 @@ typedef struct {
  * 8 (fp16), E <= 256; opts may be NULL.  On success *plan_out owns everything it allocated.
  * EMB_ERR_UNSUPPORTED when a worker would hold more gather slices than its run queue in
  * LDS takes (48 B each, about 3,400 in 160 KiB): with every table split over all workers,
- * more than ~3,400 tables; such plans need sym_max_gather < 0 (tables placed whole). */
+ * more than ~3,400 tables; such plans need sym_max_gather < 0 (tables placed whole).
+ * Environment (debugging, read at each creation): EMBX_LOG (not "0") prints the plan in one
+ * line on stderr -- strategies, LIF, predicted makespan, kernel; EMBX_FORCE_STRATEGY = lds,
+ * hot, dedup, gather or stream forces every table to that strategy over opts (any other
+ * non-empty value: EMB_ERR_INVALID_ARGUMENT; emb_plan_text honours it too);
+ * EMBX_DEBUG_CHECKS (not "0") makes every launch check its input first
+ * (emb_debug_check_input). */
 emb_status_t emb_plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_t* rows,
                              int32_t embedding_dim, emb_dtype_t dtype,
                              const emb_table_stats_t* stats, int32_t max_batch,

@@ -369,7 +369,8 @@ def report(beta: Sequence[float], configs: Sequence[int] = (1, 2, 3, 4), log=pri
             s = samples_of(plan, tr, c.batch, bt.offsets, stats, c.row_bytes)
             samples.slices += s.slices
             samples.workers += s.workers
-        text = plan.serialize()
+        # the plan's structure: every slice's placement and shape, without its cost
+        text = "\n".join(" ".join(ln.split()[:-1]) for ln in plan.serialize().splitlines() if ln.startswith("item "))
         r = dict(workload=cfg, strategies=info["n_strategy"], kernel=info["kernel"], lif_milli=info["lif_milli"],
                  predicted_us=info["max_load_ps"] / 1e6, measured_span_us=span_us, launch_us=launch_us,
                  busy_mean_us=float(busy.mean()), busy_max_us=float(busy.max()), start_skew_us=skew_us,

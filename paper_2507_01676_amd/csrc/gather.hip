@@ -5,7 +5,9 @@
 // The unit of work is a wavefront, and every decision it takes is wave-uniform: which
 // chunk of bags it walks, where a step starts and ends, where each bag ends.  So the
 // control lives in scalar registers and the vector registers hold only row data, the
-// accumulators and one index per lane (few enough for two 1024-thread workgroups per CU).
+// accumulators and one index per lane (92-117 VGPRs with kSteps = 12 rows in flight per
+// SW: one 1024-thread workgroup per CU, 4 wavefronts per SIMD; measured, 12 in flight at
+// that occupancy beats 6 or 8 at two workgroups per CU).
 //
 // A wavefront is S = 64 / G sub-wavefronts (SWs) of G lanes; lane i of a SW covers bytes
 // [16 i, 16 i + 16) of a row.  A step covers N = S * kSteps consecutive lookups of the

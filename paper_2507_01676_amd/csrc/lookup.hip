@@ -1,7 +1,9 @@
 // Multi-table embedding-bag lookup with sum pooling for gfx950 (MI355X).
 //
 // One persistent launch per batch: worker w (one 1024-thread workgroup per CU)
-// runs the plan's slices for w.  Inside a worker the unit of work is a
+// runs the plan's slices for w.  This kernel runs every plan with a staged slice (LDS,
+// HOT, DEDUP, STREAM) or with rows other than 256, 512 or 1024 bytes; gather-only plans
+// with those rows run the wave-uniform gather kernel of gather.hip.  Inside a worker the unit of work is a
 // sub-wavefront (SW) of G = (row bytes)/16 lanes rounded up to a power of two:
 // lane l of a SW covers bytes [16 l, 16 l + 16) of a row, so one SW moves one
 // row per 16-byte load (global_load_dwordx4 from HBM or ds_read_b128 from LDS).
