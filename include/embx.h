@@ -152,6 +152,9 @@ typedef struct {
                                its offsets (offsets[0] = 0, non-decreasing, within the indices'
                                and weights' allocations; else EMB_ERR_INVALID_ARGUMENT, nothing
                                launched) and reports out-of-range ids on stderr; synchronous  */
+  int32_t gather_steps;     /* gather_kernel: row loads in flight per lane per step (12, 13 or
+                               16, the one whose steps the plan's chunks fill best;
+                               EMBX_GATHER_STEPS overrides it); 0 for lookup_kernel           */
 } emb_plan_info_t;
 
 /* Builds a plan for T tables of rows[t] x E elements of `dtype`, for batches of up to

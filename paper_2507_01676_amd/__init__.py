@@ -72,7 +72,7 @@ class _Info(ctypes.Structure):
                 ("lds_budget_bytes", ctypes.c_int32), ("max_load_ps", ctypes.c_int64),
                 ("sum_load_ps", ctypes.c_int64), ("lif_milli", ctypes.c_int32), ("r_symmetric", ctypes.c_int32),
                 ("n_strategy", ctypes.c_int32 * 5), ("gather_runs", ctypes.c_int32 * 3), ("kernel", ctypes.c_int32),
-                ("debug_checks", ctypes.c_int32)]
+                ("debug_checks", ctypes.c_int32), ("gather_steps", ctypes.c_int32)]
 
 
 _vp, _i32, _i64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t

@@ -42,8 +42,10 @@ def _run(cmd, verbose):
 # lookup.hip is compiled in parts (EMBX_PART): one per (row type, weighted) kernel
 # family, plus the probes, filler and launch code
 LOOKUP_PARTS = 5
-# gather.hip: one part per (row type, weighted) kernel family
+# gather.hip: one part per (row type, weighted) kernel family, each built for every number
+# of row loads in flight per step a plan may choose (kGatherStepChoices in device_types.hpp)
 GATHER_PARTS = 4
+GATHER_STEPS = (12, 13, 16)
 
 
 def _run_all(cmds, verbose):
@@ -71,10 +73,12 @@ def build(verbose: bool = False) -> str:
         o = os.path.join(BUILD, f"lookup_{part}.o")
         cmds.append([hipcc, *HIP_FLAGS, f"-DEMBX_PART={part}", "-c", os.path.join(CSRC, "lookup.hip"), "-o", o])
         objs.append(o)
-    for part in range(GATHER_PARTS):
-        o = os.path.join(BUILD, f"gather_{part}.o")
-        cmds.append([hipcc, *HIP_FLAGS, f"-DEMBX_GPART={part}", "-c", os.path.join(CSRC, "gather.hip"), "-o", o])
-        objs.append(o)
+    for ks in GATHER_STEPS:
+        for part in range(GATHER_PARTS):
+            o = os.path.join(BUILD, f"gather_{part}_k{ks}.o")
+            cmds.append([hipcc, *HIP_FLAGS, f"-DEMBX_GPART={part}", f"-DEMBX_GKS={ks}", "-c",
+                         os.path.join(CSRC, "gather.hip"), "-o", o])
+            objs.append(o)
     o = os.path.join(BUILD, "api.o")
     cmds.append([hipcc, *HIP_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, "api.cpp"), "-o", o])
     objs.append(o)

@@ -51,6 +51,7 @@ struct emb_plan {
   bool staged = false;                   // the plan has LDS / HOT / DEDUP / STREAM slices
   bool wave_gather = false;              // launches the wave-uniform gather kernel (gather.hip)
   int block = kBlock;                    // threads per worker
+  int ksteps = 0;                        // gather_kernel: row loads in flight per lane per step
   unsigned long long* d_trace = nullptr;   // caller's timer buffer (not owned)
   std::vector<int32_t> mean;             // per table: 1 = mean pooling
   int32_t gather_runs[3] = {0, 0, 0};    // runs per gather queue class, over all workers
@@ -466,7 +467,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
   // fewer when that leaves some of the 16 wavefronts without one.
   //
   // The wave-uniform gather kernel's queues are single-lookup bags (chunks of one wavefront
-  // step: kGatherSteps S bags) and all other bags, in chunks of about 128 expected lookups, 192 when
+  // step: ksteps S bags) and all other bags, in chunks of about 128 expected lookups, 192 when
   // the worker's queue gives each wavefront at least 64 chunks (W / 16 >= 64 * 192, W the
   // worker's lookups in that queue), and at least two wavefront steps (EMBX_WAVE_CHUNK
   // overrides it).  Measured on workloads 3-5: shorter chunks keep a worker's wavefronts
@@ -474,6 +475,58 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
   // start (workload 5: 4358 us at 64 lookups, 4042 at 192, 4170 at 512).
   const char* env_chunk = std::getenv("EMBX_WAVE_CHUNK");
   const double wave_chunk_override = env_chunk ? std::atof(env_chunk) : 0.0;
+  // Rows in flight per step of the wave-uniform gather kernel (one build per choice): the
+  // choice with the fewest row rounds -- a chunk of c expected lookups takes ceil(c / N)
+  // steps of N = ks S lookups -- over the plan's multi-lookup chunks, ties to the smaller
+  // (fewer registers); plans without such chunks keep 12.  Measured on workloads 2-5 (12 /
+  // 13 / 16): workload 4's 100-lookup chunks (two bags of 50) take 3 / 2 / 2 steps and ran
+  // 14.3 / 13.5 / 14.1 us; workload 5 (chunks of ~180 lookups, N = 2 ks) 3966 / 3949 /
+  // 3929 us; workload 3 119.3 / 119.9 / 119.1 us; workload 2, single-lookup bags only, 5.4 /
+  // 5.7 / 5.8 us.  EMBX_GATHER_STEPS = 12, 13 or 16 overrides it.
+  int ksteps = 12;
+  if (wave_gather) {
+    const char* env_steps = std::getenv("EMBX_GATHER_STEPS");
+    if (env_steps && *env_steps) {
+      ksteps = std::atoi(env_steps);
+      bool known = false;
+      for (int c : kGatherStepChoices) known = known || c == ksteps;
+      if (!known) {
+        delete p;
+        return EMB_ERR_INVALID_ARGUMENT;
+      }
+    } else {
+      const int nwaves = block / 64;
+      double best = -1.0;
+      for (int cand : kGatherStepChoices) {
+        const double N = static_cast<double>(cand) * (64 / p->G);
+        double rounds = 0.0;
+        for (int w = 0; w < K; ++w) {
+          double Ws = 0.0;
+          for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
+            const DevItem& d = items[i];
+            if (d.strat != S_GATHER || stats[d.table].max_pooling == 1) continue;
+            const int64_t nb = (static_cast<int64_t>(d.j + 1) * max_batch) / d.k -
+                               (static_cast<int64_t>(d.j) * max_batch) / d.k;
+            Ws += static_cast<double>(nb) * std::max(1.0, stats[d.table].mean_pooling);
+          }
+          const double target = wave_chunk_override > 0.0 ? wave_chunk_override
+                                                          : std::max(2.0 * N, Ws / nwaves >= 64.0 * 192.0 ? 192.0 : 128.0);
+          for (int32_t i = wg_ptr[w]; i < wg_ptr[w + 1]; ++i) {
+            const DevItem& d = items[i];
+            if (d.strat != S_GATHER || stats[d.table].max_pooling == 1) continue;
+            const double s_t = std::max(1.0, stats[d.table].mean_pooling);
+            const double cb = std::max(1.0, std::floor(target / s_t));
+            const double nc = std::ceil(static_cast<double>((static_cast<int64_t>(max_batch) + d.k - 1) / d.k) / cb);
+            rounds += nc * std::ceil(cb * s_t / N);
+          }
+        }
+        if (best < 0.0 || rounds < best) {
+          best = rounds;
+          ksteps = cand;
+        }
+      }
+    }
+  }
   std::vector<GatherRun> gr;                       // runs, worker-major
   std::vector<int32_t> gr_ptr(K + 1, 0);
   std::vector<GatherSlotHeader> gr_head(K);
@@ -515,7 +568,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
       // of a SW's time and the worker's tail is up to one chunk, so ~sqrt(5 W / NSW)
       // lookups per chunk balances the two; measured, chunks past ~128 lookups lose again
       // (the SWs then work on fewer tables at a time), hence the cap
-      const double wstep = static_cast<double>(kGatherSteps) * (64 / p->G);   // lookups of one wave kernel step
+      const double wstep = static_cast<double>(ksteps) * (64 / p->G);   // lookups of one wave kernel step
       const double target =
           !wave_gather ? std::min(128.0, std::max(8.0, std::floor(std::sqrt(5.0 * Ws / nsw))))
           : wave_chunk_override > 0.0 ? wave_chunk_override
@@ -529,7 +582,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
           const DevItem& d = items[i];
           if (d.strat != S_GATHER || class_of(d) != cls) continue;
           const double s_t = std::max(1.0, stats[d.table].mean_pooling);
-          const int32_t cb = cls == 1 ? (wave_gather ? kGatherSteps * (64 / p->G) : kChunkSingle)
+          const int32_t cb = cls == 1 ? (wave_gather ? ksteps * (64 / p->G) : kChunkSingle)
                                       : static_cast<int32_t>(std::max(1.0, std::floor((cls == 0 ? wtarget : target) / s_t)));
           const int64_t nc = (slice_bags_any(d) + cb - 1) / cb;
           if (nc == 0) continue;
@@ -652,6 +705,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
   p->staged = staged;
   p->wave_gather = wave_gather;
   p->block = block;
+  p->ksteps = wave_gather ? ksteps : 0;
   p->lds_bytes = std::max(staged ? static_cast<int>(L) + kMetaReserve : 0, run_bytes);
   if (prepare_lookup_kernels(dev, static_cast<int>(smem) - kStaticLdsReserve) != 0) {
     emb_plan_destroy(p);
@@ -665,10 +719,11 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
     for (const PSlice& x : P.slices) ns[x.strat] += 1;
     std::fprintf(stderr,
                  "embx plan: T %d E %d %s R %d K %d B %d; slices %zu (LDS %d HOT %d DEDUP %d GATHER %d STREAM %d); "
-                 "LIF %.3f, %d tables symmetric; predicted makespan %.2f us; kernel %s, %d threads, LDS %d B%s\n",
+                 "LIF %.3f, %d tables symmetric; predicted makespan %.2f us; kernel %s (gather steps %d), "
+                 "%d threads, LDS %d B%s\n",
                  T, embedding_dim, p->f16 ? "f16" : "f32", P.R, K, max_batch, P.slices.size(), ns[0], ns[1], ns[2],
                  ns[3], ns[4], P.lif_milli / 1000.0, P.r_sym, P.max_ps / 1e6,
-                 wave_gather ? "gather_kernel" : "lookup_kernel", block, p->lds_bytes,
+                 wave_gather ? "gather_kernel" : "lookup_kernel", wave_gather ? ksteps : 0, block, p->lds_bytes,
                  p->debug_checks ? "; debug checks on" : "");
   }
   *plan_out = p;
@@ -805,7 +860,8 @@ emb_status_t lookup_impl(emb_plan_t* plan, const int64_t* indices, const int64_t
   a.one = 1.0f;
   a.weights = weighted ? weights : nullptr;
   if (plan->wave_gather)
-    return st(launch_gather(a, plan->G, plan->f16, weighted, plan->K, plan->block, plan->lds_bytes, stream));
+    return st(launch_gather(a, plan->G, plan->f16, weighted, plan->ksteps, plan->K, plan->block, plan->lds_bytes,
+                            stream));
   return st(launch_lookup(a, plan->G, plan->f16, plan->staged, weighted, plan->K, plan->lds_bytes, stream));
 }
 
@@ -859,6 +915,7 @@ emb_status_t emb_plan_get_info(const emb_plan_t* plan, emb_plan_info_t* info) {
   info->num_workers = plan->K;
   info->block_threads = plan->block;
   info->debug_checks = plan->debug_checks ? 1 : 0;
+  info->gather_steps = plan->ksteps;
   info->lds_bytes = plan->lds_bytes;
   info->num_items = static_cast<int32_t>(plan->plan.slices.size());
   info->max_batch = plan->Bmax;

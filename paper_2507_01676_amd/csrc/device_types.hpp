@@ -7,15 +7,6 @@
 namespace embx {
 
 constexpr int kBlock = 1024;        // threads per worker (16 wave64s: one worker per CU)
-#ifndef EMBX_KSTEPS
-#define EMBX_KSTEPS 12
-#endif
-// Wave-uniform gather kernel: row loads in flight per lane per step.  A step covers
-// kGatherSteps * 64 / G lookups (or, for single-lookup bags, bags), and a chunk of
-// single-lookup bags is one step.  Measured on MI355X (one 1024-thread worker per CU):
-// 6 -> 8 -> 12 -> 16 gave workload 5 4288 / 4120 / 3972 / 3936 us and workload 3
-// 123.8 / 120.6 / 115.1 / 119.3 us; two workers per CU at 64 VGPRs lost on every workload.
-constexpr int kGatherSteps = EMBX_KSTEPS;
 constexpr int kTile = 2048;         // DEDUP: lookups per sorted tile
 constexpr int kMetaReserve = 28928;   // LDS beyond the row budget: hot hash or dedup tile
 
@@ -107,19 +98,28 @@ constexpr int kTraceWorker = 2 + kBlock / 64;
 
 // Gather-only kernels with wave-uniform control (gather.hip), for rows of G = 16, 32 or
 // 64 lanes; one family per (row type, weighted) pair, nullptr for other G.
+// gather.hip is built once per number of row loads in flight per lane per step (a step
+// covers ks * 64 / G lookups, or single-lookup bags, and a chunk of single-lookup bags is
+// one step); each plan runs one of them, chosen at creation.
 using GatherKernelFn = void (*)(LookupArgs);
-GatherKernelFn gather_kernel_f32(int G);
-GatherKernelFn gather_kernel_f32_weighted(int G);
-GatherKernelFn gather_kernel_f16(int G);
-GatherKernelFn gather_kernel_f16_weighted(int G);
+constexpr int kGatherStepChoices[3] = {12, 13, 16};
+#define EMBX_DECL_GATHER(ks)                               \
+  GatherKernelFn gather_kernel_f32_k##ks(int G);          \
+  GatherKernelFn gather_kernel_f32_weighted_k##ks(int G); \
+  GatherKernelFn gather_kernel_f16_k##ks(int G);          \
+  GatherKernelFn gather_kernel_f16_weighted_k##ks(int G);
+EMBX_DECL_GATHER(12)
+EMBX_DECL_GATHER(13)
+EMBX_DECL_GATHER(16)
+#undef EMBX_DECL_GATHER
 
 // Host-callable launchers (defined in lookup.hip).
 int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weighted, int grid, int lds_bytes,
                   void* stream);
-int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int block, int lds_bytes,
+int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int ks, int grid, int block, int lds_bytes,
                   void* stream);
 // workgroups of `block` threads of the gather kernels for rows of G lanes that fit on one CU
-// at once (the smaller of the weighted and unweighted kernel's), 0 on error
+// at once (the least over weighted or not and every ks), 0 on error
 int gather_blocks_per_cu(int G, bool f16, int block);
 // once per device: lets every lookup kernel launch with up to max_dynamic_lds bytes of
 // dynamic LDS (0 = done, else an emb_status_t code)

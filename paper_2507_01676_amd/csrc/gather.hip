@@ -5,9 +5,10 @@
 // The unit of work is a wavefront, and every decision it takes is wave-uniform: which
 // chunk of bags it walks, where a step starts and ends, where each bag ends.  So the
 // control lives in scalar registers and the vector registers hold only row data, the
-// accumulators and one index per lane (92-117 VGPRs with kSteps = 12 rows in flight per
-// SW: one 1024-thread workgroup per CU, 4 wavefronts per SIMD; measured, 12 in flight at
-// that occupancy beats 6 or 8 at two workgroups per CU).
+// accumulators and one index per lane (92-128 VGPRs with kSteps = 12-16 rows in flight
+// per SW: one 1024-thread workgroup per CU, 4 wavefronts per SIMD; measured, 12 in flight
+// at that occupancy beats 6 or 8 at two workgroups per CU).  The file is built once per
+// kSteps (EMBX_GKS = 12, 13, 16) and a plan picks the one whose steps its chunks fill best.
 //
 // A wavefront is S = 64 / G sub-wavefronts (SWs) of G lanes; lane i of a SW covers bytes
 // [16 i, 16 i + 16) of a row.  A step covers N = S * kSteps consecutive lookups of the
@@ -39,6 +40,9 @@
 #ifndef EMBX_GPART
 #define EMBX_GPART -1
 #endif
+#ifndef EMBX_GKS
+#define EMBX_GKS 12
+#endif
 #ifndef EMBX_NT_IDS
 #define EMBX_NT_IDS 0
 #endif
@@ -69,7 +73,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 
-constexpr int kSteps = kGatherSteps;   // row loads in flight per lane per step
+constexpr int kSteps = EMBX_GKS;   // row loads in flight per lane per step (one build per value)
 static_assert(kSteps >= 1 && kSteps <= 16, "one id per lane of a row of 16 for each step");
 
 // f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>): a loop whose index
@@ -764,17 +768,19 @@ GatherFn pick_gather(int G) {
 
 }  // namespace
 
+#define EMBX_GNAME2(name, ks) name##_k##ks
+#define EMBX_GNAME(name, ks) EMBX_GNAME2(name, ks)
 #if EMBX_HAS_GPART(0)
-GatherKernelFn gather_kernel_f32(int G) { return pick_gather<false, false>(G); }
+GatherKernelFn EMBX_GNAME(gather_kernel_f32, EMBX_GKS)(int G) { return pick_gather<false, false>(G); }
 #endif
 #if EMBX_HAS_GPART(1)
-GatherKernelFn gather_kernel_f32_weighted(int G) { return pick_gather<false, true>(G); }
+GatherKernelFn EMBX_GNAME(gather_kernel_f32_weighted, EMBX_GKS)(int G) { return pick_gather<false, true>(G); }
 #endif
 #if EMBX_HAS_GPART(2)
-GatherKernelFn gather_kernel_f16(int G) { return pick_gather<true, false>(G); }
+GatherKernelFn EMBX_GNAME(gather_kernel_f16, EMBX_GKS)(int G) { return pick_gather<true, false>(G); }
 #endif
 #if EMBX_HAS_GPART(3)
-GatherKernelFn gather_kernel_f16_weighted(int G) { return pick_gather<true, true>(G); }
+GatherKernelFn EMBX_GNAME(gather_kernel_f16_weighted, EMBX_GKS)(int G) { return pick_gather<true, true>(G); }
 #endif
 
 }  // namespace embx

@@ -1717,9 +1717,18 @@ LookupKernelFn pick_any(int G, bool f16, bool staged, bool weighted) {
   return weighted ? lookup_kernel_f32_weighted(G, staged) : lookup_kernel_f32(G, staged);
 }
 
-GatherKernelFn pick_gather_any(int G, bool f16, bool weighted) {
-  if (f16) return weighted ? gather_kernel_f16_weighted(G) : gather_kernel_f16(G);
-  return weighted ? gather_kernel_f32_weighted(G) : gather_kernel_f32(G);
+GatherKernelFn pick_gather_any(int G, bool f16, bool weighted, int ks) {
+#define EMBX_PICK(k)                                                                  \
+  case k:                                                                            \
+    if (f16) return weighted ? gather_kernel_f16_weighted_k##k(G) : gather_kernel_f16_k##k(G); \
+    return weighted ? gather_kernel_f32_weighted_k##k(G) : gather_kernel_f32_k##k(G);
+  switch (ks) {
+    EMBX_PICK(12)
+    EMBX_PICK(13)
+    EMBX_PICK(16)
+    default: return nullptr;
+  }
+#undef EMBX_PICK
 }
 
 }  // namespace
@@ -1741,12 +1750,14 @@ int prepare_lookup_kernels(int device, int max_dynamic_lds) {
         return 4;
     }
   }
-  for (int G = 16; G <= 64; G <<= 1) {
-    for (int f = 0; f < 4; ++f) {
-      GatherKernelFn k = pick_gather_any(G, (f & 1) != 0, (f & 2) != 0);
-      if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
-                              max_dynamic_lds) != hipSuccess)
-        return 4;
+  for (int ks : kGatherStepChoices) {
+    for (int G = 16; G <= 64; G <<= 1) {
+      for (int f = 0; f < 4; ++f) {
+        GatherKernelFn k = pick_gather_any(G, (f & 1) != 0, (f & 2) != 0, ks);
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                max_dynamic_lds) != hipSuccess)
+          return 4;
+      }
     }
   }
   if (hipFuncSetAttribute(reinterpret_cast<const void*>(&dedup_probe_kernel),
@@ -1765,26 +1776,29 @@ int launch_lookup(const LookupArgs& a, int G, bool f16, bool staged, bool weight
   return hipGetLastError() == hipSuccess ? 0 : 4;
 }
 
-int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int grid, int block, int lds_bytes,
+int launch_gather(const LookupArgs& a, int G, bool f16, bool weighted, int ks, int grid, int block, int lds_bytes,
                   void* stream) {
-  GatherKernelFn k = pick_gather_any(G, f16, weighted);
+  GatherKernelFn k = pick_gather_any(G, f16, weighted, ks);
   if (!k) return 2;
   hipLaunchKernelGGL(k, dim3(grid), dim3(block), lds_bytes, static_cast<hipStream_t>(stream), a);
   return hipGetLastError() == hipSuccess ? 0 : 4;
 }
 
 int gather_blocks_per_cu(int G, bool f16, int block) {
-  int best = 0;
-  for (int w = 0; w < 2; ++w) {
-    GatherKernelFn k = pick_gather_any(G, f16, w != 0);
-    if (!k) return 0;
-    int n = 0;
-    // the run queue's LDS is small against a CU's 160 KiB; 16 KiB is assumed here
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(k), block, 16384) != hipSuccess)
-      return 0;
-    best = w == 0 ? n : std::min(best, n);
+  int best = -1;
+  for (int ks : kGatherStepChoices) {
+    for (int w = 0; w < 2; ++w) {
+      GatherKernelFn k = pick_gather_any(G, f16, w != 0, ks);
+      if (!k) return 0;
+      int n = 0;
+      // the run queue's LDS is small against a CU's 160 KiB; 16 KiB is assumed here
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(k), block, 16384) !=
+          hipSuccess)
+        return 0;
+      best = best < 0 ? n : std::min(best, n);
+    }
   }
-  return best;
+  return best < 0 ? 0 : best;
 }
 
 int launch_dedup_probe(const int64_t* idx, int n, int32_t* uniq, int32_t* inv, int32_t* n_uniq, void* stream) {
