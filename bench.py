@@ -436,6 +436,7 @@ def main():
         "launch_floor_us": floor_us,
         "plan": {"kernel": info["kernel"], "strategies": info["n_strategy"], "items": info["num_items"],
                  "lif_milli": info["lif_milli"], "predicted_us": info["max_load_ps"] / 1e6,
+                 "gather_steps": info["gather_steps"],
                  "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms,
                  "options": {k: opts[k] for k in ("lif_milli", "sym_max", "order_mode", "no_replication")
                              if k in opts}},

@@ -133,3 +133,40 @@ def test_unweighted_fit_misses_the_fixed_cost():
         x = CAL._lstsq(np.array(rows), np.array(ys))
         misses += abs(x[0] - b[CAL.H0]) > 0.25 * b[CAL.H0]
     assert misses >= 3
+
+
+def test_samples_csv_round_trip_keeps_each_group(tmp_path):
+    """write_samples_csv / read_samples_csv: every field survives (8 significant digits),
+    and the cap takes at most max_rows of each group (workers, whole LDS, LDS chunks,
+    HOT, DEDUP)."""
+    s = _samples(np.random.default_rng(11), n=600)
+    p = tmp_path / "s.csv"
+    CAL.write_samples_csv(s, str(p), max_rows=1000)
+    r = CAL.read_samples_csv(str(p))
+    assert len(r.workers) == len(s.workers) and len(r.slices) == len(s.slices)
+    key = lambda x: (x.strat, x.lam, x.mu, x.c, x.ps)   # noqa: E731
+    for a, b in zip(sorted(s.slices, key=key), sorted(r.slices, key=key)):
+        for f in ("strat", "R", "c"):
+            assert getattr(a, f) == getattr(b, f)
+        for f in ("lam", "mu", "h", "u", "ps"):
+            assert getattr(b, f) == pytest.approx(getattr(a, f), rel=1e-7, abs=1e-12)
+    for a, b in zip(sorted(s.workers, key=lambda x: (x.lam, x.ps)), sorted(r.workers, key=lambda x: (x.lam, x.ps))):
+        assert a.n_slices == b.n_slices and b.ps == pytest.approx(a.ps, rel=1e-7)
+    # the fit of what was read equals the fit of what was written, to the rounding
+    for x, y in zip(CAL.fit_beta(s), CAL.fit_beta(r)):
+        assert y == pytest.approx(x, rel=1e-5, abs=1e-3)
+    CAL.write_samples_csv(s, str(p), max_rows=7)
+    r = CAL.read_samples_csv(str(p))
+    assert len(r.workers) == 7
+    groups = [[x for x in r.slices if x.strat == CAL.LDS and x.c == 1],
+              [x for x in r.slices if x.strat == CAL.LDS and x.c > 1],
+              [x for x in r.slices if x.strat == CAL.HOT], [x for x in r.slices if x.strat == CAL.DEDUP]]
+    assert [len(g) for g in groups] == [7, 7, 7, 7]
+
+
+def test_committed_samples_read_back_as_written():
+    import os
+    here = os.path.dirname(os.path.abspath(__file__))
+    r = CAL.read_samples_csv(os.path.join(here, "golden", "calibration_samples.csv"))
+    assert len(r.workers) == 250 and len(r.slices) == 1000
+    assert {x.strat for x in r.slices} == {CAL.LDS, CAL.HOT, CAL.DEDUP}
