@@ -103,3 +103,26 @@ def check_sampled(c: W.Config, got: np.ndarray, batch: W.Batch, n_bags: int, see
         emp = (hi - lo) == 0
         assert np.all(got[bs[emp], t, :] == 0)
     return worst
+
+
+def check_index_columns(got: np.ndarray, batch: W.Batch, T: int, rows=None):
+    """Every bag of an integer-mode lookup, columns 0-4 only: they are functions of the row
+    id alone (1, the three base-2048 digits of the row, the table id + 1), so their sums
+    follow from the indices without the tables.  Exact in fp32 at any batch size.
+    ``rows`` (per table) marks out-of-range ids, which add nothing."""
+    B = batch.B
+    for t in range(T):
+        lo, hi = batch.offsets[t * B], batch.offsets[(t + 1) * B]
+        ids = batch.indices[lo:hi]
+        ok = np.ones(ids.size, bool) if rows is None else (ids >= 0) & (ids < rows[t])
+        idv = np.where(ok, ids, 0)
+        cols = np.stack([ok.astype(np.float64), (idv & 2047) * ok, ((idv >> 11) & 2047) * ok,
+                         ((idv >> 22) & 2047) * ok, (t + 1.0) * ok], axis=1).astype(np.float64)
+        # per-bag sums as differences of running sums (integers below 2^53: exact)
+        csum = np.zeros((ids.size + 1, 5))
+        np.cumsum(cols, axis=0, out=csum[1:])
+        ends = batch.offsets[t * B:(t + 1) * B + 1] - lo
+        want = (csum[ends[1:]] - csum[ends[:-1]]).astype(np.float32)
+        mine = got[:, t, :5]
+        bad = np.argwhere(mine != want)
+        assert bad.size == 0, f"table {t}: {bad.shape[0]} of {B * 5} index-column elements differ, first {bad[:3].tolist()}"

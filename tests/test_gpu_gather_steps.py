@@ -31,7 +31,7 @@ def steps_config(cfg_id, E, dtype, B=203):
 
 
 @pytest.mark.parametrize("ks", STEPS)
-@pytest.mark.parametrize("E,dtype", [(64, "f32"), (128, "f32"), (256, "f32"), (128, "f16")])
+@pytest.mark.parametrize("E,dtype", [(64, "f32"), (128, "f32"), (256, "f32"), (128, "f16"), (256, "f16")])
 def test_every_build_matches_the_oracle(monkeypatch, ks, E, dtype):
     import torch
     log(f"gather steps {ks}, E{E} {dtype}")
@@ -62,11 +62,12 @@ def test_every_build_matches_the_oracle(monkeypatch, ks, E, dtype):
 
 
 @pytest.mark.parametrize("ks", STEPS)
-def test_every_build_weighted_and_mean(monkeypatch, ks):
+@pytest.mark.parametrize("E,dtype", [(64, "f32"), (128, "f32"), (256, "f32"), (128, "f16"), (256, "f16")])
+def test_every_build_weighted_and_mean(monkeypatch, ks, E, dtype):
     import torch
-    log(f"gather steps {ks}: weighted, mean and sum tables")
+    log(f"gather steps {ks}, E{E} {dtype}: weighted, mean and sum tables")
     monkeypatch.setenv("EMBX_GATHER_STEPS", str(ks))
-    c = steps_config(161, 128, "f32")
+    c = steps_config(161, E, dtype)
     batch = W.gen_batch(c, 0)
     hw = host_tables(c, W.VAL_INTEGER)
     pooling = ["mean" if t % 2 == 0 else "sum" for t in range(c.T)]

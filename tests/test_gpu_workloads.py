@@ -1,8 +1,9 @@
 """Parity at the five workloads' full sizes, with the plan and launch the benchmark uses.
 
 Workloads 1-4 are checked on every output element (tables built on the host and
-uploaded); workload 5 (132.7 GB of tables) on sampled bags whose rows the oracle
-regenerates on the host, bit-exact on integer tables.  The batch-size sweep's plans
+uploaded); workload 5 (132.7 GB of tables) on every bag in the columns that follow from the
+indices alone (integer tables) and on sampled bags whose rows the oracle regenerates
+on the host, bit-exact on integer tables.  The batch-size sweep's plans
 are checked at two of its batch sizes.
 """
 import gc
@@ -12,7 +13,8 @@ import pytest
 
 import workloads as W
 
-from gpu_helpers import check_full, check_sampled, filled_tables, host_tables, log, plan_for, to_device, upload_tables
+from gpu_helpers import (check_full, check_index_columns, check_sampled, filled_tables, host_tables, log, plan_for,
+                         to_device, upload_tables)
 
 pytestmark = pytest.mark.gpu
 
@@ -132,7 +134,7 @@ def test_workload_full_size_sampled_weighted_and_mean(cfg):
 def test_workload5_full_size_sampled():
     """Workload 5 at full size (132.7 GB of tables, 131M lookups) with the plan bench.py uses:
     uniform tables to the tolerance on 3000 sampled bags; integer tables bit-exact on 20000
-    sampled bags; then weighted lookups with mean and sum tables alternating on the same
+    sampled bags, and on every bag in columns 0-4 (functions of the row id alone); then weighted lookups with mean and sum tables alternating on the same
     integer tables, to the tolerance on 4000 sampled bags."""
     import torch
     log("workload 5 (100 tables <= 150 GB, E128 fp32, B65536): full size, sampled bags")
@@ -152,6 +154,8 @@ def test_workload5_full_size_sampled():
     got = _lookup(c, batch, wi, stats)
     check_sampled(c, got, batch, 20000, seed=55, mode=W.VAL_INTEGER, exact=True)
     log("  integer tables: 20000 sampled bags bit-exact")
+    check_index_columns(got, batch, c.T)
+    log(f"  integer tables: every bag ({batch.B * c.T}), columns 0-4 (count, row digits, table) bit-exact")
     del got
     pooling = ["mean" if t % 2 == 0 else "sum" for t in range(c.T)]
     psw = np.random.default_rng(1005).uniform(0.5, 1.5, size=batch.indices.size).astype(np.float32)
