@@ -153,8 +153,9 @@ typedef struct {
                                and weights' allocations; else EMB_ERR_INVALID_ARGUMENT, nothing
                                launched) and reports out-of-range ids on stderr; synchronous  */
   int32_t gather_steps;     /* gather_kernel: row loads in flight per lane per step (12, 13 or
-                               16, the one whose steps the plan's chunks fill best;
-                               EMBX_GATHER_STEPS overrides it); 0 for lookup_kernel           */
+                               16: the fewest row rounds over the plan's multi-lookup chunks,
+                               ties to the larger, 12 without such chunks; EMBX_GATHER_STEPS
+                               overrides it); 0 for lookup_kernel                             */
 } emb_plan_info_t;
 
 /* Builds a plan for T tables of rows[t] x E elements of `dtype`, for batches of up to

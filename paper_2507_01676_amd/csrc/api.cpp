@@ -477,12 +477,14 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
   const double wave_chunk_override = env_chunk ? std::atof(env_chunk) : 0.0;
   // Rows in flight per step of the wave-uniform gather kernel (one build per choice): the
   // choice with the fewest row rounds -- a chunk of c expected lookups takes ceil(c / N)
-  // steps of N = ks S lookups -- over the plan's multi-lookup chunks, ties to the smaller
-  // (fewer registers); plans without such chunks keep 12.  Measured on workloads 2-5 (12 /
-  // 13 / 16): workload 4's 100-lookup chunks (two bags of 50) take 3 / 2 / 2 steps and ran
-  // 14.3 / 13.5 / 14.1 us; workload 5 (chunks of ~180 lookups, N = 2 ks) 3966 / 3949 /
-  // 3929 us; workload 3 119.3 / 119.9 / 119.1 us; workload 2, single-lookup bags only, 5.4 /
-  // 5.7 / 5.8 us.  EMBX_GATHER_STEPS = 12, 13 or 16 overrides it.
+  // steps of N = ks S lookups -- over the plan's multi-lookup chunks, ties to the larger
+  // (more rows in flight for the same rounds); plans without such chunks keep 12 (their
+  // single-lookup chunks are one step each, and larger steps make fewer of them).  Measured
+  // (12 / 13 / 16): workload 4's 100-lookup chunks (two bags of 50) take 3 / 2 / 2 steps and
+  // ran 14.36 / 14.03 / 13.92 us and, on another box, 14.08 / 13.86 / 13.75 us; workload 5
+  // (chunks of ~180 lookups, N = 2 ks) 3966 / 3949 / 3929 us; workload 3 119.3 / 119.9 /
+  // 119.1 us; workload 2, single-lookup bags only, 5.30 / 5.36 / 5.51 us.
+  // EMBX_GATHER_STEPS = 12, 13 or 16 overrides it.
   int ksteps = 12;
   if (wave_gather) {
     const char* env_steps = std::getenv("EMBX_GATHER_STEPS");
@@ -520,11 +522,12 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
             rounds += nc * std::ceil(cb * s_t / N);
           }
         }
-        if (best < 0.0 || rounds < best) {
+        if (best < 0.0 || rounds <= best) {   // candidates ascend: ties go to the larger
           best = rounds;
           ksteps = cand;
         }
       }
+      if (best == 0.0) ksteps = 12;   // no multi-lookup chunks
     }
   }
   std::vector<GatherRun> gr;                       // runs, worker-major

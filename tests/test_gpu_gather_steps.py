@@ -91,9 +91,9 @@ def test_unknown_step_count_is_refused(monkeypatch):
 
 def test_the_workloads_choices(monkeypatch):
     """The plan's choice: the fewest row rounds over its multi-lookup chunks, ties to the
-    smaller; single-lookup bags only (workload 2) keep 12."""
+    larger; single-lookup bags only (workload 2) keep 12."""
     monkeypatch.delenv("EMBX_GATHER_STEPS", raising=False)
-    want = {2: 12, 3: 16, 4: 13, 5: 16}
+    want = {2: 12, 3: 16, 4: 16, 5: 16}
     for cfg, ks in want.items():
         c = W.make_config(cfg)
         p = plan_for(c, c.batch, stats=W.history_stats(c))
