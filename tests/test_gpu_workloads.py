@@ -75,7 +75,8 @@ def test_workload_full_size_every_element(cfg):
         gc.collect()
 
 
-@pytest.mark.parametrize("cfg,dist", [(1, "fixed"), (2, "fixed"), (2, "uniform"), (4, "fixed")])
+@pytest.mark.parametrize("cfg,dist", [(1, "fixed"), (2, "fixed"), (2, "uniform"), (3, "fixed"), (3, "uniform"),
+                                      (4, "fixed"), (4, "uniform")])
 def test_workload_query_distributions(cfg, dist):
     """The workloads under the paper's other query distributions (Sec. IV-A): uniform,
     and fixed (every lookup of a table on one row, the paper's stress test for
