@@ -256,7 +256,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the lookup runs on a single MI355X "
-              "(multi-GPU sharding is a design note, not part of this build); use --gpus 1", file=sys.stderr)
+              "(multi-GPU sharding is a design note here, not implemented); use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -481,7 +481,7 @@ emb_status_t plan_create(emb_plan_t** plan_out, int32_t num_tables, const int64_
   // (more rows in flight for the same rounds); plans without such chunks keep 12 (their
   // single-lookup chunks are one step each, and larger steps make fewer of them).  Measured
   // (12 / 13 / 16): workload 4's 100-lookup chunks (two bags of 50) take 3 / 2 / 2 steps and
-  // ran 14.36 / 14.03 / 13.92 us and, on another box, 14.08 / 13.86 / 13.75 us; workload 5
+  // ran 14.36 / 14.03 / 13.92 us and, in a second session, 14.08 / 13.86 / 13.75 us; workload 5
   // (chunks of ~180 lookups, N = 2 ks) 3966 / 3949 / 3929 us; workload 3 119.3 / 119.9 /
   // 119.1 us; workload 2, single-lookup bags only, 5.30 / 5.36 / 5.51 us.
   // EMBX_GATHER_STEPS = 12, 13 or 16 overrides it.
