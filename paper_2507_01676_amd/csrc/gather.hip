@@ -746,7 +746,11 @@ __global__ void __launch_bounds__(kBlock) EMBX_OCCUPANCY gather_kernel(LookupArg
     w.walk(a, runs, q);
   }
   if (nr > n_single) {
-    WaveQueue q{runs, n_single, nr, multi_chunks, a.B, (LMEM int*)&s_ctr[1], wave, waves};
+    // the wavefronts that took a single-lookup chunk take their first multi-lookup chunk
+    // last, so that the others start on this queue at once (a permutation of [0, waves):
+    // every chunk below `waves` is still some wavefront's first)
+    const int busy = n_single > 0 ? min(single_chunks, waves) : 0;
+    WaveQueue q{runs, n_single, nr, multi_chunks, a.B, (LMEM int*)&s_ctr[1], (wave + waves - busy) % waves, waves};
     Multi<G, F16, W> w;
     w.init(a);
     w.walk(a, runs, q);
