@@ -6,7 +6,9 @@
 - a table whose statistics leave the maximum pooling unknown (0) is summed like any other,
   not treated as single-lookup bags;
 - a plan launched with nearly all of a workgroup's LDS keeps working after smaller plans
-  and the dedup probe have been created and run.
+  and the dedup probe have been created and run;
+- workers that hold both single-lookup bags and summed bags (the second queue's first
+  chunks are rotated past the wavefronts busy with single-lookup chunks) walk every bag once.
 """
 import numpy as np
 import pytest
@@ -157,4 +159,36 @@ def test_tables_beyond_4_gib_read_the_right_rows():
             a0, a1 = batch.offsets[t * c.batch + b], batch.offsets[t * c.batch + b + 1]
             rows = W.table_rows_at(t, batch.indices[a0:a1], c.E, c.dtype, seed=c.value_seeds[t], mode=W.VAL_INTEGER)
             assert np.array_equal(got[b, t], rows.astype(np.float64).sum(axis=0).astype(np.float32)), (t, b)
+    assert p.check_errors() == 0
+
+
+@pytest.mark.parametrize("B", [256, 1000, 4096])
+def test_workers_holding_both_queues_walk_every_bag(B):
+    """Three workers, every table split over all of them: each worker holds two single-lookup
+    runs and one summed run, with 4, 12 or 44 single-lookup chunks (fewer wavefronts busy with
+    them than the worker has, or all 16).  Integer tables, bit-exact, also at runtime batches
+    below the max batch."""
+    import torch
+    log(f"3 workers, max batch {B}: pooling-1, pooling-8 and pooling-1 tables on every worker")
+    c = fixed_pf_config(145, [30_000, 30_000, 500], [1, 8, 1], B=B)
+    hw = host_tables(c, W.VAL_INTEGER)
+    p = plan_for(c, B, num_workers=3).bind(upload_tables(hw))
+    per = {}
+    for ln in p.serialize().splitlines():
+        if ln.startswith("item "):
+            f = ln.split()
+            per.setdefault(int(f[1]), set()).add(int(f[2]))
+    assert sorted(per) == [0, 1, 2] and all(v == {0, 1, 2} for v in per.values())
+    runs = p.info()["gather_runs"]
+    log(f"  gather runs per queue {runs}")
+    assert runs["single"] == 6 and runs["sw"] + runs["wave"] == 3
+    for Bt in sorted({B, B // 2 + 1, 7}):
+        batch = W.gen_batch(c, Bt, B=Bt)
+        idx, off = to_device(batch)
+        out = torch.full((Bt, c.T, c.E), float("nan"), device="cuda")
+        p.lookup(idx, off, Bt, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        assert not np.isnan(got).any(), f"batch {Bt}: bags never written"
+        check_full(got, hw, batch, c.dtype, exact=True)
     assert p.check_errors() == 0
