@@ -5,15 +5,22 @@ One step = one emb_lookup over one batch of the workload (all tables, all
 samples).  Inputs (tables, indices, offsets) are resident in HBM before timing;
 R distinct batches are cycled.  Prints ONE JSON line:
 
-  value            lookups/s over the K timed steps (whole job, one GPU)
-  queries_per_s    samples/s (the paper's TPS)
+  value            lookups/s over the K timed steps (whole job, one GPU), one batch at a time
+                   on one stream.  With --streams S > 1 the steps of another timed pass are
+                   dealt round-robin to S streams (one plan per stream, each writing its own
+                   output), so that one batch's last workers overlap the next batch's first;
+                   value and ms_per_step then come from that pass, and single_stream holds
+                   the one-stream figures (a kernel trace then also holds the overlapped
+                   dispatches, whose begin-to-end times are longer than launch_us)
+  queries_per_s    samples/s (the paper's TPS), from the same pass as value
   p99_us           nearest-rank P99 of the per-batch latency (a separate pass of 1000
                    batches, 200 for workload 5, with HIP events around each launch;
                    mean_us is that pass's mean)
   cold_cache       the same latency with L2 and MALL flushed (a 512 MiB write) before
                    each batch, outside the timed region
-  launch_us        average launch duration over the K timed steps (one HIP event pair on
-                   the launch stream around the back-to-back launches)
+  launch_us        average launch duration over the K single-stream steps (one HIP event
+                   pair on the launch stream around the back-to-back launches); this pass runs
+                   last, so that a kernel trace's last K dispatches are these
   useful_hbm_frac  (lookups x row bytes) per launch_us over the 8 TB/s HBM peak: every
                    lookup's row counted, also when L2 or the MALL serves it (can exceed 1)
   roofline         compulsory bytes per launch over launch_us, against the 8 TB/s HBM peak:
@@ -29,7 +36,7 @@ R distinct batches are cycled.  Prints ONE JSON line:
                    (torch_embedding_bag) torch's CPU embedding_bag on the same sample, with
                    the threads it used, for unweighted runs
 
-  python bench.py [--config 5] [--steps 200] [--warmup 20]
+  python bench.py [--config 5] [--steps 200] [--warmup 20] [--streams 1]
 """
 from __future__ import annotations
 
@@ -253,6 +260,8 @@ def main():
                     help="slice order of the placement: 0 longest first, 1 the paper's (s desc, m asc)")
     ap.add_argument("--no-replication", action="store_true",
                     help="no batch splits (replication 1); with --order-mode 1 the paper's solver as printed")
+    ap.add_argument("--streams", type=int, default=1, choices=[1, 2, 3, 4],
+                    help="streams a second throughput pass deals its steps to (1: none, one batch at a time)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the lookup runs on a single MI355X "
@@ -359,8 +368,37 @@ def main():
                 "useful_gbps": cuse / (cmean * 1e-3) / 1e9}
         del flush
 
-    # throughput: the K timed steps back to back, synchronized on both sides; one event
-    # pair on the launch stream gives the average launch duration
+    total_lookups = sum(n_look[i % R] for i in range(K))
+    # throughput: the K steps dealt round-robin to S streams, each with its own plan (the
+    # same tables) and output, synchronized on both sides of the timed region
+    S = args.streams
+    pipe = None
+    if S > 1:
+        plans = [plan] + [embx.Plan(c.rows, c.E, c.dtype, stats, c.batch, **opts).bind(weights) for _ in range(S - 1)]
+        side = [torch.cuda.Stream() for _ in range(S)]
+        outs = [out] + [torch.empty_like(out) for _ in range(S - 1)]
+        sps, ops = [x.cuda_stream for x in side], [x.data_ptr() for x in outs]
+
+        def dealt(n):
+            for x in side:
+                x.wait_stream(stream)
+            for i in range(n):
+                ip, op = ptrs[i % R]
+                plans[i % S].lookup_ptr(ip, op, B, ops[i % S], sps[i % S], wptr[i % R])
+            for x in side:
+                stream.wait_stream(x)
+        dealt(max(args.warmup, S))
+        torch.cuda.synchronize()
+        wallp0 = time.perf_counter()
+        dealt(K)
+        torch.cuda.synchronize()
+        pipe = time.perf_counter() - wallp0
+        for x in plans[1:]:
+            assert x.check_errors() == 0
+            x.close()
+        del outs, plans
+    # one batch at a time: the K steps back to back on one stream; one event pair on the
+    # launch stream gives the average launch duration
     e_start, e_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
@@ -370,9 +408,9 @@ def main():
         plan.lookup_ptr(ip, op, B, outp, sp, wptr[i % R])
     e_stop.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    wall1 = time.perf_counter() - wall0
     launch_ms = e_start.elapsed_time(e_stop) / K
-    total_lookups = sum(n_look[i % R] for i in range(K))
+    wall = pipe if pipe is not None else wall1
     mean_ms = sum(lat_ms) / len(lat_ms)
 
     R_b = c.row_bytes
@@ -415,6 +453,9 @@ def main():
                    "table_bytes": sum(c.rows) * R_b, "pooling": args.pooling, "weighted": bool(args.weighted),
                    "queries": args.dist},
         "queries_per_s": B * K / wall,
+        "streams": S,
+        "single_stream": {"value": total_lookups / wall1, "ms_per_step": wall1 * 1e3 / K,
+                          "queries_per_s": B * K / wall1},
         "p99_us": p99(lat_ms) * 1e3,
         "mean_us": mean_ms * 1e3,
         "launch_us": launch_ms * 1e3,

@@ -49,3 +49,30 @@ def test_two_plans_on_two_streams():
             ref_a = got_a
         assert np.array_equal(got_a, ref_a), f"plan A launch {i} differs"
         check_full(outs_b[i].cpu().numpy(), hb, bb, "f16", exact=True)
+
+
+def test_two_batches_in_flight_over_the_same_tables():
+    """The throughput mode of bench.py --streams 2: consecutive batches dealt to two
+    streams, each with its own plan over the same device tables and its own outputs, so
+    that one batch's last workers overlap the next batch's first. Integer tables: every
+    output bit-exact against the oracle."""
+    import torch
+    log("two plans over one set of tables, batches dealt to two streams")
+    c = mixed_config(132, 64, "f32")
+    hw = host_tables(c, W.VAL_INTEGER)
+    wd = upload_tables(hw)
+    plans = [plan_for(c, c.batch).bind(wd) for _ in range(2)]
+    log(f"  kernel {plans[0].info()['kernel']}")
+    batches = [W.gen_batch(c, s) for s in range(4)]
+    dev = [(torch.from_numpy(b.indices).cuda(), torch.from_numpy(b.offsets).cuda()) for b in batches]
+    n = 16
+    outs = [torch.full((c.batch, c.T, c.E), float("nan"), device="cuda") for _ in range(n)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for i in range(n):
+        plans[i % 2].lookup(*dev[i % 4], c.batch, outs[i], stream=streams[i % 2])
+    torch.cuda.synchronize()
+    for i in range(n):
+        check_full(outs[i].cpu().numpy(), hw, batches[i % 4], "f32", exact=True)
+    assert all(p.check_errors() == 0 for p in plans)
