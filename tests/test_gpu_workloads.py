@@ -191,7 +191,8 @@ def test_batch_sweep_plans_match_the_oracle(cfg):
         seen.append(batch.B)
 
     pts = pareto.sweep(cfg, fractions=(1 / 16, 1 / 2), steps=5, warmup=2, n_p99=5, n_batches=2,
-                       log=lambda m: log("  " + m), verify=verify)
+                       log=lambda m: log("  " + m), verify=verify, streams=(1, 2))
     full = W.make_config(cfg).batch
     assert seen == [max(1, round(full / 16)), max(1, round(full / 2))]
-    assert len(pts) == 2 and all(p["lookups_per_s"] > 0 for p in pts)
+    assert [p["streams"] for p in pts] == [1, 2, 1, 2]
+    assert all(p["lookups_per_s"] > 0 for p in pts)
