@@ -4,7 +4,8 @@ Workloads 1-4 are checked on every output element (tables built on the host and
 uploaded); workload 5 (132.7 GB of tables) on every bag in the columns that follow from the
 indices alone (integer tables) and on sampled bags whose rows the oracle regenerates
 on the host, bit-exact on integer tables.  The batch-size sweep's plans
-are checked at two of its batch sizes.
+are checked at two of its batch sizes, and workloads 2 and 4 also with two batches in
+flight (bench.py --streams 2).
 """
 import gc
 
@@ -73,6 +74,35 @@ def test_workload_full_size_every_element(cfg):
         log(f"  {batch.B * c.T * c.E} elements checked, pooled error {err:.2e}")
         del hw, got
         gc.collect()
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_workload_two_batches_in_flight_every_element(cfg):
+    """The launch configuration of bench.py --streams 2 at full size: four batches dealt to
+    two streams, a plan each over the same integer tables, each into its own output; every
+    element of every batch bit for bit against the oracle."""
+    import torch
+    log(f"workload {cfg}: full size, two batches in flight, every element")
+    c = W.make_config(cfg)
+    stats = W.history_stats(c)
+    hw = host_tables(c, W.VAL_INTEGER)
+    wd = upload_tables(hw)
+    plans = [plan_for(c, c.batch, stats=stats).bind(wd) for _ in range(2)]
+    batches = [W.gen_batch(c, i) for i in range(4)]
+    dev = [to_device(b) for b in batches]
+    outs = [torch.full((c.batch, c.T, c.E), float("nan"), device="cuda") for _ in range(4)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for i in range(4):
+        plans[i % 2].lookup(*dev[i], c.batch, outs[i], stream=streams[i % 2])
+    torch.cuda.synchronize()
+    assert all(p.check_errors() == 0 for p in plans)
+    for i in range(4):
+        check_full(outs[i].cpu().numpy(), hw, batches[i], c.dtype, exact=True)
+    log(f"  {4 * c.batch * c.T * c.E} elements checked")
+    del plans, wd, outs, dev
+    _free()
 
 
 @pytest.mark.parametrize("cfg,dist", [(1, "fixed"), (2, "fixed"), (2, "uniform"), (3, "fixed"), (3, "uniform"),
