@@ -260,6 +260,10 @@ def main():
                     help="slice order of the placement: 0 longest first, 1 the paper's (s desc, m asc)")
     ap.add_argument("--no-replication", action="store_true",
                     help="no batch splits (replication 1); with --order-mode 1 the paper's solver as printed")
+    ap.add_argument("--table-costs", type=int, default=0,
+                    help="rounds of per-table lookup-cost calibration before timing: traced launches of "
+                         "the plan over the resident batches, a fit of each table's cost of a lookup "
+                         "served from memory, and a re-plan with those costs (0: the vector's G1 for all)")
     ap.add_argument("--streams", type=int, default=1, choices=[1, 2, 3, 4],
                     help="streams a second throughput pass deals its steps to (1: none, one batch at a time)")
     args = ap.parse_args()
@@ -318,6 +322,34 @@ def main():
     info = plan.info()
     torch.cuda.synchronize()
     log(f"plan: {info['n_strategy']} items={info['num_items']} lif={info['lif_milli']} ({plan_ms:.1f} ms)")
+
+    table_costs = None
+    if args.table_costs > 0:
+        # closed loop per table: the plan's traced launches over the resident batches, one
+        # fit of every table's cost per lookup on all of them, a re-plan with those costs
+        from paper_2507_01676_amd import calibrate as CAL
+        g0 = (opts.get("beta") or embx.default_beta(c.row_bytes))[0]
+        for rnd in range(args.table_costs):
+            ps, ns, lams = [], [], []
+            for i in range(R):
+                # the batch before it first, as in the timed loop: its rows are not the
+                # ones left in the caches
+                plan.lookup(d_idx[(i - 1) % R], d_off[(i - 1) % R], c.batch, out)
+                tr = CAL.traced_launch(plan, d_idx[i], d_off[i], c.batch, out, warm=0)
+                a, n, lm = CAL.worker_gather_samples(plan, tr, c.batch, batches[i].offsets, c.T)
+                ps.append(a)
+                ns.append(n)
+                lams.append(lm)
+            table_costs = CAL.fit_table_lookup_costs(np.concatenate(ps), np.concatenate(ns), np.concatenate(lams), g0)
+            opts["gather_lookup_ps"] = table_costs
+            plan.close()
+            tp = time.time()
+            plan = embx.Plan(c.rows, c.E, c.dtype, stats, c.batch, **opts).bind(weights)
+            plan_ms = (time.time() - tp) * 1e3
+            info = plan.info()
+            log(f"table costs round {rnd + 1}: " + " ".join(f"{x / 1e3:.1f}" for x in table_costs)
+                + f" ns; plan items={info['num_items']} lif={info['lif_milli']}")
+        torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
@@ -480,7 +512,9 @@ def main():
                  "gather_steps": info["gather_steps"],
                  "workers": info["num_workers"], "lds_bytes": info["lds_bytes"], "build_ms": plan_ms,
                  "options": {k: opts[k] for k in ("lif_milli", "sym_max", "order_mode", "no_replication")
-                             if k in opts}},
+                             if k in opts},
+                 "table_lookup_ps": None if table_costs is None else [round(x, 1) for x in table_costs],
+                 "table_cost_rounds": args.table_costs},
         "kernel_source_hash": src_hash,
         "cpu_baseline": cpu,
     }

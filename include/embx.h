@@ -128,6 +128,11 @@ typedef struct {
   int32_t no_replication;   /* 1: no batch splits of any item (replication fixed to 1, as the
                                paper's solver does, Sec. III-B); with order_mode 1 the plan is
                                Sec. III-B steps 1-4 as printed; 0: splits allowed (default)       */
+  const double* gather_lookup_ps; /* host, T entries or NULL: table t's cost of one lookup served
+                               from memory in picoseconds (beta's G1 for that table: its gathers,
+                               HOT misses and DEDUP's distinct rows), fitted on the device for the
+                               table's size and query distribution (Sec. III-A fits the model per
+                               configuration); 0 -> beta's G1; negative or non-finite: invalid   */
 } emb_plan_options_t;
 
 typedef struct emb_plan emb_plan_t;   /* opaque */

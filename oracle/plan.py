@@ -63,6 +63,11 @@ budget for rows):
       until LIF is within the threshold; if no r gets there, the r (0
       included) with the smallest maximum load.
   P8  canonical text: one line per slice in worker order then placement order.
+
+A table may carry its own G1, the cost of one lookup served from memory (its
+gathers, HOT misses and DEDUP's distinct rows), fitted on the device for that
+table's size and query distribution: Sec. III-A fits the model's coefficients per
+configuration.  Every other coefficient is shared.
 """
 from __future__ import annotations
 
@@ -141,6 +146,7 @@ class Options:
     force: Optional[Sequence[int]] = None
     sym_max: int = 0                  # > 0: GATHER items split symmetrically while at most this many; < 0: never
     no_replication: bool = False      # True: no batch splits (P4 off), replication factor 1
+    gather_lookup_ps: Optional[Sequence[float]] = None   # per table G1 (0: beta's), or None
 
 
 @dataclass
@@ -233,8 +239,9 @@ def cost_stream(b, m, R, lam, c):
 
 
 class _Table:
-    def __init__(self, t, m, st: Stat, R, L, B, force):
+    def __init__(self, t, m, st: Stat, R, L, B, force, g1=None):
         self.t, self.m, self.R = t, m, R
+        self.g1 = float(g1) if g1 else None   # this table's G1, None: beta's
         self.s = float(st.mean_pooling)
         self.Lam = float(B) * self.s
         self.C = min(st.n_hot, L // R, MAX_HOT_SLOTS)
@@ -275,6 +282,8 @@ class _Table:
 
     def cost(self, b, strat, k):
         """(cost, fixed cost, hot rows staged) of one slice at split k."""
+        if self.g1 is not None:
+            b = list(b[:G1]) + [self.g1] + list(b[G1 + 1:])
         lam = self.Lam / float(k)
         if strat == LDS:
             return cost_lds(b, self.m, self.R, lam) + (0,)
@@ -349,21 +358,25 @@ def _validate(rows, E, dtype, stats, B, K, opts: Options):
     # nothing, and least-loaded placement would then pile such slices onto one worker
     if len(beta) != NBETA or not all(math.isfinite(x) and x >= 0.0 for x in beta):
         raise PlanError("beta")
+    g1 = list(opts.gather_lookup_ps) if opts.gather_lookup_ps is not None else None
+    if g1 is not None and (len(g1) != T or not all(math.isfinite(x) and x >= 0.0 for x in g1)):
+        raise PlanError("gather_lookup_ps")
     force = list(opts.force) if opts.force is not None else [AUTO] * T
     if len(force) != T or any(f not in (AUTO, LDS, HOT, DEDUP, GATHER, STREAM) for f in force):
         raise PlanError("force_strategy")
-    return T, R, L, beta, force
+    return T, R, L, beta, force, g1
 
 
 def plan_reference(rows: Sequence[int], E: int, dtype: str, stats: Sequence[Stat], B: int, K: int,
                    opts: Optional[Options] = None) -> Plan:
     opts = opts or Options()
-    T, R, L, b, force = _validate(rows, E, dtype, stats, B, K, opts)
+    T, R, L, b, force, g1 = _validate(rows, E, dtype, stats, B, K, opts)
     cm = opts.chunk_max_bytes if opts.chunk_max_bytes > 0 else L
     crow = min(cm, L) // R
     if crow < 1:
         raise PlanError("chunk_max_bytes below one row")
-    tabs = [_Table(t, int(rows[t]), stats[t], R, L, B, force[t]) for t in range(T)]
+    tabs = [_Table(t, int(rows[t]), stats[t], R, L, B, force[t], g1[t] if g1 is not None else None)
+            for t in range(T)]
     for tb in tabs:
         if tb.force == HOT and tb.C < 1:
             raise PlanError("HOT forced on a table without hot rows")

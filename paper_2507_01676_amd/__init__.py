@@ -62,7 +62,8 @@ class _Opts(ctypes.Structure):
                 ("order_mode", ctypes.c_int32), ("chunk_max_bytes", ctypes.c_int64),
                 ("beta", ctypes.POINTER(ctypes.c_double)), ("force_strategy", ctypes.POINTER(ctypes.c_int32)),
                 ("num_workers", ctypes.c_int32), ("sym_max_gather", ctypes.c_int32),
-                ("pooling", ctypes.POINTER(ctypes.c_int32)), ("no_replication", ctypes.c_int32)]
+                ("pooling", ctypes.POINTER(ctypes.c_int32)), ("no_replication", ctypes.c_int32),
+                ("gather_lookup_ps", ctypes.POINTER(ctypes.c_double))]
 
 
 class _Info(ctypes.Structure):
@@ -185,6 +186,13 @@ class _Marshal:
                 raise ValueError(f"pooling needs one reduction per table ({T}), got {pc.size}")
             self.keep.append(pc)
             o.pooling = pc.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        g1 = opts.get("gather_lookup_ps")
+        if g1 is not None:
+            g = np.ascontiguousarray(np.asarray(g1, dtype=np.float64))
+            if g.size != T:
+                raise ValueError(f"gather_lookup_ps needs one cost per table ({T}), got {g.size}")
+            self.keep.append(g)
+            o.gather_lookup_ps = g.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
         self.opts = o
 
 

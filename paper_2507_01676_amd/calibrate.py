@@ -223,6 +223,49 @@ def samples_of(plan, tr: np.ndarray, batch: int, host_offsets: np.ndarray, stats
     return s
 
 
+def worker_gather_samples(plan, tr: np.ndarray, batch: int, host_offsets: np.ndarray, T: int):
+    """From one traced launch: for each worker with gather slices, its gather-phase time
+    (ps), its number of gather slices and its lookups from each table at this batch
+    (rows of a K' x T matrix)."""
+    info = plan.info()
+    K = info["num_workers"]
+    per = 2 + 1024 // 64
+    tw = tr[:K * per].reshape(K, per)
+    lam = np.zeros((K, T), dtype=np.float64)
+    n = np.zeros(K, dtype=np.int64)
+    for it in _plan_items(plan.serialize()):
+        if it["strat"] != GATHER:
+            continue
+        bs, be = it["j"] * batch // it["k"], (it["j"] + 1) * batch // it["k"]
+        t = it["t"]
+        lam[it["wg"], t] += float(host_offsets[t * batch + be] - host_offsets[t * batch + bs])
+        n[it["wg"]] += 1
+    gat = (tw[:, 2:].max(axis=1) - tw[:, 1]).astype(np.float64) * TICK_PS
+    keep = n > 0
+    return gat[keep], n[keep], lam[keep]
+
+
+def fit_table_lookup_costs(ps: np.ndarray, n_slices: np.ndarray, lam: np.ndarray, g0: float) -> List[float]:
+    """Each table's cost of one lookup served from memory (ps), from workers' gather
+    phases: time = c + G0 x slices + sum over tables of G1_t x lookups_t, with one shared
+    c (the latency chain every worker pays once: launch skew, run header, first loads)
+    and G0 from the cost vector, fitted with non-negative coefficients and residuals
+    relative to each worker's predicted time.  Eq. (2) prices a lookup alike in every
+    table; on this device one that misses the caches costs a CU several times one that
+    hits, and Sec. III-A fits the coefficients per configuration.  A table with no
+    lookups in the samples gets 0 (the planner then uses the vector's G1)."""
+    ps = np.asarray(ps, dtype=np.float64)
+    lam = np.asarray(lam, dtype=np.float64)
+    used = np.flatnonzero(lam.sum(axis=0) > 0)
+    A = np.column_stack([np.ones(len(ps)), lam[:, used]])
+    y = ps - g0 * np.asarray(n_slices, dtype=np.float64)
+    x = _lstsq(A, y, np.zeros(len(y)))
+    out = [0.0] * lam.shape[1]
+    for i, t in enumerate(used):
+        out[int(t)] = float(x[1 + i])
+    return out
+
+
 def measure(plan, indices, offsets, batch: int, out, host_offsets: np.ndarray, stats, R: int,
             warm: int = 3) -> Samples:
     """Runs one traced launch of ``plan`` and turns its timers into samples."""

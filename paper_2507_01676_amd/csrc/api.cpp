@@ -110,6 +110,7 @@ emb_status_t to_plan_in(int32_t T, const int64_t* rows, int32_t E, emb_dtype_t d
       for (int i = 0; i < B_COUNT; ++i) in->beta[i] = opts->beta[i];
     }
     if (opts->force_strategy) in->force.assign(opts->force_strategy, opts->force_strategy + T);
+    if (opts->gather_lookup_ps) in->g1.assign(opts->gather_lookup_ps, opts->gather_lookup_ps + T);
   }
   // EMBX_FORCE_STRATEGY (debugging): every table to one strategy, over the options
   if (const char* fs = std::getenv("EMBX_FORCE_STRATEGY")) {

@@ -25,6 +25,9 @@
 //      first), r = 1, 2, ... until LIF is within the threshold, else the r with the
 //      smallest maximum load;
 //   P8 canonical text.
+// A table may carry its own cost of a lookup served from memory (G1: gathers, HOT
+// misses, DEDUP's distinct rows), fitted on the device for that table's size and query
+// distribution; the other coefficients are shared.
 // All costs are floored to integer picoseconds as soon as they are computed and
 // every decision compares integers.
 #include "planner.hpp"
@@ -86,6 +89,7 @@ struct Tab {
   int32_t t;
   int64_t m;
   double s, Lam, u;
+  std::array<double, B_COUNT> b;   // the cost vector with this table's G1
   int32_t C;             // hot rows that may be staged: min(listed, L / R, kMaxHotSlots)
   std::vector<std::pair<int32_t, double>> hc;   // HOT candidates (C, h(C)), C ascending
   bool fits;
@@ -124,7 +128,7 @@ struct Planner {
     CF out{0, 0};
     *C = 0;
     for (const auto& ch : tb.hc) {
-      CF c = cost_hot(b, ch.first, R, ch.second, lam);
+      CF c = cost_hot(tb.b, ch.first, R, ch.second, lam);
       if (*C == 0 || c.cost < out.cost) {
         out = c;
         *C = ch.first;
@@ -137,11 +141,11 @@ struct Planner {
     const double lam = tb.Lam / static_cast<double>(k);
     *C = 0;
     switch (strat) {
-      case S_LDS: return cost_lds(b, tb.m, R, lam);
+      case S_LDS: return cost_lds(tb.b, tb.m, R, lam);
       case S_HOT: return hot_best(tb, lam, C);
-      case S_DEDUP: return cost_dedup(b, tb.u, lam);
-      case S_STREAM: return cost_stream(b, tb.m, R, lam, tb.sc);
-      default: return cost_gather(b, lam);
+      case S_DEDUP: return cost_dedup(tb.b, tb.u, lam);
+      case S_STREAM: return cost_stream(tb.b, tb.m, R, lam, tb.sc);
+      default: return cost_gather(tb.b, lam);
     }
   }
 
@@ -311,6 +315,9 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
   P.b = in.has_beta ? in.beta : default_beta(static_cast<int32_t>(P.R));
   for (double x : P.b)
     if (!std::isfinite(x) || x < 0.0) return fail(1, "beta");   // negative times would pile slices on one worker
+  if (!in.g1.empty() && static_cast<int32_t>(in.g1.size()) != T) return fail(1, "gather_lookup_ps");
+  for (double x : in.g1)
+    if (!std::isfinite(x) || x < 0.0) return fail(1, "gather_lookup_ps");
   if (!in.force.empty() && static_cast<int32_t>(in.force.size()) != T) return fail(1, "force_strategy");
   for (int32_t f : in.force)
     if (f < S_AUTO || f > S_STREAM) return fail(1, "force_strategy");
@@ -325,6 +332,8 @@ int build_plan(const PlanIn& in, PlanOut* out, std::string* err) {
     const TableIn& ti = in.tables[t];
     Tab tb;
     tb.t = t;
+    tb.b = P.b;
+    if (!in.g1.empty() && in.g1[t] > 0.0) tb.b[B_G1] = in.g1[t];
     tb.m = ti.rows;
     tb.s = ti.mean_pooling;
     tb.Lam = static_cast<double>(in.B) * tb.s;

@@ -42,6 +42,7 @@ struct PlanIn {
   std::vector<int32_t> force;   // empty = all AUTO
   int32_t sym_max = 0;          // > 0: GATHER items split symmetrically while at most this many; < 0: never
   bool no_replication = false;  // true: no batch splits (P4 off), the paper's replication factor of 1
+  std::vector<double> g1;       // per table: ps per lookup served from memory (0: beta's G1); empty = beta's
 };
 constexpr double kSymShareMin = 64.0;   // GATHER tables split over all workers when each slice would hold
                                         // at least this many expected lookups

@@ -170,3 +170,25 @@ def test_committed_samples_read_back_as_written():
     r = CAL.read_samples_csv(os.path.join(here, "golden", "calibration_samples.csv"))
     assert len(r.workers) == 250 and len(r.slices) == 1000
     assert {x.strat for x in r.slices} == {CAL.LDS, CAL.HOT, CAL.DEDUP}
+
+
+def test_table_lookup_costs_recovered_from_noiseless_workers():
+    """Workers' gather phases made from a known shared latency c, G0 per slice and a cost
+    per lookup for each table (one table unused): the fit returns each used table's cost
+    and 0 for the unused one."""
+    from paper_2507_01676_amd.calibrate import fit_table_lookup_costs
+    g = np.random.default_rng(7)
+    T, K = 6, 200
+    g1 = np.array([5200.0, 6400.0, 10800.0, 0.0, 7300.0, 25000.0])
+    lam = np.zeros((K, T))
+    n = np.zeros(K, dtype=np.int64)
+    for w in range(K):
+        for t in g.choice([0, 1, 2, 4, 5], size=int(g.integers(1, 3)), replace=False):
+            lam[w, t] += float(g.integers(50, 2000))
+            n[w] += 1
+    c, g0 = 2.5e6, 480_000.0
+    ps = c + g0 * n + lam @ g1
+    got = fit_table_lookup_costs(ps, n, lam, g0)
+    assert got[3] == 0.0
+    for t in (0, 1, 2, 4, 5):
+        assert abs(got[t] - g1[t]) <= 1e-6 * g1[t], (t, got[t])

@@ -192,3 +192,25 @@ def test_workers_holding_both_queues_walk_every_bag(B):
         assert not np.isnan(got).any(), f"batch {Bt}: bags never written"
         check_full(got, hw, batch, c.dtype, exact=True)
     assert p.check_errors() == 0
+
+
+def test_plan_with_per_table_lookup_costs():
+    """A plan made with a cost per lookup for each table (gather_lookup_ps: two tables
+    priced high, one left to the vector's G1) places them differently and still matches the
+    oracle bit for bit on integer tables."""
+    import torch
+    log("per-table lookup costs: 12,000 / 3,000 / 0 (vector's) / 25,000 ps")
+    c = fixed_pf_config(146, [200_000, 5_000, 60_000, 300_000], [8, 1, 3, 20], B=2048)
+    hw = host_tables(c, W.VAL_INTEGER)
+    wd = upload_tables(hw)
+    base = plan_for(c, c.batch).bind(wd)
+    p = plan_for(c, c.batch, gather_lookup_ps=[12_000.0, 3_000.0, 0.0, 25_000.0]).bind(wd)
+    assert p.serialize() != base.serialize()
+    batch = W.gen_batch(c, 0)
+    idx, off = to_device(batch)
+    for plan in (p, base):
+        out = torch.full((c.batch, c.T, c.E), float("nan"), device="cuda")
+        plan.lookup(idx, off, c.batch, out)
+        torch.cuda.synchronize()
+        check_full(out.cpu().numpy(), hw, batch, c.dtype, exact=True)
+        assert plan.check_errors() == 0

@@ -578,3 +578,33 @@ def test_hot_stages_the_cheapest_hot_set_worked_by_hand(case):
     freq, SH, C, cost = HOT_WORKED[case]
     p = OPL.plan_reference(*_hot_worked(freq, SH))
     assert [(sl.strat, sl.C, sl.cost) for sl in p.slices] == [(OPL.HOT, C, cost)]
+
+
+def test_per_table_lookup_cost_worked_by_hand():
+    """Two GATHER tables alike but for their fitted cost of a lookup served from memory:
+    table 0 keeps beta's G1 (6,370 ps; given as 0), table 1 costs 4x (25,480 ps).
+    E 64 fp32 (R 256), 1,000,000 rows each (no LDS, chunking needs 1,954 > K chunks, no
+    hot rows, u = 1, STREAM past 64 chunks), B 64, s 2 (Lam 128), K 4, so k <= 4 and no
+    symmetric split (128 / 4 = 32 < 64 lookups per slice).  By hand, G0 = 480,000:
+      unsplit: t0 480,000 + 6,370 x 128 = 1,295,360;  t1 480,000 + 25,480 x 128 = 3,741,440
+      tau = ceil(5,036,800 / 4) = 1,259,200, above 2 x G0 = 960,000, so k is the smallest
+      split whose slice costs at most tau:
+      t0: k = 2 gives 480,000 + 6,370 x 64 = 887,680 <= tau            -> k = 2
+      t1: k = 2: 2,110,720; k = 3: 1,567,146; k = 4: 1,295,360, all > tau -> k = 4
+      LPT: t1's four slices on workers 0-3, then t0's two on workers 0 and 1:
+      max 1,295,360 + 887,680 = 2,183,040, sum 6,956,800, LIF floor(4000 x 2,183,040 /
+      6,956,800) = 1,255.
+    With one shared G1 both tables are split alike: tau = ceil(2,590,720 / 4) = 647,680,
+    the bound max(tau, 2 x G0) = 960,000, and k = 2 (887,680) for each."""
+    stats = [OPL.Stat(2.0, 2, [], 1.0)] * 2
+    p = OPL.plan_reference([1_000_000] * 2, 64, "f32", stats, 64, 4, OPL.Options(gather_lookup_ps=[0.0, 25480.0]))
+    ks = {(s.t, s.k, s.cost) for s in p.slices}
+    assert ks == {(0, 2, 887_680), (1, 4, 1_295_360)}
+    assert all(s.strat == OPL.GATHER for s in p.slices)
+    assert sorted((s.wg, s.t) for s in p.slices) == [(0, 0), (0, 1), (1, 0), (1, 1), (2, 1), (3, 1)]
+    assert (p.max_ps, p.sum_ps, p.lif_milli) == (2_183_040, 6_956_800, 1255)
+    # 0 stands for beta's G1
+    q = OPL.plan_reference([1_000_000] * 2, 64, "f32", stats, 64, 4, OPL.Options(gather_lookup_ps=[6370.0, 25480.0]))
+    assert q.text() == p.text()
+    shared = OPL.plan_reference([1_000_000] * 2, 64, "f32", stats, 64, 4, OPL.Options())
+    assert {(s.t, s.k, s.cost) for s in shared.slices} == {(0, 2, 887_680), (1, 2, 887_680)}

@@ -55,7 +55,8 @@ def _cpp(rows, E, dtype, stats, B, K, opts: OPL.Options):
            for s in stats]
     return embx.plan_text(rows, E, dtype, cst, B, K, lds_budget=opts.lds_budget, lif_milli=opts.lif_milli,
                           chunk_max_bytes=opts.chunk_max_bytes, order_mode=opts.order_mode, beta=opts.beta,
-                          force=opts.force, sym_max=opts.sym_max, no_replication=opts.no_replication)
+                          force=opts.force, sym_max=opts.sym_max, no_replication=opts.no_replication,
+                          gather_lookup_ps=opts.gather_lookup_ps)
 
 
 def _both(rows, E, dtype, stats, B, K, opts: OPL.Options):
@@ -71,11 +72,13 @@ def test_cpp_planner_equals_oracle_random(seed):
 
 
 @settings(max_examples=80, deadline=None, suppress_health_check=[HealthCheck.too_slow])
-@given(st.integers(0, 10 ** 7), st.sampled_from([None, "skewbeta", "force"]))
+@given(st.integers(0, 10 ** 7), st.sampled_from([None, "skewbeta", "force", "tableg1"]))
 def test_cpp_planner_equals_oracle_hypothesis(seed, variant):
     rows, E, dtype, stats, B, K, opts = _random_instance(seed)
     g = np.random.default_rng(seed)
-    if variant == "skewbeta":
+    if variant == "tableg1":   # per-table G1, some left to beta's (0)
+        opts.gather_lookup_ps = [float(x) * float(g.integers(0, 2)) for x in g.uniform(1e3, 3e4, size=len(rows))]
+    elif variant == "skewbeta":
         opts.beta = [float(x) for x in g.uniform(0.0, 5e4, size=OPL.NBETA)]
         opts.chunk_max_bytes = int(g.choice([0, 4096, 32768]))
     elif variant == "force":
@@ -93,6 +96,29 @@ def test_cpp_planner_equals_oracle_hypothesis(seed, variant):
         return
     got, _ = _both(rows, E, dtype, stats, B, K, opts)
     assert got == want
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_cpp_planner_equals_oracle_with_per_table_lookup_costs(seed):
+    rows, E, dtype, stats, B, K, opts = _random_instance(seed)
+    g = np.random.default_rng(1000 + seed)
+    opts.gather_lookup_ps = [float(x) for x in g.choice([0.0, 3000.0, 6370.0, 11000.0, 25000.0], size=len(rows))]
+    got, want = _both(rows, E, dtype, stats, B, K, opts)
+    assert got == want
+
+
+def test_per_table_lookup_costs_are_validated():
+    embx = _lib()
+    st1 = [dict(mean_pooling=2.0, max_pooling=2, hot_rows=[], hot_freq=[], unique_frac=1.0)] * 2
+    for bad in ([1.0], [1.0, -1.0], [1.0, float("nan")], [float("inf"), 1.0]):
+        with pytest.raises(OPL.PlanError):
+            OPL.plan_reference([100, 100], 64, "f32", [OPL.Stat(2.0, 2, [], 1.0)] * 2, 64, 4,
+                               OPL.Options(gather_lookup_ps=bad))
+        if len(bad) == 2:
+            with pytest.raises(embx.EmbxError):
+                embx.plan_text([100, 100], 64, "f32", st1, 64, 4, gather_lookup_ps=bad)
+    with pytest.raises(ValueError):
+        embx.plan_text([100, 100], 64, "f32", st1, 64, 4, gather_lookup_ps=[1.0])
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
