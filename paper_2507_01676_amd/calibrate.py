@@ -257,6 +257,8 @@ def fit_table_lookup_costs(ps: np.ndarray, n_slices: np.ndarray, lam: np.ndarray
     ps = np.asarray(ps, dtype=np.float64)
     lam = np.asarray(lam, dtype=np.float64)
     used = np.flatnonzero(lam.sum(axis=0) > 0)
+    if used.size == 0 or len(ps) <= used.size:   # nothing to fit, or fewer workers than unknowns
+        return [0.0] * lam.shape[1]
     A = np.column_stack([np.ones(len(ps)), lam[:, used]])
     y = ps - g0 * np.asarray(n_slices, dtype=np.float64)
     x = _lstsq(A, y, np.zeros(len(y)))

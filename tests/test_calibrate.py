@@ -192,3 +192,12 @@ def test_table_lookup_costs_recovered_from_noiseless_workers():
     assert got[3] == 0.0
     for t in (0, 1, 2, 4, 5):
         assert abs(got[t] - g1[t]) <= 1e-6 * g1[t], (t, got[t])
+
+
+def test_table_lookup_costs_without_enough_workers_fall_back():
+    """No gather lookups, or fewer workers than unknowns: every table keeps the vector's G1
+    (0), rather than an underdetermined fit."""
+    from paper_2507_01676_amd.calibrate import fit_table_lookup_costs
+    assert fit_table_lookup_costs(np.zeros(0), np.zeros(0), np.zeros((0, 3)), 480_000.0) == [0.0] * 3
+    lam = np.array([[100.0, 0.0, 50.0]])
+    assert fit_table_lookup_costs(np.array([2e6]), np.array([2]), lam, 480_000.0) == [0.0] * 3
