@@ -43,3 +43,11 @@ def test_traffic_only_for_the_matching_source():
         assert bench.load_traffic(w, "0" * 16) is None
         assert d["hbm_bytes_per_launch"] == pytest.approx(d["hbm_read_bytes_per_launch"] + d["hbm_write_bytes_per_launch"])
     assert bench.load_traffic("no-such-workload", bench.kernel_source_hash()) is None
+
+
+@pytest.mark.parametrize("args", [["--streams", "5"], ["--streams", "0"], ["--table-costs", "x"]])
+def test_bad_throughput_options_are_refused_before_the_gpu(args):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2 and r.stdout == ""
+    assert "--streams" in r.stderr or "--table-costs" in r.stderr
