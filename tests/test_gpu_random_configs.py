@@ -1,7 +1,8 @@
 """Seeded random configurations against the oracle, bit-exact on integer tables: table
 counts, row counts (1 .. 300k), E and dtype (every row width both kernels take), pooling
 factors (empty bags, single-lookup tables, long bags), index distributions, mean or sum per
-table, weights, and a runtime batch below the max batch -- each planned automatically."""
+table, weights, and a runtime batch below the max batch -- each planned automatically, and
+the same configurations again with every table forced to each staged flow."""
 import numpy as np
 import pytest
 
@@ -66,4 +67,29 @@ def test_random_configuration_matches_the_oracle(seed):
         else:
             diff = np.argwhere(got != ref)
             assert diff.size == 0, f"batch {B}: {diff.shape[0]} elements differ, first {diff[:3].tolist()}"
+        assert p.check_errors() == bad
+
+
+@pytest.mark.parametrize("strat", ["lds", "hot", "dedup", "stream"])
+@pytest.mark.parametrize("seed", range(20))
+def test_random_configuration_with_a_forced_staged_strategy(seed, strat):
+    """The same random configurations with every table forced to one staged flow (the
+    planner would pick GATHER): row chunks, hot-row caches, tile dedup and chunked scans
+    on odd shapes, bit-exact on integer tables at the max batch and a third of it."""
+    import torch
+    code = {"lds": 0, "hot": 1, "dedup": 2, "stream": 4}[strat]
+    c, _ = random_config(seed)
+    log(f"seed {seed}, all {strat}: T {c.T}, E {c.E} {c.dtype}, max batch {c.batch}, rows {c.rows}")
+    hw = host_tables(c, W.VAL_INTEGER)
+    p = plan_for(c, c.batch, force=[code] * c.T).bind(upload_tables(hw))
+    for B in sorted({c.batch, max(1, c.batch // 3)}):
+        batch = W.gen_batch(c, B, B=B)
+        idx, off = to_device(batch)
+        out = torch.full((B, c.T, c.E), float("nan"), device="cuda")
+        p.lookup(idx, off, B, out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        ref, _, bad = OP.pool_reference(hw, batch.indices, batch.offsets, B)
+        diff = np.argwhere(got != ref)
+        assert diff.size == 0, f"batch {B}: {diff.shape[0]} elements differ, first {diff[:3].tolist()}"
         assert p.check_errors() == bad
